@@ -1,0 +1,369 @@
+"""Pins of the CPU oracle: checks against what the paper and the mathematics fix.
+
+Each pin takes the oracle module (so the mutation tests can hand it a copy with
+one planted mistake) and raises AssertionError when the oracle disagrees.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# ------------------------------------------------------------- attention --
+def pin_attention_worked(O):
+    """Hand-worked single-query cases (tests/golden/attention_worked.json, sec. 2.1)."""
+    for c in _load("attention_worked.json")["cases"]:
+        q = np.array(c["q"], float)
+        K = np.array(c["K"], float)
+        V = np.array(c["V"], float)
+        scale = 1.0 / math.sqrt(len(q)) if c["scale"] is None else c["scale"]
+        out = O.attend(q, K, V, scale)
+        assert np.allclose(out, c["out"], rtol=0, atol=1e-12), (c["name"], out, c["out"])
+
+
+def pin_attention_closed_forms(O):
+    """Closed forms of softmax attention, on random inputs."""
+    rng = np.random.default_rng(11)
+    for n, D in ((1, 8), (2, 4), (17, 64), (300, 128)):
+        q = rng.standard_normal(D)
+        K = rng.standard_normal((n, D))
+        V = rng.standard_normal((n, D))
+        s = 1.0 / math.sqrt(D)
+        # one token: the output is its value
+        assert np.allclose(O.attend(q, K[:1], V[:1], s), V[0], atol=1e-14)
+        # identical keys: uniform weights, the output is the mean value
+        Krep = np.repeat(K[:1], n, axis=0)
+        assert np.allclose(O.attend(q, Krep, V, s), V.mean(axis=0), atol=1e-12)
+        # zero query: uniform weights
+        assert np.allclose(O.attend(np.zeros(D), K, V, s), V.mean(axis=0), atol=1e-12)
+        # identical values: the output is that value
+        Vrep = np.repeat(V[:1], n, axis=0)
+        assert np.allclose(O.attend(q, K, Vrep, s), V[0], atol=1e-12)
+        # two tokens: o = v0 + sigmoid(s1 - s0) (v1 - v0)
+        if n >= 2:
+            d = s * (K[1] @ q - K[0] @ q)
+            want = V[0] + (V[1] - V[0]) / (1.0 + math.exp(-d))
+            assert np.allclose(O.attend(q, K[:2], V[:2], s), want, atol=1e-12)
+
+
+def pin_attention_sdpa(O):
+    """The library routine: torch's scaled_dot_product_attention on the CPU in float64."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(5)
+    for n, D, scale in ((1, 64, None), (5, 64, None), (129, 128, None), (40, 32, 0.3)):
+        q = rng.standard_normal(D)
+        K = rng.standard_normal((n, D))
+        V = rng.standard_normal((n, D))
+        s = 1.0 / math.sqrt(D) if scale is None else scale
+        ref = F.scaled_dot_product_attention(
+            torch.tensor(q)[None, None, None], torch.tensor(K)[None, None],
+            torch.tensor(V)[None, None], scale=scale).numpy()[0, 0, 0]
+        assert np.allclose(O.attend(q, K, V, s), ref, atol=1e-12), (n, D)
+
+
+def pin_attention_permutation(O):
+    """Attention is a set function of the (key, value) pairs."""
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal(16)
+    K = rng.standard_normal((9, 16))
+    V = rng.standard_normal((9, 16))
+    p = rng.permutation(9)
+    assert np.allclose(O.attend(q, K, V, 0.25), O.attend(q, K[p], V[p], 0.25), atol=1e-13)
+
+
+# ----------------------------------------------------- the padded batch --
+def _code(qid, t):
+    return float(1000 * qid + t + 1)
+
+
+def _decode_cell(x):
+    if math.isinf(x):
+        return "."
+    c = int(x) - 1
+    return f"q{c // 1000}.{c % 1000}"
+
+
+def _src(qid, n):
+    """fp32 bits [1 layer][1 head][n][1 dim] whose values name (qid, t)."""
+    vals = np.array([_code(qid, t) for t in range(n)], np.float32).reshape(1, 1, n, 1)
+    return vals.view(np.uint32)
+
+
+def pin_insertion_replay(O):
+    """Replay of the sec. 4.1 / sec. 4.2 insertion story against hand-derived states
+    (tests/golden/insertion_replay.json): lengths, cell contents, mask."""
+    g = _load("insertion_replay.json")
+    B = g["batch"]
+    pb = O.PaddedBatch(1, B, 1, 1, 1, O.F32)
+    slot_qid = [None] * B
+    for op in g["ops"]:
+        if op["op"] == "embed":
+            srcs = [_src(q, n) for q, n in zip(op["qids"], op["lens"])]
+            pb.embed(op["slots"], op["lens"], srcs, srcs)
+            for s, q in zip(op["slots"], op["qids"]):
+                slot_qid[s] = q
+        elif op["op"] == "evict":
+            pb.evict(op["slots"], release=True)
+            for s in op["slots"]:
+                slot_qid[s] = None
+        elif op["op"] == "decode":
+            kn = np.full((B, 1, 1), O.NEG_INF_BITS[O.F32], np.uint32)
+            for b in range(B):
+                if slot_qid[b] is not None:
+                    kn[b, 0, 0] = np.float32(_code(slot_qid[b], pb.lens[b])).view(np.uint32)
+            q = np.zeros((B, 1, 1), np.uint32)
+            pb.decode_layer(0, q, kn, kn)
+            pb.advance()
+        assert pb.L == op["L"], (op, pb.L)
+        cells = pb.K[0, :, 0, :, 0].view(np.float32)
+        for b in range(B):
+            got = " ".join(_decode_cell(x) for x in cells[b])
+            assert got == op["rows"][b], (op["op"], b, got, op["rows"][b])
+        want_mask = np.array([[int(x) for x in r.split()] for r in op["mask"]], np.uint8)
+        assert np.array_equal(pb.mask(), want_mask), (op["op"], pb.mask(), want_mask)
+
+
+def pin_gqa_mapping(O):
+    """Grouped-query reading (tests/golden/attention_worked.json, gqa)."""
+    g = _load("attention_worked.json")["gqa"]
+    Hq, Hkv, D = g["n_q_heads"], g["n_kv_heads"], 4
+    pb = O.PaddedBatch(1, 1, Hq, Hkv, D, O.F32)
+    rng = np.random.default_rng(0)
+    n = 6
+    k = rng.standard_normal((1, Hkv, n, D)).astype(np.float32).view(np.uint32)
+    v = np.stack([np.full((n, D), c, np.float32) for c in g["v_const"]])[None].view(np.uint32)
+    pb.embed([0], [n], [k], [v])
+    q = rng.standard_normal((1, Hq, D)).astype(np.float32).view(np.uint32)
+    kn = rng.standard_normal((1, Hkv, D)).astype(np.float32).view(np.uint32)
+    vn = np.array([[np.full(D, c, np.float32) for c in g["v_const"]]]).view(np.uint32)
+    out = pb.decode_layer(0, q, kn, vn)
+    assert np.allclose(out[0], np.array(g["out_const"])[:, None], atol=1e-12), out
+
+
+def _random_ops(rng, B, steps, max_len):
+    ops = []
+    live = set()
+    for _ in range(steps):
+        free = [b for b in range(B) if b not in live]
+        r = rng.random()
+        if live and r < 0.3:
+            k = int(rng.integers(1, len(live) + 1))
+            ev = sorted(rng.choice(sorted(live), k, replace=False).tolist())
+            ops.append(("evict", ev))
+            live -= set(ev)
+        elif free and r < 0.6:
+            k = int(rng.integers(1, len(free) + 1))
+            ins = rng.choice(free, k, replace=False).tolist()
+            ops.append(("embed", ins, [int(rng.integers(1, max_len + 1)) for _ in ins]))
+            live |= set(ins)
+        else:
+            ops.append(("decode",))
+    return ops
+
+
+def _run(O, ops, NL, B, Hq, Hkv, D, dtype, seed, fill=None, check=None):
+    """Apply ops to a PaddedBatch with random tensors; call check(pb, op, outs)."""
+    rng = np.random.default_rng(seed)
+    pb = O.PaddedBatch(NL, B, Hq, Hkv, D, dtype, fill_bits=fill)
+
+    def rand_bits(shape):
+        x = rng.standard_normal(shape).astype(np.float32)
+        if dtype == O.BF16:
+            return (x.view(np.uint32) >> 16).astype(np.uint16)
+        return x.view(np.uint32)
+
+    for op in ops:
+        outs = None
+        if op[0] == "evict":
+            pb.evict(op[1], release=True)
+        elif op[0] == "embed":
+            ks = [rand_bits((NL, Hkv, n, D)) for n in op[2]]
+            vs = [rand_bits((NL, Hkv, n, D)) for n in op[2]]
+            pb.embed(op[1], op[2], ks, vs)
+        else:
+            outs = []
+            for layer in range(NL):
+                q = rand_bits((B, Hq, D))
+                kn = rand_bits((B, Hkv, D))
+                vn = rand_bits((B, Hkv, D))
+                o = pb.decode_layer(layer, q, kn, vn)
+                outs.append((q, o, pb.decode_layer_padded(layer, q)))
+            pb.advance()
+        if check is not None:
+            check(pb, op, outs)
+    return pb
+
+
+def pin_isolation_invariant(O):
+    """The paper's correctness claim (sec. 4.1): a query's output in the shaped,
+    masked batch equals its output over its own tokens alone."""
+    rng = np.random.default_rng(21)
+
+    def check(pb, op, outs):
+        if outs:
+            for _, iso, batched in outs:
+                assert np.allclose(iso, batched, rtol=0, atol=1e-12)
+
+    for trial in range(6):
+        ops = _random_ops(rng, B=4, steps=14, max_len=9)
+        _run(O, ops, 2, 4, 4, 2, 8, O.BF16 if trial % 2 else O.F32, seed=trial, check=check)
+
+
+def pin_layout_invariants(O):
+    """Shape rules of secs. 4.1-4.2 on random op sequences: live rows are
+    placeholders then the query's own history (end-aligned), free rows are all
+    placeholders, L is the longest live row after a release, an insertion makes
+    L = max(L, l_q), the mask row is a suffix of ones of length len+1."""
+    rng = np.random.default_rng(8)
+
+    def check(pb, op, outs):
+        fill = pb.fill
+        for b in range(pb.B):
+            n = pb.lens[b]
+            assert 0 <= n <= pb.L
+            row = pb.K[:, b]
+            if n == 0:
+                assert np.all(row == fill)
+            else:
+                assert np.all(row[:, :, : pb.L - n] == fill)
+                assert np.array_equal(row[:, :, pb.L - n:], pb.hist_k[b])
+                assert np.array_equal(pb.V[:, b, :, pb.L - n:], pb.hist_v[b])
+            m = pb.mask()[b]
+            want = np.zeros(pb.L + 1, np.uint8)
+            if n:
+                want[pb.L - n:] = 1
+            assert np.array_equal(m, want)
+        if op[0] == "evict":
+            assert pb.L == max(pb.lens)
+        elif op[0] == "embed":
+            assert pb.L == max(check.prev_L, max(op[2]))
+        else:
+            assert pb.L == check.prev_L + 1
+        check.prev_L = pb.L
+
+    for trial in range(8):
+        check.prev_L = 0
+        ops = _random_ops(rng, B=3, steps=16, max_len=7)
+        _run(O, ops, 1, 3, 2, 1, 4, O.F32, seed=100 + trial, check=check)
+
+
+def pin_embed_order_and_release(O):
+    """Insertions commute (one growth to the longest equals growths one by one),
+    and releasing twice drops nothing more."""
+    rng = np.random.default_rng(4)
+    for trial in range(10):
+        lens = [int(x) for x in rng.integers(1, 12, size=3)]
+        base = int(rng.integers(1, 12))
+        srcs = [rng.integers(0, 2**31, size=(1, 2, n, 3)).astype(np.uint32) for n in [base] + lens]
+        states = []
+        for order in itertools.permutations(range(3)):
+            pb = O.PaddedBatch(1, 4, 2, 2, 3, O.F32)
+            pb.embed([0], [base], [srcs[0]], [srcs[0]])
+            pb.embed([1 + i for i in order], [lens[i] for i in order],
+                     [srcs[1 + i] for i in order], [srcs[1 + i] for i in order])
+            states.append((pb.L, pb.K.copy(), pb.mask()))
+        for L, K, M in states[1:]:
+            assert L == states[0][0] and np.array_equal(K, states[0][1])
+            assert np.array_equal(M, states[0][2])
+        assert states[0][0] == max([base] + lens)
+        pb.evict([0], release=True)
+        L1 = pb.L
+        assert pb.release() == 0 and pb.L == L1
+
+
+def pin_brute_force_small(O):
+    """Every sequence of up to four operations on 2 slots with lengths <= 2:
+    the padded rows always equal placeholders + the query's own history, and
+    every query's batched output equals its isolated output."""
+    B = 2
+    choices = []
+    for s in range(B):
+        for n in (1, 2):
+            choices.append(("embed", [s], [n]))
+        choices.append(("evict", [s]))
+    choices.append(("evict", [0, 1]))
+    choices.append(("embed", [0, 1], [2, 1]))
+    choices.append(("decode",))
+    count = 0
+
+    def check(pb, op, outs):
+        for b in range(pb.B):
+            n = pb.lens[b]
+            if n:
+                assert np.array_equal(pb.K[:, b, :, pb.L - n:], pb.hist_k[b])
+                assert np.all(pb.K[:, b, :, : pb.L - n] == pb.fill)
+            else:
+                assert np.all(pb.K[:, b] == pb.fill)
+        if outs:
+            for _, iso, batched in outs:
+                assert np.allclose(iso, batched, atol=1e-12)
+
+    for length in range(1, 5):
+        for seq in itertools.product(choices, repeat=length):
+            live = set()
+            ok = True
+            for op in seq:      # keep only valid sequences
+                if op[0] == "embed":
+                    ok &= not (set(op[1]) & live)
+                    live |= set(op[1])
+                elif op[0] == "evict":
+                    ok &= set(op[1]) <= live
+                    live -= set(op[1])
+            if not ok:
+                continue
+            _run(O, list(seq), 1, B, 2, 1, 2, O.F32, seed=length, check=check)
+            count += 1
+    assert count > 100
+
+
+def pin_placeholder_poison(O):
+    """Placeholder bits never enter the arithmetic: -inf, 0 and NaN placeholders
+    give bit-identical outputs (the paper's -inf would poison a product with 0)."""
+    rng = np.random.default_rng(9)
+    ops = _random_ops(rng, B=3, steps=12, max_len=6)
+    results = []
+    for fill in (0xFF800000, 0x00000000, 0x7FC00001):
+        outs = []
+        _run(O, ops, 1, 3, 2, 2, 4, O.F32, seed=77, fill=fill,
+             check=lambda pb, op, o: outs.extend(x[1] for x in (o or [])))
+        results.append(outs)
+    for other in results[1:]:
+        assert len(other) == len(results[0])
+        for a, b in zip(results[0], other):
+            assert np.array_equal(a, b)
+            assert np.all(np.isfinite(a))
+
+
+def pin_error_paths(O):
+    """Invalid operations are refused and leave the batch as it was."""
+    pb = O.PaddedBatch(1, 3, 1, 1, 2, O.F32)
+    src = np.zeros((1, 1, 4, 2), np.uint32)
+    pb.embed([0], [4], [src], [src])
+    before = (pb.L, list(pb.lens), pb.K.copy())
+    for bad in (lambda: pb.evict([1]), lambda: pb.embed([0], [2], [src[:, :, :2]], [src[:, :, :2]]),
+                lambda: pb.embed([1, 1], [1, 1], [src[:, :, :1]] * 2, [src[:, :, :1]] * 2),
+                lambda: pb.embed([2], [0], [src[:, :, :0]], [src[:, :, :0]]),
+                lambda: pb.evict([5]), lambda: pb.advance()):
+        try:
+            bad()
+        except (ValueError, LookupError, RuntimeError):
+            pass
+        else:
+            raise AssertionError("invalid operation accepted")
+        assert (pb.L, list(pb.lens)) == before[:2] and np.array_equal(pb.K, before[2])
+
+
+ALL_PINS = [pin_attention_worked, pin_attention_closed_forms, pin_attention_sdpa,
+            pin_attention_permutation, pin_insertion_replay, pin_gqa_mapping,
+            pin_isolation_invariant, pin_layout_invariants, pin_embed_order_and_release,
+            pin_brute_force_small, pin_placeholder_poison, pin_error_paths]
