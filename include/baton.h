@@ -1,0 +1,203 @@
+/*
+ * baton.h -- C ABI of libbaton.so: the re-batched decode step of Baton
+ * (Cong, Chen, Zhao, Yang, "Baton: Enhancing Batch-wise Inference Efficiency
+ * for Large Language Models via Dynamic Re-batching", 2024) on MI355X (gfx950).
+ *
+ * One batch of `batch` slots decodes together over a dimension-aligned KV cache
+ * (sec. 4.1, "Vector Shaping"): every row (layer, slot, kv-head) has the same
+ * padded length L, a live slot's tokens sit at the right end of its row
+ * (columns L-len .. L-1) and everything before them is a placeholder.  Between
+ * decode steps, finished queries leave (baton_kv_evict) and prefilled queries
+ * take free slots (baton_kv_embed, sec. 4.2, "Vector Embedding"); each step
+ * then runs masked attention for one new token per query (baton_decode_attn)
+ * and appends that token's key/value as column L (sec. 4.1, second iteration).
+ *
+ * Conventions
+ *  - Every call returns a baton_status.  Arguments and state are checked on the
+ *    host before anything is enqueued; on any error nothing is enqueued and the
+ *    cache's state is unchanged.
+ *  - Device work is enqueued on the caller's stream and the call returns at
+ *    once (stream order, no host synchronisation).  All work on one cache must
+ *    go to one stream; a handle is not thread-safe.
+ *  - Ownership: the caller allocates and owns all device memory (the K/V ring
+ *    buffers, sources, q/k_new/v_new/out, mask, workspace).  The library owns
+ *    only the host handle and never allocates device memory.  Device buffers
+ *    must stay valid until the stream has passed the call that uses them.
+ *  - Element types: fp32 or bf16 storage, fp32 arithmetic.  head_dim 64 or 128;
+ *    n_q_heads / n_kv_heads in {1, 2, 4, 8}; batch <= BATON_MAX_BATCH.
+ *
+ * Memory layout (device).  K and V are each
+ *     [n_layers][batch][n_kv_heads][capacity][head_dim]
+ * contiguous elements.  The `capacity` columns of a row form a ring: logical
+ * column j of the aligned cache (0 <= j < L) lives at physical column
+ * (base + j) mod capacity, where base is reported by baton_cache_query.  Every
+ * physical position that is not a live token holds the placeholder bits
+ * (fill_bits) at every call boundary -- free rows, the placeholder fronts of
+ * live rows and the capacity - L unused columns alike.
+ */
+#ifndef BATON_H
+#define BATON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum baton_status {
+  BATON_OK = 0,
+  BATON_EINVAL = 1,    /* malformed argument: null pointer, size or index out of range, duplicate slot */
+  BATON_ESLOT = 2,     /* evicting a free slot, or embedding into a live one */
+  BATON_ECAPACITY = 3, /* the padded length plus the next appended column would exceed capacity */
+  BATON_EDTYPE = 4,    /* unsupported element type, head_dim or head grouping */
+  BATON_ESTATE = 5,    /* call out of order with the decode step in progress */
+  BATON_EHIP = 6       /* the HIP runtime refused a launch */
+} baton_status;
+
+typedef enum baton_dtype { BATON_F32 = 0, BATON_BF16 = 1 } baton_dtype;
+
+/* The paper's placeholder value, -inf (sec. 4.1, KV_Cache paragraph; sec. 4.2). */
+#define BATON_FILL_NEG_INF_F32 0xFF800000u
+#define BATON_FILL_NEG_INF_BF16 0xFF80u
+
+#define BATON_MAX_BATCH 512
+
+/* baton_cache_create flags */
+#define BATON_CREATE_ASSUME_FILLED 1u /* K and V already hold fill_bits everywhere: enqueue nothing */
+
+/* baton_kv_evict flags */
+#define BATON_RELEASE 1u /* then release the leading columns that are placeholders in every live row */
+
+typedef struct baton_cache_desc {
+  int32_t dtype;      /* baton_dtype of K, V, sources, q, k_new, v_new and out */
+  int32_t n_layers;   /* >= 1 */
+  int32_t batch;      /* slots, 1 .. BATON_MAX_BATCH */
+  int32_t n_q_heads;  /* query heads per layer */
+  int32_t n_kv_heads; /* key/value heads per layer (n_q_heads / n_kv_heads in {1,2,4,8}) */
+  int32_t head_dim;   /* 64 or 128 */
+  int64_t capacity;   /* ring columns per row, >= 2 */
+  void* k;            /* device, [n_layers][batch][n_kv_heads][capacity][head_dim], 16-byte aligned */
+  void* v;            /* device, same shape as k */
+  uint32_t fill_bits; /* placeholder bit pattern in the low 32 (fp32) or 16 (bf16) bits */
+} baton_cache_desc;
+
+typedef struct baton_cache baton_cache; /* opaque host handle */
+
+/*
+ * Create a handle for an empty batch: L = 0, every slot free.  Unless
+ * BATON_CREATE_ASSUME_FILLED is given, enqueues on `stream` the write of
+ * fill_bits over all of K and V.  The descriptor is copied.
+ * Errors: EINVAL (null out/k/v, sizes out of range, misaligned k/v),
+ * EDTYPE (dtype, head_dim or grouping unsupported), EHIP.
+ */
+baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hipStream_t stream,
+                                baton_cache** out);
+
+/* Free the host handle (device memory stays the caller's).  NULL is accepted. */
+baton_status baton_cache_destroy(baton_cache* cache);
+
+/*
+ * Finished queries leave their slots (sec. 4.1, Attention_mask and KV_Cache
+ * paragraphs: the finished query's cached keys/values are overwritten with the
+ * placeholder and its mask row zeroed).  slots: host array of n distinct live
+ * slot indices (n may be 0).  Enqueues the placeholder write over each slot's
+ * live tokens in every layer and head; the slot becomes free.  With
+ * BATON_RELEASE, the columns [0 : min over live rows of (L - len)] are then
+ * released (sec. 4.1, "Resources releasing"): L becomes the longest live
+ * length (0 when no slot is live).  Release itself moves no data.
+ * Errors: EINVAL (n < 0, null slots with n > 0, index out of range, duplicate,
+ * unknown flag), ESLOT (a slot is free), ESTATE (inside a decode step), EHIP.
+ */
+baton_status baton_kv_evict(baton_cache* cache, const int32_t* slots, int32_t n, uint32_t flags,
+                            hipStream_t stream);
+
+/*
+ * Prefilled queries take free slots (sec. 4.2, "Vector Embedding").  slots and
+ * lens: host arrays of n entries (n may be 0); k_src and v_src: host arrays of
+ * n device pointers, each [n_layers][n_kv_heads][lens[i]][head_dim] contiguous,
+ * 16-byte aligned.  If the longest query exceeds L (the case l_q > l_kv), the
+ * batch first grows on the left to that length, every other row's new front
+ * being placeholders; then each query's keys/values are copied end-aligned into
+ * its slot, placeholders in front (the case l_q <= l_kv).  Growth moves no
+ * data: the new front columns already hold placeholders.
+ * Errors: EINVAL (n < 0, null arrays or pointers, slot out of range, duplicate,
+ * lens[i] < 1), ESLOT (a slot is live), ECAPACITY (max(L, max lens) + 1 >
+ * capacity), ESTATE (inside a decode step), EHIP.
+ */
+baton_status baton_kv_embed(baton_cache* cache, const int32_t* slots, int32_t n, const int32_t* lens,
+                            const void* const* k_src, const void* const* v_src, hipStream_t stream);
+
+/*
+ * The 0-1 attention mask of the current step (sec. 2.1, "Batch-wise inference";
+ * sec. 4.1: a column of ones for the current token, zero rows for finished
+ * queries; sec. 4.2: zeros over the grown front of existing rows).  Writes
+ * mask[b * ld + j] for 0 <= j <= L: 1 when slot b is live and j >= L - len_b,
+ * else 0.  Column L is the token being decoded.  mask: device uint8, >= batch
+ * rows of ld bytes.  Bytes at j > L are not touched.
+ * Errors: EINVAL (null mask, ld < L + 1), EHIP.
+ */
+baton_status baton_build_mask(const baton_cache* cache, uint8_t* mask, int64_t ld,
+                              hipStream_t stream);
+
+/* Bytes of device workspace baton_decode_attn needs for this cache (fixed for its lifetime). */
+size_t baton_decode_attn_workspace_bytes(const baton_cache* cache);
+
+/*
+ * Decode attention of one layer (sec. 2.1, "General architecture": dot products
+ * of the query with the keys, scaling, softmax, weighted sum of the values).
+ * For every live slot b and query head hq (kv-head h = hq / (n_q_heads /
+ * n_kv_heads)): appends k_new[b][h], v_new[b][h] to the layer's cache as
+ * column L, then
+ *     out[b][hq] = softmax_j(scale * q[b][hq] . K[b][h][j]) . V[b][h][j]
+ * over the slot's own columns j in [L - len_b, L] only; placeholder columns
+ * are skipped, never read into arithmetic.  Free slots: nothing appended, out
+ * rows set to 0.  Arithmetic in fp32; out rounded to nearest-even in the
+ * cache's dtype.
+ * q, out: device [batch][n_q_heads][head_dim]; k_new, v_new: device
+ * [batch][n_kv_heads][head_dim]; all 16-byte aligned.  scale = 0 selects
+ * 1/sqrt(head_dim).  ws: device workspace of >= baton_decode_attn_workspace_bytes
+ * bytes, 16-byte aligned, used by one cache at a time; its contents are the
+ * library's between calls.  Call once per layer per step, then
+ * baton_step_advance.
+ * Errors: EINVAL (layer out of range, null pointer, ws too small, scale not
+ * finite), ESTATE (layer already decoded this step), ECAPACITY (L + 1 >
+ * capacity), EHIP.
+ */
+baton_status baton_decode_attn(baton_cache* cache, int32_t layer, const void* q, const void* k_new,
+                               const void* v_new, void* out, float scale, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * Close the decode step once every layer has been decoded: L += 1 and every
+ * live slot's length += 1 (sec. 4.1: cache and mask grow by one column per
+ * iteration).  Host metadata only.
+ * Errors: ESTATE (some layer not decoded this step).
+ */
+baton_status baton_step_advance(baton_cache* cache);
+
+/*
+ * Current metadata: padded length L, ring base (physical column of logical
+ * column 0), and per-slot lengths (host array of batch entries, 0 = free).
+ * Any output pointer may be NULL.  A caller applying rotary position
+ * embeddings uses position len_b for slot b's next token.
+ */
+baton_status baton_cache_query(const baton_cache* cache, int64_t* L, int64_t* base, int32_t* lens);
+
+/*
+ * Tuning: tokens per split of a row in baton_decode_attn (a multiple of 64,
+ * 64 .. 4096).  Changes baton_decode_attn_workspace_bytes; only between steps.
+ * Errors: EINVAL (out of range), ESTATE (inside a decode step).
+ */
+baton_status baton_set_split_tokens(baton_cache* cache, int32_t tokens);
+
+/* Static English text of a status. */
+const char* baton_status_string(baton_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BATON_H */

@@ -1,0 +1,108 @@
+"""BatonCache: one libbaton handle plus the device buffers it works on.
+
+PyTorch provides device memory and the stream; every operation is one call of
+the C ABI (paper_2410_18701_amd/baton.py).
+"""
+from . import baton as B
+
+_DTYPE_CODE = {"f32": B.BATON_F32, "bf16": B.BATON_BF16}
+_FILL = {"f32": B.BATON_FILL_NEG_INF_F32, "bf16": B.BATON_FILL_NEG_INF_BF16}
+
+
+def torch_dtype(dtype):
+    import torch
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+def _cur_stream():
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+class BatonCache:
+    """A batch of `batch` slots over a K/V ring of `capacity` columns per row.
+
+    k, v: [n_layers][batch][n_kv_heads][capacity][head_dim] device tensors.
+    """
+
+    def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, capacity, dtype="bf16",
+                 fill_bits=None, device="cuda", k=None, v=None, assume_filled=False):
+        import torch
+        self.dtype = dtype
+        self.n_layers, self.batch = n_layers, batch
+        self.n_q_heads, self.n_kv_heads, self.head_dim = n_q_heads, n_kv_heads, head_dim
+        self.capacity = capacity
+        self.fill_bits = _FILL[dtype] if fill_bits is None else fill_bits
+        tdt = torch_dtype(dtype)
+        shape = (n_layers, batch, n_kv_heads, capacity, head_dim)
+        self.k = torch.empty(shape, dtype=tdt, device=device) if k is None else k
+        self.v = torch.empty(shape, dtype=tdt, device=device) if v is None else v
+        desc = B.baton_cache_desc(_DTYPE_CODE[dtype], n_layers, batch, n_q_heads, n_kv_heads,
+                                  head_dim, capacity, self.k.data_ptr(), self.v.data_ptr(),
+                                  self.fill_bits)
+        flags = B.BATON_CREATE_ASSUME_FILLED if assume_filled else 0
+        self.handle = B.baton_cache_create(desc, flags, _cur_stream())
+        self._ws = None
+
+    # -- workspace --
+    def workspace(self):
+        import torch
+        need = B.baton_decode_attn_workspace_bytes(self.handle)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.k.device)
+        return self._ws
+
+    def set_split_tokens(self, tokens):
+        B.baton_set_split_tokens(self.handle, tokens)
+
+    # -- the step --
+    def evict(self, slots, release=True, stream=None):
+        B.baton_kv_evict(self.handle, slots, B.BATON_RELEASE if release else 0,
+                         stream if stream is not None else _cur_stream())
+
+    def embed(self, slots, lens, k_src, v_src, stream=None):
+        B.baton_kv_embed(self.handle, slots, lens, k_src, v_src,
+                         stream if stream is not None else _cur_stream())
+
+    def build_mask(self, out=None, stream=None):
+        import torch
+        L = self.query()[0]
+        if out is None:
+            out = torch.empty((self.batch, L + 1), dtype=torch.uint8, device=self.k.device)
+        B.baton_build_mask(self.handle, out, out.stride(0), stream if stream is not None else _cur_stream())
+        return out
+
+    def decode_attn(self, layer, q, k_new, v_new, out=None, scale=0.0, stream=None):
+        import torch
+        if out is None:
+            out = torch.empty_like(q)
+        ws = self.workspace()
+        B.baton_decode_attn(self.handle, layer, q, k_new, v_new, out, scale, ws, ws.numel(),
+                            stream if stream is not None else _cur_stream())
+        return out
+
+    def advance(self):
+        B.baton_step_advance(self.handle)
+
+    def query(self):
+        """(L, base, lens)."""
+        return B.baton_cache_query(self.handle, self.batch)
+
+    def logical(self, which="k"):
+        """The aligned cache [layer][batch][head][L][dim] read off the ring (a copy)."""
+        import torch
+        L, base, _ = self.query()
+        buf = self.k if which == "k" else self.v
+        idx = (torch.arange(L, device=buf.device) + base) % self.capacity
+        return buf.index_select(3, idx)
+
+    def close(self):
+        if self.handle:
+            B.baton_cache_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

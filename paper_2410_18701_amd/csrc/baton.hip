@@ -1,0 +1,409 @@
+// Host runtime of libbaton.so: handle, validation, metadata, launches.
+// The C ABI is documented in include/baton.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "baton.h"
+#include "common.hpp"
+#include "decode_attn.hpp"
+#include "kv_ops.hpp"
+
+static_assert(BATON_MAX_BATCH == baton::kMetaThreads, "meta kernel covers every slot");
+
+struct baton_cache {
+  baton_cache_desc d;
+  int32_t esz;             // bytes per element
+  int32_t vpt;             // 16-byte vectors per token row
+  int32_t group;           // q-heads per kv-head
+  int32_t split;           // tokens per attention work item
+  int64_t L = 0;           // padded length
+  int64_t base = 0;        // physical column of logical column 0
+  std::vector<int32_t> lens;
+  std::vector<uint8_t> layer_done;
+  int32_t n_done = 0;      // layers decoded in the current step
+  // Work list of the current step as last written into a workspace.
+  const void* meta_ws = nullptr;
+  bool meta_valid = false;
+  int32_t n_items = 0;
+};
+
+namespace {
+
+using baton::SegArgs;
+
+uint32_t fill_word(const baton_cache* c) {
+  if (c->esz == 4) return c->d.fill_bits;
+  const uint32_t h = c->d.fill_bits & 0xFFFFu;
+  return h | (h << 16);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+baton_status hip_status(hipError_t e) { return e == hipSuccess ? BATON_OK : BATON_EHIP; }
+
+int64_t ring(int64_t x, int64_t cap) {
+  x %= cap;
+  return x < 0 ? x + cap : x;
+}
+
+// Workspace layout: [lens: batch][item_start: batch + 1] [items: max_items]
+// [partials: n_kv_heads][max_items][group][head_dim + 4].
+struct WsLayout {
+  size_t lens_off, start_off, items_off, partial_off, total;
+  int64_t max_items;
+};
+
+WsLayout ws_layout(const baton_cache* c) {
+  WsLayout w;
+  const int64_t B = c->d.batch;
+  w.max_items = B * ((c->d.capacity + c->split - 1) / c->split);
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  w.lens_off = 0;
+  w.start_off = up(w.lens_off + sizeof(int32_t) * B);
+  w.items_off = up(w.start_off + sizeof(int32_t) * (B + 1));
+  w.partial_off = up(w.items_off + sizeof(int2) * w.max_items);
+  w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * w.max_items * c->group *
+                                   (c->d.head_dim + 4));
+  return w;
+}
+
+// Launches seg_kernel over the segments, kMaxSegs at a time.
+struct Seg {
+  int32_t slot, len;
+  int64_t col0;
+  const void* ks;
+  const void* vs;
+};
+
+template <int VPT>
+baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs, hipStream_t s) {
+  constexpr int TT = baton::kCopyThreads * baton::kCopyVecs / VPT;
+  for (size_t off = 0; off < segs.size(); off += baton::kMaxSegs) {
+    SegArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.k = static_cast<uint32_t*>(c->d.k);
+    a.v = static_cast<uint32_t*>(c->d.v);
+    a.cap = c->d.capacity;
+    a.n_layers = c->d.n_layers;
+    a.batch = c->d.batch;
+    a.n_kv_heads = c->d.n_kv_heads;
+    a.fill_word = fill_word(c);
+    const size_t n = std::min<size_t>(baton::kMaxSegs, segs.size() - off);
+    int64_t tiles = 0;
+    int32_t used = 0;
+    for (size_t i = 0; i < n; ++i) {
+      const Seg& g = segs[off + i];
+      if (g.len <= 0) continue;
+      const int32_t tpr = (g.len + TT - 1) / TT;
+      a.slot[used] = g.slot;
+      a.len[used] = g.len;
+      a.col0[used] = g.col0;
+      a.tiles_per_row[used] = tpr;
+      a.ksrc[used] = static_cast<const uint32_t*>(g.ks);
+      a.vsrc[used] = static_cast<const uint32_t*>(g.vs);
+      tiles += (int64_t)tpr * 2 * c->d.n_layers * c->d.n_kv_heads;
+      a.tile_end[used] = tiles;
+      ++used;
+    }
+    a.n_segs = used;
+    if (used == 0) continue;
+    if (tiles > 0x7FFFFFFF) return BATON_EINVAL;
+    hipLaunchKernelGGL(baton::seg_kernel<VPT>, dim3((unsigned)tiles), dim3(baton::kCopyThreads), 0,
+                       s, a);
+    const baton_status st = hip_status(hipGetLastError());
+    if (st != BATON_OK) return st;
+  }
+  return BATON_OK;
+}
+
+baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hipStream_t s) {
+  switch (c->vpt) {
+    case 8: return launch_segs_vpt<8>(c, segs, s);
+    case 16: return launch_segs_vpt<16>(c, segs, s);
+    case 32: return launch_segs_vpt<32>(c, segs, s);
+    default: return BATON_EDTYPE;
+  }
+}
+
+// ---------------------------------------------------------------- attention --
+template <typename T, int D, int G>
+void launch_attn_t(const baton::AttnArgs& a, int n_items, int batch, int hkv, hipStream_t s) {
+  constexpr int U = G <= 2 ? 8 : 4;
+  if (n_items > 0)
+    hipLaunchKernelGGL((baton::attn_kernel<T, D, G, U>), dim3(n_items, hkv), dim3(baton::kWave), 0,
+                       s, a);
+  hipLaunchKernelGGL((baton::combine_kernel<T, D, G>), dim3(batch, hkv), dim3(baton::kWave), 0, s,
+                     a);
+}
+
+template <typename T, int D>
+bool launch_attn_d(int g, const baton::AttnArgs& a, int n_items, int batch, int hkv,
+                   hipStream_t s) {
+  switch (g) {
+    case 1: launch_attn_t<T, D, 1>(a, n_items, batch, hkv, s); return true;
+    case 2: launch_attn_t<T, D, 2>(a, n_items, batch, hkv, s); return true;
+    case 4: launch_attn_t<T, D, 4>(a, n_items, batch, hkv, s); return true;
+    case 8: launch_attn_t<T, D, 8>(a, n_items, batch, hkv, s); return true;
+    default: return false;
+  }
+}
+
+bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, int n_items, hipStream_t s) {
+  const int B = c->d.batch, H = c->d.n_kv_heads;
+  if (c->d.dtype == BATON_F32) {
+    if (c->d.head_dim == 64) return launch_attn_d<baton::F32Tag, 64>(c->group, a, n_items, B, H, s);
+    return launch_attn_d<baton::F32Tag, 128>(c->group, a, n_items, B, H, s);
+  }
+  if (c->d.head_dim == 64) return launch_attn_d<baton::BF16Tag, 64>(c->group, a, n_items, B, H, s);
+  return launch_attn_d<baton::BF16Tag, 128>(c->group, a, n_items, B, H, s);
+}
+
+int default_split(const baton_cache_desc& d) { return d.dtype == BATON_F32 ? 128 : 256; }
+
+}  // namespace
+
+extern "C" {
+
+const char* baton_status_string(baton_status s) {
+  switch (s) {
+    case BATON_OK: return "ok";
+    case BATON_EINVAL: return "invalid argument";
+    case BATON_ESLOT: return "slot is in the wrong state (evicting a free slot or embedding into a live one)";
+    case BATON_ECAPACITY: return "padded length would exceed the ring capacity";
+    case BATON_EDTYPE: return "unsupported element type, head_dim or head grouping";
+    case BATON_ESTATE: return "call out of order with the decode step in progress";
+    case BATON_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hipStream_t stream,
+                                baton_cache** out) {
+  if (!desc || !out) return BATON_EINVAL;
+  if (flags & ~BATON_CREATE_ASSUME_FILLED) return BATON_EINVAL;
+  const baton_cache_desc& d = *desc;
+  if (d.dtype != BATON_F32 && d.dtype != BATON_BF16) return BATON_EDTYPE;
+  if (d.head_dim != 64 && d.head_dim != 128) return BATON_EDTYPE;
+  if (d.n_layers < 1 || d.batch < 1 || d.batch > BATON_MAX_BATCH || d.n_q_heads < 1 ||
+      d.n_kv_heads < 1 || d.capacity < 2 || d.capacity > (int64_t(1) << 31))
+    return BATON_EINVAL;
+  if (d.n_q_heads % d.n_kv_heads) return BATON_EDTYPE;
+  const int32_t g = d.n_q_heads / d.n_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return BATON_EDTYPE;
+  if (!d.k || !d.v || !aligned16(d.k) || !aligned16(d.v)) return BATON_EINVAL;
+  baton_cache* c = new (std::nothrow) baton_cache();
+  if (!c) return BATON_EINVAL;
+  c->d = d;
+  c->esz = d.dtype == BATON_F32 ? 4 : 2;
+  c->vpt = d.head_dim * c->esz / 16;
+  c->group = g;
+  c->split = default_split(d);
+  c->lens.assign(d.batch, 0);
+  c->layer_done.assign(d.n_layers, 0);
+  if (!(flags & BATON_CREATE_ASSUME_FILLED)) {
+    const int64_t n_vec = (int64_t)d.n_layers * d.batch * d.n_kv_heads * d.capacity * c->vpt;
+    const int64_t blocks = std::min<int64_t>((n_vec + 255) / 256, 256 * 64);
+    hipLaunchKernelGGL(baton::fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       static_cast<baton::u32x4*>(d.k), static_cast<baton::u32x4*>(d.v), n_vec,
+                       fill_word(c));
+    const baton_status st = hip_status(hipGetLastError());
+    if (st != BATON_OK) {
+      delete c;
+      return st;
+    }
+  }
+  *out = c;
+  return BATON_OK;
+}
+
+baton_status baton_cache_destroy(baton_cache* c) {
+  delete c;
+  return BATON_OK;
+}
+
+baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uint32_t flags,
+                            hipStream_t stream) {
+  if (!c || n < 0 || (n > 0 && !slots) || (flags & ~BATON_RELEASE)) return BATON_EINVAL;
+  if (c->n_done) return BATON_ESTATE;
+  std::vector<uint8_t> seen(c->d.batch, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = slots[i];
+    if (s < 0 || s >= c->d.batch || seen[s]) return BATON_EINVAL;
+    seen[s] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i)
+    if (c->lens[slots[i]] == 0) return BATON_ESLOT;
+  // The finished queries' tokens become placeholders (the rest of their rows already is).
+  std::vector<Seg> segs;
+  segs.reserve(n);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = slots[i], len = c->lens[s];
+    segs.push_back({s, len, ring(c->base + c->L - len, c->d.capacity), nullptr, nullptr});
+  }
+  const baton_status st = launch_segs(c, segs, stream);
+  if (st != BATON_OK) return st;
+  for (int32_t i = 0; i < n; ++i) c->lens[slots[i]] = 0;
+  if (flags & BATON_RELEASE) {
+    int64_t r = c->L;
+    for (int32_t b = 0; b < c->d.batch; ++b)
+      if (c->lens[b] > 0) r = std::min<int64_t>(r, c->L - c->lens[b]);
+    c->base = ring(c->base + r, c->d.capacity);
+    c->L -= r;
+  }
+  c->meta_valid = false;
+  return BATON_OK;
+}
+
+baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, const int32_t* lens,
+                            const void* const* k_src, const void* const* v_src,
+                            hipStream_t stream) {
+  if (!c || n < 0) return BATON_EINVAL;
+  if (n > 0 && (!slots || !lens || !k_src || !v_src)) return BATON_EINVAL;
+  if (c->n_done) return BATON_ESTATE;
+  std::vector<uint8_t> seen(c->d.batch, 0);
+  int64_t longest = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = slots[i];
+    if (s < 0 || s >= c->d.batch || seen[s] || lens[i] < 1) return BATON_EINVAL;
+    if (!k_src[i] || !v_src[i] || !aligned16(k_src[i]) || !aligned16(v_src[i])) return BATON_EINVAL;
+    seen[s] = 1;
+    longest = std::max<int64_t>(longest, lens[i]);
+  }
+  for (int32_t i = 0; i < n; ++i)
+    if (c->lens[slots[i]] != 0) return BATON_ESLOT;
+  const int64_t L_new = std::max(c->L, longest);
+  if (L_new + 1 > c->d.capacity) return BATON_ECAPACITY;
+  // Growth on the left: the new front columns come out of the unused part of
+  // the ring, which holds placeholders in every row already.
+  const int64_t base_new = ring(c->base - (L_new - c->L), c->d.capacity);
+  std::vector<Seg> segs;
+  segs.reserve(n);
+  for (int32_t i = 0; i < n; ++i)
+    segs.push_back({slots[i], lens[i], ring(base_new + L_new - lens[i], c->d.capacity), k_src[i],
+                    v_src[i]});
+  const baton_status st = launch_segs(c, segs, stream);
+  if (st != BATON_OK) return st;
+  c->base = base_new;
+  c->L = L_new;
+  for (int32_t i = 0; i < n; ++i) c->lens[slots[i]] = lens[i];
+  c->meta_valid = false;
+  return BATON_OK;
+}
+
+baton_status baton_build_mask(const baton_cache* c, uint8_t* mask, int64_t ld, hipStream_t stream) {
+  if (!c || !mask || ld < c->L + 1) return BATON_EINVAL;
+  baton::MaskArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.mask = mask;
+  a.ld = ld;
+  a.L = c->L;
+  a.batch = c->d.batch;
+  for (int32_t b = 0; b < c->d.batch; ++b) a.lens[b] = c->lens[b];
+  const int64_t per_block = 256 * 4;
+  const int64_t bx = std::min<int64_t>((c->L + 1 + per_block - 1) / per_block, 1024);
+  hipLaunchKernelGGL(baton::mask_kernel, dim3((unsigned)bx, c->d.batch), dim3(256), 0, stream, a);
+  return hip_status(hipGetLastError());
+}
+
+size_t baton_decode_attn_workspace_bytes(const baton_cache* c) {
+  return c ? ws_layout(c).total : 0;
+}
+
+baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, const void* k_new,
+                               const void* v_new, void* out, float scale, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  if (!c || layer < 0 || layer >= c->d.n_layers) return BATON_EINVAL;
+  if (!q || !k_new || !v_new || !out || !ws) return BATON_EINVAL;
+  if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out) || !aligned16(ws))
+    return BATON_EINVAL;
+  if (!std::isfinite(scale)) return BATON_EINVAL;
+  const WsLayout w = ws_layout(c);
+  if (ws_bytes < w.total) return BATON_EINVAL;
+  if (c->layer_done[layer]) return BATON_ESTATE;
+  if (c->L + 1 > c->d.capacity) return BATON_ECAPACITY;
+  char* wsb = static_cast<char*>(ws);
+  if (!c->meta_valid || c->meta_ws != ws) {
+    baton::MetaArgs m;
+    std::memset(&m, 0, sizeof(m));
+    m.batch = c->d.batch;
+    m.split = c->split;
+    int64_t items = 0;
+    for (int32_t b = 0; b < c->d.batch; ++b) {
+      m.lens[b] = c->lens[b];
+      if (c->lens[b] > 0) items += (c->lens[b] + c->split) / c->split;
+    }
+    hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, m,
+                       reinterpret_cast<int32_t*>(wsb + w.lens_off),
+                       reinterpret_cast<int32_t*>(wsb + w.start_off),
+                       reinterpret_cast<int2*>(wsb + w.items_off));
+    const baton_status st = hip_status(hipGetLastError());
+    if (st != BATON_OK) return st;
+    c->n_items = (int32_t)items;
+    c->meta_ws = ws;
+    c->meta_valid = true;
+  }
+  baton::AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k = static_cast<const uint32_t*>(c->d.k);
+  a.k_w = static_cast<uint32_t*>(c->d.k);
+  a.v = static_cast<uint32_t*>(c->d.v);
+  a.q = static_cast<const uint32_t*>(q);
+  a.knew = static_cast<const uint32_t*>(k_new);
+  a.vnew = static_cast<const uint32_t*>(v_new);
+  a.out = static_cast<uint32_t*>(out);
+  a.lens = reinterpret_cast<const int32_t*>(wsb + w.lens_off);
+  a.item_start = reinterpret_cast<const int32_t*>(wsb + w.start_off);
+  a.items = reinterpret_cast<const int2*>(wsb + w.items_off);
+  a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
+  a.cap = c->d.capacity;
+  a.base = c->base;
+  a.L = c->L;
+  a.layer = layer;
+  a.batch = c->d.batch;
+  a.n_kv_heads = c->d.n_kv_heads;
+  a.split = c->split;
+  a.n_items = c->n_items;
+  const float sc = scale == 0.f ? 1.0f / std::sqrt((float)c->d.head_dim) : scale;
+  a.qscale = sc * 1.4426950408889634f;
+  if (!launch_attn(c, a, c->n_items, stream)) return BATON_EDTYPE;
+  const baton_status st = hip_status(hipGetLastError());
+  if (st != BATON_OK) return st;
+  c->layer_done[layer] = 1;
+  ++c->n_done;
+  return BATON_OK;
+}
+
+baton_status baton_step_advance(baton_cache* c) {
+  if (!c) return BATON_EINVAL;
+  if (c->n_done != c->d.n_layers) return BATON_ESTATE;
+  c->L += 1;
+  for (int32_t b = 0; b < c->d.batch; ++b)
+    if (c->lens[b] > 0) c->lens[b] += 1;
+  std::fill(c->layer_done.begin(), c->layer_done.end(), 0);
+  c->n_done = 0;
+  c->meta_valid = false;
+  return BATON_OK;
+}
+
+baton_status baton_cache_query(const baton_cache* c, int64_t* L, int64_t* base, int32_t* lens) {
+  if (!c) return BATON_EINVAL;
+  if (L) *L = c->L;
+  if (base) *base = c->base;
+  if (lens) std::copy(c->lens.begin(), c->lens.end(), lens);
+  return BATON_OK;
+}
+
+baton_status baton_set_split_tokens(baton_cache* c, int32_t tokens) {
+  if (!c || tokens < 64 || tokens > 4096 || tokens % 64) return BATON_EINVAL;
+  if (c->n_done) return BATON_ESTATE;
+  c->split = tokens;
+  c->meta_valid = false;
+  return BATON_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+// KV-cache shaping kernels: placeholder fill, end-aligned embed / evict scrub,
+// attention-mask build.  Pure data movement: every kernel streams 16-byte
+// vectors per lane with non-temporal stores (the data is not re-read before it
+// leaves the caches).
+#pragma once
+
+#include "common.hpp"
+
+namespace baton {
+
+constexpr int kMaxSegs = 32;   // inserts (or evictions) per launch
+constexpr int kCopyThreads = 256;
+constexpr int kCopyVecs = 4;   // 16-byte vectors per thread per tile
+
+// Work of one launch: up to kMaxSegs row sets.  Segment i covers, in every
+// layer and kv-head and for both K and V, `len[i]` tokens of slot `slot[i]`
+// starting at physical ring column `col0[i]`; with a source it copies
+// src[i][layer][head][0:len][:] there, without one it writes the placeholder.
+struct SegArgs {
+  uint32_t* k;              // ring buffers, viewed as 32-bit words
+  uint32_t* v;
+  int64_t cap;              // ring columns
+  int32_t n_layers, batch, n_kv_heads;
+  int32_t n_segs;
+  uint32_t fill_word;       // placeholder bits replicated to a 32-bit word
+  int32_t slot[kMaxSegs];
+  int32_t len[kMaxSegs];
+  int32_t tiles_per_row[kMaxSegs];
+  int64_t col0[kMaxSegs];
+  int64_t tile_end[kMaxSegs];           // inclusive prefix of tiles over segments
+  const uint32_t* ksrc[kMaxSegs];       // null: write placeholders
+  const uint32_t* vsrc[kMaxSegs];
+};
+
+// VPT = 16-byte vectors per token row (head_dim * elem_bytes / 16).  One block
+// moves one tile of TT = kCopyThreads * kCopyVecs / VPT tokens of one row.
+template <int VPT>
+__global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
+  constexpr int TT = kCopyThreads * kCopyVecs / VPT;
+  const int64_t g = blockIdx.x;
+  int i = 0;
+  while (i < a.n_segs - 1 && g >= a.tile_end[i]) ++i;
+  const int64_t local = g - (i > 0 ? a.tile_end[i - 1] : 0);
+  const int32_t tpr = a.tiles_per_row[i];
+  const int64_t row = local / tpr;
+  const int32_t tile = (int32_t)(local - row * tpr);
+  const int32_t lh_count = a.n_layers * a.n_kv_heads;
+  const int32_t which = (int32_t)(row / lh_count);          // 0: K, 1: V
+  const int32_t lh = (int32_t)(row - (int64_t)which * lh_count);
+  const int32_t layer = lh / a.n_kv_heads, h = lh - layer * a.n_kv_heads;
+  const int32_t len = a.len[i];
+  const int32_t t0 = tile * TT;
+  const int32_t nt = min(TT, len - t0);
+
+  u32x4* dst = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
+               (((int64_t)layer * a.batch + a.slot[i]) * a.n_kv_heads + h) * a.cap * VPT;
+  const uint32_t* srcw = which ? a.vsrc[i] : a.ksrc[i];
+  const u32x4* src = srcw ? reinterpret_cast<const u32x4*>(srcw) +
+                                (((int64_t)layer * a.n_kv_heads + h) * len + t0) * VPT
+                          : nullptr;
+  const int64_t c0 = ring_add(a.col0[i], t0, a.cap);
+
+  u32x4 val[kCopyVecs];
+  const u32x4 fill = {a.fill_word, a.fill_word, a.fill_word, a.fill_word};
+#pragma unroll
+  for (int r = 0; r < kCopyVecs; ++r) {
+    const int idx = threadIdx.x + r * kCopyThreads;
+    val[r] = fill;
+    if (src && idx < nt * VPT) val[r] = __builtin_nontemporal_load(src + idx);
+  }
+#pragma unroll
+  for (int r = 0; r < kCopyVecs; ++r) {
+    const int idx = threadIdx.x + r * kCopyThreads;
+    if (idx < nt * VPT) {
+      const int t = idx / VPT, e = idx - (idx / VPT) * VPT;
+      const int64_t col = ring_add(c0, t, a.cap);
+      __builtin_nontemporal_store(val[r], dst + col * VPT + e);
+    }
+  }
+}
+
+// Writes the placeholder over n_vec 16-byte vectors of each of K and V.
+__global__ void __launch_bounds__(256) fill_kernel(u32x4* __restrict__ k, u32x4* __restrict__ v,
+                                                   int64_t n_vec, uint32_t fill_word) {
+  const u32x4 fill = {fill_word, fill_word, fill_word, fill_word};
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_vec; i += stride) {
+    __builtin_nontemporal_store(fill, k + i);
+    __builtin_nontemporal_store(fill, v + i);
+  }
+}
+
+// mask[b * ld + j] = (len_b > 0 && j >= L - len_b) for j in [0, L]; one block
+// row per slot, 4 bytes per thread.
+struct MaskArgs {
+  uint8_t* mask;
+  int64_t ld, L;
+  int32_t batch;
+  int32_t lens[512];
+};
+
+__global__ void __launch_bounds__(256) mask_kernel(const MaskArgs a) {
+  const int b = blockIdx.y;
+  const int64_t n = a.lens[b];
+  const int64_t first = n > 0 ? a.L - n : a.L + 1;   // first column that is 1
+  uint8_t* row = a.mask + (int64_t)b * a.ld;
+  for (int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; j0 <= a.L;
+       j0 += (int64_t)gridDim.x * blockDim.x * 4) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t j = j0 + e;
+      if (j <= a.L) row[j] = (uint8_t)(j >= first);
+    }
+  }
+}
+
+}  // namespace baton

@@ -1,0 +1,91 @@
+"""The C ABI on the CPU: the library loads, exports every symbol of
+include/baton.h, and its host-side checks refuse bad calls before any device
+work (no GPU is touched: every call here returns before enqueueing)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2410_18701_amd import baton as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "baton.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(baton_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert "baton_decode_attn" in names and "baton_kv_embed" in names
+    lib = B.lib()
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in baton.h but not exported"
+
+
+def test_status_strings():
+    for s in range(7):
+        assert B.baton_status_string(s)
+    assert B.baton_status_string(99) == "unknown status"
+
+
+FAKE_K, FAKE_V = 0x10000, 0x20000   # never dereferenced: every call below fails host checks
+
+
+def desc(**kw):
+    d = dict(dtype=B.BATON_BF16, n_layers=2, batch=4, n_q_heads=8, n_kv_heads=2, head_dim=128,
+             capacity=300, k=FAKE_K, v=FAKE_V, fill_bits=B.BATON_FILL_NEG_INF_BF16)
+    d.update(kw)
+    return B.baton_cache_desc(**d)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), B.BATON_EDTYPE), (dict(head_dim=96), B.BATON_EDTYPE),
+    (dict(n_q_heads=6, n_kv_heads=4), B.BATON_EDTYPE), (dict(n_q_heads=32, n_kv_heads=2), B.BATON_EDTYPE),
+    (dict(batch=0), B.BATON_EINVAL), (dict(batch=513), B.BATON_EINVAL), (dict(capacity=1), B.BATON_EINVAL),
+    (dict(n_layers=0), B.BATON_EINVAL), (dict(k=0), B.BATON_EINVAL), (dict(v=FAKE_V + 8), B.BATON_EINVAL),
+])
+def test_create_rejects(kw, status):
+    with pytest.raises(B.BatonError) as e:
+        B.baton_cache_create(desc(**kw), B.BATON_CREATE_ASSUME_FILLED)
+    assert e.value.status == status
+
+
+def test_host_checks_leave_state_unchanged():
+    h = B.baton_cache_create(desc(), B.BATON_CREATE_ASSUME_FILLED)
+    try:
+        assert B.baton_cache_query(h, 4) == (0, 0, [0, 0, 0, 0])
+        assert B.baton_decode_attn_workspace_bytes(h) > 0
+
+        def status(fn, *a):
+            with pytest.raises(B.BatonError) as e:
+                fn(*a)
+            return e.value.status
+
+        assert status(B.baton_kv_evict, h, [1]) == B.BATON_ESLOT          # free slot
+        assert status(B.baton_kv_evict, h, [4]) == B.BATON_EINVAL         # out of range
+        assert status(B.baton_kv_evict, h, [0, 0]) == B.BATON_EINVAL      # duplicate
+        assert status(B.baton_kv_evict, h, [], 2) == B.BATON_EINVAL       # unknown flag
+        assert status(B.baton_kv_embed, h, [0], [0], [FAKE_K], [FAKE_V]) == B.BATON_EINVAL   # empty query
+        assert status(B.baton_kv_embed, h, [0], [300], [FAKE_K], [FAKE_V]) == B.BATON_ECAPACITY  # 300+1 > 300
+        assert status(B.baton_kv_embed, h, [0, 0], [3, 3], [FAKE_K] * 2, [FAKE_V] * 2) == B.BATON_EINVAL
+        assert status(B.baton_kv_embed, h, [0], [3], [0], [FAKE_V]) == B.BATON_EINVAL      # null source
+        assert status(B.baton_kv_embed, h, [0], [3], [FAKE_K + 4], [FAKE_V]) == B.BATON_EINVAL  # misaligned
+        assert status(B.baton_step_advance, h) == B.BATON_ESTATE          # no layer decoded
+        ws = B.baton_decode_attn_workspace_bytes(h)
+        assert status(B.baton_decode_attn, h, 2, FAKE_K, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws) == B.BATON_EINVAL
+        assert status(B.baton_decode_attn, h, 0, 0, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws) == B.BATON_EINVAL
+        assert status(B.baton_decode_attn, h, 0, FAKE_K, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws - 1) == B.BATON_EINVAL
+        assert status(B.baton_decode_attn, h, 0, FAKE_K, FAKE_K, FAKE_K, FAKE_K, float("nan"), FAKE_V, ws) == B.BATON_EINVAL
+        assert status(B.baton_build_mask, h, 0, 1) == B.BATON_EINVAL
+        assert status(B.baton_build_mask, h, FAKE_K, 0) == B.BATON_EINVAL   # ld < L + 1
+        assert status(B.baton_set_split_tokens, h, 100) == B.BATON_EINVAL
+        assert B.baton_cache_query(h, 4) == (0, 0, [0, 0, 0, 0])
+        B.baton_set_split_tokens(h, 64)
+        assert B.baton_decode_attn_workspace_bytes(h) > ws                # more, smaller splits
+    finally:
+        B.baton_cache_destroy(h)

@@ -1,0 +1,50 @@
+"""HIP path vs the oracle on whole schedules (GPU): K/V ring and mask bit-exact
+after every operation, attention within tolerance after every layer."""
+import pytest
+
+from tests import parity
+from workload import configs
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    # fp32, the tiny configuration: 4 slots, 4 heads, D=64, L=128, one insert into slot 2
+    "tiny-f32": (configs.tiny(), {}),
+    # MHA bf16 D=128, rows spanning three 256-token splits, ragged tails
+    "mha-bf16-d128": (configs.small("bf16", 2, 6, 8, 8, 128, L0=600, n_steps=4, n_evict=2, seed=31), {}),
+    # GQA 4:1, bf16 D=128
+    "gqa4-bf16-d128": (configs.small("bf16", 2, 5, 8, 2, 128, L0=300, n_steps=4, n_evict=2, seed=32), {}),
+    # GQA 8:1, 64-token splits: many items per row and the combine kernel
+    "gqa8-bf16-d128-split64": (configs.small("bf16", 1, 4, 16, 2, 128, L0=200, n_steps=3, n_evict=1, seed=33),
+                               {"split": 64}),
+    # fp32 D=128 (a token row spans 32 lanes), GQA 2:1
+    "gqa2-f32-d128-split64": (configs.small("f32", 2, 4, 4, 2, 128, L0=150, n_steps=3, n_evict=2, seed=34),
+                              {"split": 64}),
+    # bf16 D=64 (8 lanes per row, 8 rows per instruction)
+    "gqa2-bf16-d64-split64": (configs.small("bf16", 1, 7, 4, 2, 64, L0=500, n_steps=4, n_evict=3, seed=35),
+                              {"split": 64}),
+    # fp32 D=64 GQA 8:1
+    "gqa8-f32-d64": (configs.small("f32", 1, 3, 8, 1, 64, L0=90, n_steps=3, n_evict=1, seed=36), {}),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_schedule_parity(name):
+    w, kw = SMALL[name]
+    print(f"[parity] {name}: {w.name}", flush=True)
+    err = parity.run(w, **kw)
+    print(f"[parity] {name}: max abs error {err:.3g}", flush=True)
+
+
+def test_ring_wraparound_tight_capacity():
+    """Capacity = the most the run can need: releases and growths move the window
+    base across the end of the ring again and again."""
+    w = configs.small("bf16", 1, 6, 4, 4, 64, L0=160, n_steps=10, n_evict=3, seed=41)
+    cap = w.L0 + w.n_steps + 1
+    print(f"[parity] wraparound cap={cap}", flush=True)
+    parity.run(w, capacity=cap, split=64)
+
+
+def test_explicit_scale():
+    w = configs.small("f32", 1, 3, 2, 2, 64, L0=70, n_steps=2, n_evict=1, seed=42)
+    parity.run(w, scale=0.3)
