@@ -1,0 +1,283 @@
+"""Benchmark of the re-batched decode step on one MI355X.
+
+One step = the whole hot path over the batch: evict the queries that finished
+(placeholders over their tokens, release of shared leading placeholders),
+embed the newly prefilled queries end-aligned (growing the batch on the left
+when one is longer), build the mask, then masked decode attention layer by
+layer (appending each layer's new key/value column), then advance.
+
+Default workload (config 3): bf16, 32 layers x 32 heads x head_dim 128
+(7B-shaped attention), batch 64, initial padded length 4096, lengths
+lognormal(6.5, 0.8) clipped to [32, 4096], Poisson(4) arrivals per step with
+as many queries finishing, 64 decode steps (warmup + timed).  All inputs are
+synthetic and seeded, generated into HBM before the timed region.
+
+Prints one JSON line: query-tokens/s of whole steps, the dominant kernel's
+roofline (decode attention, HBM-bound), per-op HBM GB/s, and the CPU oracle
+timed on a bounded sample on this host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=60)
+    p.add_argument("--warmup", type=int, default=4)
+    p.add_argument("--config", default="cfg3", choices=["cfg2", "cfg3", "cfg5"])
+    p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-layers", type=int, default=16, help="layers of step 0 the oracle runs")
+    p.add_argument("--copy-bytes", type=int, default=2 << 30,
+                   help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
+    p.add_argument("--traffic", default=None,
+                   help="JSON file with rocprofv3-derived HBM bytes per attention launch")
+    return p.parse_args()
+
+
+def attn_bytes(w, lens):
+    """Algorithmic HBM bytes of one decode_attn launch: cached K and V of live
+    rows, k_new/v_new read and appended, q of live rows, out of every row."""
+    sz, D = w.elem_bytes, w.head_dim
+    live = [n for n in lens if n > 0]
+    kv = 2 * w.n_kv_heads * D * sum(live)
+    new = 2 * 2 * w.n_kv_heads * D * len(live)
+    qo = w.n_q_heads * D * (len(live) + w.batch)
+    return sz * (kv + new + qo)
+
+
+def embed_bytes(w, insert_lens):
+    """Read of the prefilled K/V plus its write into the cache, all layers."""
+    return 2 * sum(2 * w.n_layers * w.n_kv_heads * n * w.head_dim * w.elem_bytes for n in insert_lens)
+
+
+def evict_bytes(w, lens_before, slots):
+    """Placeholder writes over the evicted queries' tokens (overhead, not algorithmic)."""
+    return sum(2 * w.n_layers * w.n_kv_heads * lens_before[s] * w.head_dim * w.elem_bytes for s in slots)
+
+
+def cpu_baseline(w, n_layers):
+    """The oracle, timed on this host over step 0 of the workload for n_layers
+    layers (one layer of the batch at a time), scaled to query-tokens/s of the
+    whole step.  Input generation is outside the timed part."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle.baton_oracle as O
+    from workload import gen
+
+    ev = w.steps[0]
+    elapsed = 0.0
+    live_after = None
+    with threadpool_limits(limits=1):
+        for layer in range(n_layers):
+            pb = O.PaddedBatch(1, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype)
+
+            def layer_src(qid, n):
+                c0, st = gen.prefill_counter(qid, w.n_layers, w.n_kv_heads, w.head_dim, layer0=layer)
+                shp = (1, w.n_kv_heads, n, w.head_dim)
+                return (gen.fill_host(w.seed, gen.S_PREFILL_K, w.dtype, shp, c0, st),
+                        gen.fill_host(w.seed, gen.S_PREFILL_V, w.dtype, shp, c0, st))
+
+            # the initial batch, longest query first so the batch grows once
+            order = sorted(range(w.batch), key=lambda b: -w.init_lens[b])
+            init = [layer_src(b, w.init_lens[b]) for b in order]
+            pb.embed(order, [w.init_lens[b] for b in order], [x[0] for x in init], [x[1] for x in init])
+            del init
+            ins = [layer_src(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+            dec = [gen.decode_host(w.seed, sid, 0, layer, w.n_layers, w.batch, h, w.head_dim, w.dtype)
+                   for sid, h in ((gen.S_Q, w.n_q_heads), (gen.S_KNEW, w.n_kv_heads),
+                                  (gen.S_VNEW, w.n_kv_heads))]
+            t0 = time.perf_counter()
+            pb.evict(ev.evict, release=True)
+            pb.embed(ev.insert, ev.insert_lens, [x[0] for x in ins], [x[1] for x in ins])
+            pb.mask()
+            pb.decode_layer(0, dec[0], dec[1], dec[2])
+            pb.advance()
+            elapsed += time.perf_counter() - t0
+            live_after = len(pb.live())
+            del pb, ins
+    per_step = elapsed / n_layers * w.n_layers
+    return {"value": live_after / per_step, "unit": "query-tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"step 0 of {w.name} (evict, embed, mask, attention, advance) for layers "
+                      f"0..{n_layers - 1}, one layer at a time, numpy float64 on 1 thread; "
+                      f"{elapsed:.1f} s measured, scaled by {w.n_layers}/{n_layers} layers"}
+
+
+def copy_probe(nbytes, reps=5):
+    """A plain device-to-device copy of nbytes (torch's copy kernel): the
+    achievable HBM bandwidth on this GPU, and the reference kernel of known
+    traffic for scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    t = a.elapsed_time(b) * 1e-3 / reps
+    del src, dst
+    return {"bytes_per_launch": 2 * nbytes, "avg_launch_us": round(t * 1e6, 2),
+            "GB/s": round(2 * nbytes / t / 1e9, 1)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); "
+              "the batch shards by slot or by kv-head with no exchange on this path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from workload import configs, driver
+
+    torch.cuda.set_device(0)
+    copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
+    total_steps = args.warmup + args.steps
+    w = configs.CONFIGS[args.config](total_steps)
+    cache, inputs = driver.open_cache(w, split=args.split)
+    cap = cache.capacity
+
+    # Inputs of the timed steps, generated into HBM now.
+    need = sum(driver.prefill_bytes(w, n) for e in w.steps[args.warmup:] for n in e.insert_lens)
+    need += args.steps * w.n_layers * w.batch * (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes
+    free, _ = torch.cuda.mem_get_info()
+    if need + (2 << 30) > free:
+        sys.exit(f"timed inputs need {need / 1e9:.1f} GB, {free / 1e9:.1f} GB free: use fewer --steps")
+
+    for s in range(args.warmup):
+        driver.run_step(cache, inputs, s, w.steps[s])
+    torch.cuda.synchronize()
+
+    pre = []
+    for s in range(args.warmup, total_steps):
+        ev = w.steps[s]
+        srcs = [inputs.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+        dec = [inputs.decode(s, layer) for layer in range(w.n_layers)]
+        pre.append((srcs, dec))
+    mask_buf = torch.empty((w.batch, cap + 1), dtype=torch.uint8, device="cuda")
+    ws = cache.workspace()
+    outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=inputs.tdt, device="cuda")
+            for _ in range(2)]
+    torch.cuda.synchronize()
+
+    # Host-side bookkeeping of algorithmic bytes (lengths as the library reports them).
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    ev_attn, ev_embed, ev_evict, ev_mask = [], [], [], []
+    bytes_attn = bytes_embed = bytes_evict = 0
+    live_tokens = 0
+    t_start, t_end = E(), E()
+    torch.cuda.synchronize()
+    t_start.record()
+    for i, s in enumerate(range(args.warmup, total_steps)):
+        ev = w.steps[s]
+        srcs, dec = pre[i]
+        _, _, lens = cache.query()
+        a, b = E(), E()
+        a.record()
+        cache.evict(ev.evict, release=True)
+        b.record()
+        ev_evict.append((a, b))
+        bytes_evict += evict_bytes(w, lens, ev.evict)
+        if ev.insert:
+            a, b = E(), E()
+            a.record()
+            cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+            b.record()
+            ev_embed.append((a, b))
+            bytes_embed += embed_bytes(w, ev.insert_lens)
+        a, b = E(), E()
+        a.record()
+        cache.build_mask(out=mask_buf)
+        b.record()
+        ev_mask.append((a, b))
+        _, _, lens = cache.query()
+        step_attn = attn_bytes(w, lens)
+        for layer in range(w.n_layers):
+            q, kn, vn = dec[layer]
+            a, b = E(), E()
+            a.record()
+            cache.decode_attn(layer, q, kn, vn, out=outs[layer & 1])
+            b.record()
+            ev_attn.append((a, b))
+            bytes_attn += step_attn
+        live_tokens += sum(1 for n in lens if n > 0)
+        cache.advance()
+    t_end.record()
+    torch.cuda.synchronize()
+
+    total_ms = t_start.elapsed_time(t_end)
+    ms = lambda evs: sum(x.elapsed_time(y) for x, y in evs)
+    attn_ms, embed_ms, evict_ms, mask_ms = ms(ev_attn), ms(ev_embed), ms(ev_evict), ms(ev_mask)
+    n_attn = len(ev_attn)
+    attn_gbs = bytes_attn / (attn_ms * 1e-3) / 1e9
+    embed_gbs = bytes_embed / (embed_ms * 1e-3) / 1e9 if embed_ms > 0 else None
+    value = live_tokens / (total_ms * 1e-3)
+
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            traffic = json.load(f).get("bytes_per_launch")
+
+    result = {
+        "metric": "decode-attention query-tokens/s + achieved HBM GB/s (attn, kv_embed) at 1 GPU",
+        "value": round(value, 1),
+        "unit": "query-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded counter-based generator, values ~N(0,1))",
+        "config": {
+            "workload": f"{w.name}: {w.dtype}, {w.n_layers} layers x {w.n_q_heads} q-heads / "
+                        f"{w.n_kv_heads} kv-heads x head_dim {w.head_dim}, batch {w.batch}, "
+                        f"initial padded length {w.L0}, ring capacity {cap}, "
+                        f"{total_steps} decode steps with re-batching",
+            "global_batch": w.batch, "seq_len": w.L0, "parallelism": "none (1 GPU)",
+            "split_tokens": args.split,
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "decode_attn (attn_kernel + combine_kernel)",
+            "achieved": round(attn_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(attn_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+            "bytes_per_launch": round(bytes_attn / n_attn), "avg_launch_us": round(attn_ms / n_attn * 1e3, 2),
+        },
+        "ops": {
+            "decode_attn": {"ms_per_step": round(attn_ms / args.steps, 4), "GB/s": round(attn_gbs, 1),
+                            "query_tokens_per_s": round(live_tokens / (attn_ms * 1e-3), 1)},
+            "kv_embed": {"ms_per_step": round(embed_ms / args.steps, 4),
+                         "GB/s": round(embed_gbs, 1) if embed_gbs else None,
+                         "bytes_per_step": round(bytes_embed / args.steps)},
+            "kv_evict": {"ms_per_step": round(evict_ms / args.steps, 4),
+                         "placeholder_GB/s": round(bytes_evict / (evict_ms * 1e-3) / 1e9, 1) if evict_ms else None},
+            "build_mask": {"ms_per_step": round(mask_ms / args.steps, 4)},
+        },
+        "hbm_copy_reference": copy_ref,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
