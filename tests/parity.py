@@ -113,3 +113,124 @@ def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale
             check_ring(cache, pb, f"step {s} advance")
     cache.close()
     return worst
+
+
+# ------------------------------------------------------------ sampled mode --
+class History:
+    """Where each slot's query came from, to rebuild any row's history on the host."""
+
+    def __init__(self, w):
+        self.w = w
+        self.qid = list(range(w.batch))
+        self.plen = list(w.init_lens)
+        self.first_step = [0] * w.batch      # first decode step of the query
+
+    def insert(self, slot, qid, n, step):
+        self.qid[slot], self.plen[slot], self.first_step[slot] = qid, n, step
+
+    def row(self, slot, layer, head, step, which):
+        """Host bits [n, D] of the query's own K (which='k') or V tokens for layer/head,
+        including the token decoded at `step`."""
+        w = self.w
+        sid = gen.S_PREFILL_K if which == "k" else gen.S_PREFILL_V
+        c0, st = gen.prefill_counter(self.qid[slot], w.n_layers, w.n_kv_heads, w.head_dim,
+                                     layer0=layer, head0=head)
+        pre = gen.fill_host(w.seed, sid, w.dtype, (1, 1, self.plen[slot], w.head_dim), c0, st)[0, 0]
+        dsid = gen.S_KNEW if which == "k" else gen.S_VNEW
+        toks = []
+        for s in range(self.first_step[slot], step + 1):
+            c0, st = gen.decode_counter(s, layer, w.n_layers, w.batch, w.n_kv_heads, w.head_dim)
+            c0 += (slot * w.n_kv_heads + head) * w.head_dim
+            toks.append(gen.fill_host(w.seed, dsid, w.dtype, (1, 1, 1, w.head_dim), c0, st)[0, 0])
+        return np.concatenate([pre] + toks) if toks else pre
+
+
+def check_placeholders_outside_live(cache, fill_bits):
+    """On the GPU: a ring position holds non-placeholder bits iff it is a live token."""
+    L, base, lens = cache.query()
+    cap = cache.capacity
+    col = torch.arange(cap, device=cache.k.device)
+    logical = (col - base) % cap                                 # logical column of each physical one
+    lens_t = torch.tensor(lens, device=cache.k.device)[:, None]
+    live = (logical[None, :] < L) & (logical[None, :] >= L - lens_t) & (lens_t > 0)   # [B][cap]
+    if cache.k.dtype == torch.bfloat16:
+        idt, fill = torch.int16, int(np.array(fill_bits, np.uint16).view(np.int16))
+    else:
+        idt, fill = torch.int32, int(np.array(fill_bits, np.uint32).view(np.int32))
+    for buf in (cache.k, cache.v):
+        for layer in range(buf.shape[0]):
+            for b0 in range(0, cache.batch, 16):
+                rows = buf[layer, b0:b0 + 16].view(idt)
+                written = (rows != fill).any(dim=-1)                            # [b][H][cap]
+                want = live[b0:b0 + 16, None, :].expand_as(written)
+                if not torch.equal(written, want):
+                    raise AssertionError(f"layer {layer} rows {b0}..: placeholders and live tokens disagree")
+
+
+def run_sampled(w, sample_steps, sample_layers, n_slots=4, seed=0, split=None, capacity=None):
+    """Whole schedule on the GPU; the oracle checks metadata at every step and,
+    at the sampled (step, layer) points, whole rows of K/V (bit-exact) and the
+    attention output of every q-head of the sampled slots."""
+    rng = np.random.default_rng(seed)
+    cache, dev = driver.open_cache(w, capacity=capacity, split=split)
+    pb = O.PaddedBatch(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype,
+                       fill_bits=cache.fill_bits, materialize=False)
+    pb.embed(list(range(w.batch)), w.init_lens, [None] * w.batch, [None] * w.batch)
+    hist = History(w)
+    g = w.n_q_heads // w.n_kv_heads
+    worst, checked = 0.0, 0
+    for s, ev in enumerate(w.steps):
+        cache.evict(ev.evict, release=True)
+        pb.evict(ev.evict, release=True)
+        if ev.insert:
+            srcs = [dev.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+            cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+            pb.embed(ev.insert, ev.insert_lens, [None] * len(ev.insert), [None] * len(ev.insert))
+            for slot, q, n in zip(ev.insert, ev.insert_qids, ev.insert_lens):
+                hist.insert(slot, q, n, s)
+            del srcs
+        L, base, lens = cache.query()
+        assert (L, lens) == (pb.L, pb.lens), f"step {s}: metadata"
+        if s in sample_steps:
+            m = cache.build_mask().cpu().numpy()
+            assert np.array_equal(m, O.build_mask(pb.L, pb.lens)), f"step {s}: mask"
+        live = pb.live()
+        for layer in range(w.n_layers):
+            q, kn, vn = dev.decode(s, layer)
+            out = cache.decode_attn(layer, q, kn, vn)
+            if s not in sample_steps or layer not in sample_layers:
+                continue
+            slots = sorted(set(rng.choice(live, min(n_slots, len(live)), replace=False).tolist())
+                           | set(x for x in ev.insert if x in live))
+            qh = host_bits(q)
+            oh = O.widen(host_bits(out), w.dtype)
+            for b in slots:
+                for h in range(w.n_kv_heads):
+                    kh = hist.row(b, layer, h, s, "k")
+                    vh = hist.row(b, layer, h, s, "v")
+                    assert len(kh) == pb.lens[b] + 1
+                    # cached columns (before this step's token) of the ring, bit for bit
+                    cols = (np.arange(pb.L - pb.lens[b], pb.L) + base) % cache.capacity
+                    ring_k = host_bits(cache.k[layer, b, h, torch.as_tensor(cols, device=cache.k.device)])
+                    ring_v = host_bits(cache.v[layer, b, h, torch.as_tensor(cols, device=cache.k.device)])
+                    assert np.array_equal(ring_k, kh[:-1]) and np.array_equal(ring_v, vh[:-1]), \
+                        f"step {s} layer {layer} slot {b} head {h}: cached tokens"
+                    K, V = O.widen(kh, w.dtype), O.widen(vh, w.dtype)
+                    for gi in range(g):
+                        hq = h * g + gi
+                        want = O.attend(O.widen(qh[b, hq], w.dtype), K, V, 1.0 / math.sqrt(w.head_dim))
+                        err = float(np.max(np.abs(oh[b, hq] - want)))
+                        worst = max(worst, err)
+                        checked += 1
+                        assert err <= TOL[w.dtype], f"step {s} layer {layer} slot {b} q-head {hq}: {err}"
+            free = [b for b in range(w.batch) if pb.lens[b] == 0]
+            if free:
+                assert np.all(host_bits(out)[free] == 0)
+        cache.advance()
+        for layer in range(w.n_layers):
+            pb.decode_layer(layer, None, None, None)
+        pb.advance()
+    torch.cuda.synchronize()
+    check_placeholders_outside_live(cache, cache.fill_bits)
+    cache.close()
+    return worst, checked

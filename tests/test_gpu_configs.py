@@ -1,0 +1,41 @@
+"""The HIP path at the target configurations' full sizes (GPU), in the launch
+configuration bench.py times.  cfg2 is compared whole against the
+materialized oracle; larger ones at sampled (step, layer, slot) points (whole
+K/V rows bit-exact, every q-head's output within tolerance), with metadata at
+every step and, at the end, the placeholder invariant over the whole ring."""
+import pytest
+
+from tests import parity
+from workload import configs
+
+pytestmark = pytest.mark.gpu
+
+
+def test_cfg2_whole():
+    w = configs.cfg2()
+    print(f"[configs] cfg2 whole: B={w.batch} L0={w.L0} steps={w.n_steps}", flush=True)
+    err = parity.run(w, check_every_op=False)
+    print(f"[configs] cfg2 max abs error {err:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("name,steps,layers,kw", [
+    ("cfg3", {0, 31, 63}, {0, 17, 31}, {}),
+    ("cfg5", {0, 7, 15}, {0}, {}),
+    ("cfg5b", {0, 1, 8, 16}, {0}, {}),
+])
+def test_sampled(name, steps, layers, kw):
+    w = configs.CONFIGS[name]()
+    print(f"[configs] {name} sampled: B={w.batch} L0={w.L0} layers={w.n_layers} steps={w.n_steps}",
+          flush=True)
+    err, n = parity.run_sampled(w, steps, layers, **kw)
+    print(f"[configs] {name}: {n} outputs checked, max abs error {err:.3g}", flush=True)
+    assert n > 0
+
+
+def test_cfg4_gqa_resident_layers():
+    """Config 4's per-layer shape (GQA 64/8, B=128, L=8192) with 24 of its 80
+    layers resident -- the dense padded 80-layer cache (343.6 GB) exceeds HBM."""
+    w = configs.cfg4(n_steps=6, n_layers=24)
+    print(f"[configs] cfg4 24 layers sampled", flush=True)
+    err, n = parity.run_sampled(w, {0, 5}, {0, 23}, n_slots=3)
+    print(f"[configs] cfg4: {n} outputs checked, max abs error {err:.3g}", flush=True)

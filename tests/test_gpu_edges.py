@@ -1,0 +1,138 @@
+"""Edge cases of the HIP path (GPU): empty calls, all slots free, growth ties,
+capacity limits, split boundaries, maximum batch, placeholder poisoning, and
+the dense-tensor interop check with a stock masked attention."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.baton_oracle as O
+from paper_2410_18701_amd import baton as B
+from paper_2410_18701_amd.cache import BatonCache
+from tests import parity
+from workload import configs, driver, gen
+
+pytestmark = pytest.mark.gpu
+
+
+def scripted(name, dtype, NL, batch, Hq, Hkv, D, init_lens, steps, seed=5):
+    """A workload with a given initial batch and step list [(evict, insert, lens)]."""
+    w = configs.Workload(name, dtype, NL, batch, Hq, Hkv, D, max(init_lens), len(steps), seed=seed)
+    w.init_lens = list(init_lens)
+    qid = batch
+    for ev, ins, lens in steps:
+        w.steps.append(configs.StepEvents(sorted(ev), list(ins), list(lens), list(range(qid, qid + len(ins)))))
+        qid += len(ins)
+    return w
+
+
+def test_growth_tie_growth_by_one_and_refill():
+    """l_q == L (no growth), l_q == L + 1 (growth by one), every slot finishing
+    (L drops to 0), then a fresh batch."""
+    w = scripted("edges", "bf16", 2, 3, 4, 2, 128, [5, 9, 7], [
+        ([], [], []),                 # plain decode: L 9 -> 10, lens 6, 10, 8
+        ([1], [1], [8]),              # release to L = 8, then l_q == L: no growth
+        ([0], [0], [10]),             # L = 9 after release, l_q = 10: growth by exactly one
+        ([0, 1, 2], [], []),          # everything finishes: L = 0, a decode over an empty batch
+        ([], [0, 2], [3, 6]),         # a fresh batch
+        ([2], [1], [1]),              # a one-token query
+    ])
+    parity.run(w, split=64)
+
+
+def test_split_boundaries():
+    """Rows whose len+1 is exactly one split, one past it, and two splits."""
+    w = scripted("splits", "bf16", 1, 5, 2, 2, 64, [63, 64, 127, 128, 1], [([], [], []), ([4], [4], [191])])
+    parity.run(w, split=64)
+
+
+def test_max_batch():
+    w = configs.small("bf16", 1, B.BATON_MAX_BATCH, 1, 1, 64, L0=40, n_steps=2, n_evict=100, seed=9)
+    parity.run(w, check_every_op=False)
+
+
+@pytest.mark.parametrize("dtype,nan", [("bf16", 0x7FC1), ("f32", 0x7FC00001)])
+def test_nan_placeholders_change_nothing(dtype, nan):
+    """Placeholders are never read into arithmetic: NaN placeholders give the same
+    bits as -inf ones."""
+    w = configs.small(dtype, 1, 5, 4, 2, 64, L0=200, n_steps=3, n_evict=2, seed=12)
+    outs = {}
+    for fill in (None, nan):
+        cache, dev = driver.open_cache(w, fill_bits=fill)
+        cache.set_split_tokens(64)
+        got = []
+        for s, ev in enumerate(w.steps):
+            driver.run_step(cache, dev, s, ev, outs=got)
+        outs[fill] = [parity.host_bits(o) for (_, _, _, _, o) in got]
+        cache.close()
+    for a, b in zip(outs[None], outs[nan]):
+        assert np.array_equal(a, b)
+        assert np.all(np.isfinite(O.widen(a, dtype)))
+
+
+def test_capacity_limits_leave_state():
+    """ECAPACITY from embed and from decode, with the state (metadata and bytes) unchanged."""
+    w = scripted("cap", "bf16", 1, 2, 2, 2, 64, [10, 6], [])
+    cache = BatonCache(1, 2, 2, 2, 64, capacity=12, dtype="bf16")
+    dev = driver.DeviceInputs(w)
+    srcs = [dev.prefill(q, w.init_lens[q]) for q in range(2)]
+    cache.embed([0, 1], w.init_lens, [s[0] for s in srcs], [s[1] for s in srcs])
+    big = dev.prefill(7, 12)
+    cache.evict([1], release=True)
+    torch.cuda.synchronize()
+    before = (cache.query(), parity.host_bits(cache.k).copy(), parity.host_bits(cache.v).copy())
+    with pytest.raises(B.BatonError) as e:
+        cache.embed([1], [12], [big[0]], [big[1]])        # 12 + 1 > 12
+    assert e.value.status == B.BATON_ECAPACITY
+    torch.cuda.synchronize()
+    assert cache.query() == before[0]
+    assert np.array_equal(parity.host_bits(cache.k), before[1])
+    assert np.array_equal(parity.host_bits(cache.v), before[2])
+    ok = dev.prefill(8, 11)
+    cache.embed([1], [11], [ok[0]], [ok[1]])              # 11 + 1 == 12 fits
+    q, kn, vn = dev.decode(0, 0)
+    cache.decode_attn(0, q, kn, vn)
+    cache.advance()                                       # L = 12 = capacity
+    with pytest.raises(B.BatonError) as e:
+        cache.decode_attn(0, q, kn, vn)                   # no room for column 12
+    assert e.value.status == B.BATON_ECAPACITY
+    with pytest.raises(B.BatonError) as e:
+        cache.advance()
+    assert e.value.status == B.BATON_ESTATE
+    cache.evict([0], release=True)                        # frees room: L = len of slot 1 = 12 -> still full
+    cache.evict([1], release=True)
+    assert cache.query()[0] == 0
+    parity.check_placeholders_outside_live(cache, cache.fill_bits)
+    cache.close()
+
+
+def test_dense_interop_with_stock_masked_attention():
+    """With 0.0 placeholders the aligned window is a dense padded tensor: a stock
+    masked attention (torch SDPA, CPU fp32, additive -inf mask from build_mask)
+    over it reproduces the kernel's outputs."""
+    w = configs.small("bf16", 1, 6, 8, 2, 128, L0=300, n_steps=2, n_evict=2, seed=17)
+    cache, dev = driver.open_cache(w, fill_bits=0x0000)
+    g = w.n_q_heads // w.n_kv_heads
+    for s, ev in enumerate(w.steps):
+        cache.evict(ev.evict, release=True)
+        srcs = [dev.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+        cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+        mask = cache.build_mask()
+        L, base, lens = cache.query()
+        q, kn, vn = dev.decode(s, 0)
+        out = cache.decode_attn(0, q, kn, vn)
+        idx = (torch.arange(L + 1, device="cuda") + base) % cache.capacity   # window incl. column L
+        K = cache.k[0].index_select(2, idx).float().cpu()                     # [B][Hkv][L+1][D]
+        V = cache.v[0].index_select(2, idx).float().cpu()
+        K = K.repeat_interleave(g, dim=1).contiguous()
+        V = V.repeat_interleave(g, dim=1).contiguous()
+        add = torch.zeros(mask.shape, dtype=torch.float32)
+        add[mask.cpu() == 0] = float("-inf")
+        live = [b for b in range(w.batch) if lens[b] > 0]
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            q.float().cpu()[live, :, None, :], K[live], V[live], attn_mask=add[live][:, None, None, :])
+        got = out.float().cpu()[live]
+        assert torch.max(torch.abs(got - ref[:, :, 0, :])).item() <= 2e-2
+        cache.advance()
+    cache.close()
