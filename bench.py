@@ -17,6 +17,7 @@ roofline (decode attention, HBM-bound), per-op HBM GB/s, and the CPU oracle
 timed on a bounded sample on this host.
 """
 import argparse
+import gc
 import json
 import os
 import sys
@@ -34,7 +35,9 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=60)
     p.add_argument("--warmup", type=int, default=4)
-    p.add_argument("--config", default="cfg3", choices=["cfg2", "cfg3", "cfg5"])
+    p.add_argument("--config", default="cfg3", choices=["cfg2", "cfg3", "cfg4", "cfg5", "cfg5b"])
+    p.add_argument("--layers", type=int, default=None,
+                   help="resident layers (config 4's 80-layer padded cache exceeds HBM; default 24 there)")
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=16, help="layers of step 0 the oracle runs")
@@ -150,7 +153,12 @@ def main():
     torch.cuda.set_device(0)
     copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
     total_steps = args.warmup + args.steps
-    w = configs.CONFIGS[args.config](total_steps)
+    if args.config == "cfg4":
+        w = configs.cfg4(total_steps, n_layers=args.layers or 24)
+    else:
+        w = configs.CONFIGS[args.config](total_steps)
+        if args.layers:
+            raise SystemExit("--layers applies to cfg4 only")
     cache, inputs = driver.open_cache(w, split=args.split)
     cap = cache.capacity
 
@@ -177,11 +185,20 @@ def main():
             for _ in range(2)]
     torch.cuda.synchronize()
 
-    # Host-side bookkeeping of algorithmic bytes (lengths as the library reports them).
-    E = lambda: torch.cuda.Event(enable_timing=True)
+    # Every event of the timed region exists (and has been recorded once) before
+    # it starts, and the collector is off, so the host never stalls the stream.
+    n_ev = 2 * args.steps * (3 + w.n_layers) + 2
+    pool = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+    for e in pool:
+        e.record()
+    torch.cuda.synchronize()
+    pool_it = iter(pool)
+    E = lambda: next(pool_it)
     ev_attn, ev_embed, ev_evict, ev_mask = [], [], [], []
     bytes_attn = bytes_embed = bytes_evict = 0
     live_tokens = 0
+    gc.collect()
+    gc.disable()
     t_start, t_end = E(), E()
     torch.cuda.synchronize()
     t_start.record()
@@ -221,6 +238,7 @@ def main():
         cache.advance()
     t_end.record()
     torch.cuda.synchronize()
+    gc.enable()
 
     total_ms = t_start.elapsed_time(t_end)
     ms = lambda evs: sum(x.elapsed_time(y) for x, y in evs)

@@ -11,7 +11,12 @@
 #include "baton.h"
 #include "common.hpp"
 #include "decode_attn.hpp"
+#include "decode_attn_mfma.hpp"
 #include "kv_ops.hpp"
+
+#ifndef BATON_GQA_MFMA
+#define BATON_GQA_MFMA 1   // grouped-query bf16 attention on the matrix cores
+#endif
 
 static_assert(BATON_MAX_BATCH == baton::kMetaThreads, "meta kernel covers every slot");
 
@@ -30,6 +35,7 @@ struct baton_cache {
   const void* meta_ws = nullptr;
   bool meta_valid = false;
   int32_t n_items = 0;
+  int32_t n_multi = 0;     // rows with several items
 };
 
 namespace {
@@ -51,10 +57,10 @@ int64_t ring(int64_t x, int64_t cap) {
   return x < 0 ? x + cap : x;
 }
 
-// Workspace layout: [lens: batch][item_start: batch + 1] [items: max_items]
-// [partials: n_kv_heads][max_items][group][head_dim + 4].
+// Workspace layout: [items: max_items] [rows with several items: batch]
+// [partials: n_kv_heads][max_items][group][head_dim + 4] fp32.
 struct WsLayout {
-  size_t lens_off, start_off, items_off, partial_off, total;
+  size_t items_off, multi_off, partial_off, total;
   int64_t max_items;
 };
 
@@ -63,10 +69,9 @@ WsLayout ws_layout(const baton_cache* c) {
   const int64_t B = c->d.batch;
   w.max_items = B * ((c->d.capacity + c->split - 1) / c->split);
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-  w.lens_off = 0;
-  w.start_off = up(w.lens_off + sizeof(int32_t) * B);
-  w.items_off = up(w.start_off + sizeof(int32_t) * (B + 1));
-  w.partial_off = up(w.items_off + sizeof(int2) * w.max_items);
+  w.items_off = 0;
+  w.multi_off = up(w.items_off + sizeof(baton::Item) * w.max_items);
+  w.partial_off = up(w.multi_off + sizeof(int4) * B);
   w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * w.max_items * c->group *
                                    (c->d.head_dim + 4));
   return w;
@@ -131,36 +136,47 @@ baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hip
 }
 
 // ---------------------------------------------------------------- attention --
+#ifndef BATON_ATTN_U_SMALL_G
+#define BATON_ATTN_U_SMALL_G 8   // token rows per lane group per iteration, G <= 2
+#endif
+#ifndef BATON_ATTN_U_LARGE_G
+#define BATON_ATTN_U_LARGE_G 4   // G = 4, 8
+#endif
+
 template <typename T, int D, int G>
-void launch_attn_t(const baton::AttnArgs& a, int n_items, int batch, int hkv, hipStream_t s) {
-  constexpr int U = G <= 2 ? 8 : 4;
-  if (n_items > 0)
+void launch_attn_t(const baton::AttnArgs& a, int n_items, int n_multi, int hkv, hipStream_t s) {
+  constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
+  if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= 2)
+    hipLaunchKernelGGL((baton::attn_mfma_kernel<D, G>), dim3(n_items, hkv), dim3(baton::kWave), 0,
+                       s, a);
+  else
     hipLaunchKernelGGL((baton::attn_kernel<T, D, G, U>), dim3(n_items, hkv), dim3(baton::kWave), 0,
                        s, a);
-  hipLaunchKernelGGL((baton::combine_kernel<T, D, G>), dim3(batch, hkv), dim3(baton::kWave), 0, s,
-                     a);
+  if (n_multi > 0)
+    hipLaunchKernelGGL((baton::combine_kernel<T, D, G>), dim3(n_multi, hkv * G), dim3(baton::kWave),
+                       0, s, a);
 }
 
 template <typename T, int D>
-bool launch_attn_d(int g, const baton::AttnArgs& a, int n_items, int batch, int hkv,
+bool launch_attn_d(int g, const baton::AttnArgs& a, int n_items, int n_multi, int hkv,
                    hipStream_t s) {
   switch (g) {
-    case 1: launch_attn_t<T, D, 1>(a, n_items, batch, hkv, s); return true;
-    case 2: launch_attn_t<T, D, 2>(a, n_items, batch, hkv, s); return true;
-    case 4: launch_attn_t<T, D, 4>(a, n_items, batch, hkv, s); return true;
-    case 8: launch_attn_t<T, D, 8>(a, n_items, batch, hkv, s); return true;
+    case 1: launch_attn_t<T, D, 1>(a, n_items, n_multi, hkv, s); return true;
+    case 2: launch_attn_t<T, D, 2>(a, n_items, n_multi, hkv, s); return true;
+    case 4: launch_attn_t<T, D, 4>(a, n_items, n_multi, hkv, s); return true;
+    case 8: launch_attn_t<T, D, 8>(a, n_items, n_multi, hkv, s); return true;
     default: return false;
   }
 }
 
-bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, int n_items, hipStream_t s) {
-  const int B = c->d.batch, H = c->d.n_kv_heads;
+bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, hipStream_t s) {
+  const int I = c->n_items, M = c->n_multi, H = c->d.n_kv_heads;
   if (c->d.dtype == BATON_F32) {
-    if (c->d.head_dim == 64) return launch_attn_d<baton::F32Tag, 64>(c->group, a, n_items, B, H, s);
-    return launch_attn_d<baton::F32Tag, 128>(c->group, a, n_items, B, H, s);
+    if (c->d.head_dim == 64) return launch_attn_d<baton::F32Tag, 64>(c->group, a, I, M, H, s);
+    return launch_attn_d<baton::F32Tag, 128>(c->group, a, I, M, H, s);
   }
-  if (c->d.head_dim == 64) return launch_attn_d<baton::BF16Tag, 64>(c->group, a, n_items, B, H, s);
-  return launch_attn_d<baton::BF16Tag, 128>(c->group, a, n_items, B, H, s);
+  if (c->d.head_dim == 64) return launch_attn_d<baton::BF16Tag, 64>(c->group, a, I, M, H, s);
+  return launch_attn_d<baton::BF16Tag, 128>(c->group, a, I, M, H, s);
 }
 
 int default_split(const baton_cache_desc& d) { return d.dtype == BATON_F32 ? 128 : 256; }
@@ -196,6 +212,8 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   const int32_t g = d.n_q_heads / d.n_kv_heads;
   if (g != 1 && g != 2 && g != 4 && g != 8) return BATON_EDTYPE;
   if (!d.k || !d.v || !aligned16(d.k) || !aligned16(d.v)) return BATON_EINVAL;
+  // a row of the ring is addressed with 32-bit byte offsets
+  if (d.capacity * d.head_dim * (d.dtype == BATON_F32 ? 4 : 2) >= (int64_t(1) << 31)) return BATON_EINVAL;
   baton_cache* c = new (std::nothrow) baton_cache();
   if (!c) return BATON_EINVAL;
   c->d = d;
@@ -332,18 +350,20 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     std::memset(&m, 0, sizeof(m));
     m.batch = c->d.batch;
     m.split = c->split;
-    int64_t items = 0;
+    int64_t items = 0, multi = 0;   // as meta_kernel counts them: one item for a free slot
     for (int32_t b = 0; b < c->d.batch; ++b) {
       m.lens[b] = c->lens[b];
-      if (c->lens[b] > 0) items += (c->lens[b] + c->split) / c->split;
+      const int64_t cnt = c->lens[b] > 0 ? (c->lens[b] + c->split) / c->split : 1;
+      items += cnt;
+      multi += cnt > 1;
     }
     hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, m,
-                       reinterpret_cast<int32_t*>(wsb + w.lens_off),
-                       reinterpret_cast<int32_t*>(wsb + w.start_off),
-                       reinterpret_cast<int2*>(wsb + w.items_off));
+                       reinterpret_cast<baton::Item*>(wsb + w.items_off),
+                       reinterpret_cast<int4*>(wsb + w.multi_off));
     const baton_status st = hip_status(hipGetLastError());
     if (st != BATON_OK) return st;
     c->n_items = (int32_t)items;
+    c->n_multi = (int32_t)multi;
     c->meta_ws = ws;
     c->meta_valid = true;
   }
@@ -356,9 +376,8 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.knew = static_cast<const uint32_t*>(k_new);
   a.vnew = static_cast<const uint32_t*>(v_new);
   a.out = static_cast<uint32_t*>(out);
-  a.lens = reinterpret_cast<const int32_t*>(wsb + w.lens_off);
-  a.item_start = reinterpret_cast<const int32_t*>(wsb + w.start_off);
-  a.items = reinterpret_cast<const int2*>(wsb + w.items_off);
+  a.items = reinterpret_cast<const baton::Item*>(wsb + w.items_off);
+  a.multi = reinterpret_cast<const int4*>(wsb + w.multi_off);
   a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
   a.cap = c->d.capacity;
   a.base = c->base;
@@ -370,7 +389,7 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.n_items = c->n_items;
   const float sc = scale == 0.f ? 1.0f / std::sqrt((float)c->d.head_dim) : scale;
   a.qscale = sc * 1.4426950408889634f;
-  if (!launch_attn(c, a, c->n_items, stream)) return BATON_EDTYPE;
+  if (!launch_attn(c, a, stream)) return BATON_EDTYPE;
   const baton_status st = hip_status(hipGetLastError());
   if (st != BATON_OK) return st;
   c->layer_done[layer] = 1;

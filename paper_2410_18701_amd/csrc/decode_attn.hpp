@@ -9,17 +9,26 @@
 // over LPT = D*elem/16 lanes (16 bytes each), so one wave instruction reads
 // TPI = 64/LPT whole token rows; each of those TPI lane groups keeps its own
 // online-softmax state (max m, sum l, weighted values acc) over the tokens it
-// reads, and the groups merge once at the end of the item.  Items of a row
-// that has one item write the output; otherwise they write (m, l, acc)
-// partials that the combine kernel merges with the log-sum-exp rescale.
-// Exponentials are base 2 with scale*log2(e) folded into q.
+// reads, and the groups merge once at the end of the item.  An item that is
+// its row's only one writes the output; otherwise it writes an (m, l, acc)
+// partial and combine_kernel merges the row's partials with the log-sum-exp
+// rescale.  (Merging in the attention kernel by the last item to arrive would
+// need an agent-scope release per item, which on gfx950 writes back the L2;
+// measured, that costs far more than the second launch.)  A free slot gets one
+// item that writes zeros.  Exponentials are base 2 with scale*log2(e) folded
+// into q.
 #pragma once
 
 #include "common.hpp"
 
+#ifndef BATON_ATTN_NT
+#define BATON_ATTN_NT 1      // non-temporal K/V loads (streamed once per layer and step)
+#endif
+
 namespace baton {
 
 constexpr int kMetaThreads = 512;   // == BATON_MAX_BATCH
+
 
 struct MetaArgs {
   int32_t batch;
@@ -27,29 +36,45 @@ struct MetaArgs {
   int32_t lens[kMetaThreads];
 };
 
-// Builds the per-step work list in the workspace: lens[b], item_start[b]
-// (exclusive prefix of items per row, batch + 1 entries) and items[] = (b, c).
-__global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, int32_t* ws_lens,
-                                                            int32_t* ws_item_start,
-                                                            int2* ws_items) {
+// One work item: the tokens [t_begin, t_end) of slot b's row (n = len_b
+// cached tokens, -1 for a free slot), and where the row's items start and how
+// many there are.
+struct Item {
+  int4 span;     // (b, t_begin, t_end, n)
+  int4 row;      // (first item of the row, items of the row, 0, 0)
+};
+
+// Builds the per-step work list in the workspace: one descriptor per item, so
+// that an item needs a single load to start, and the list of rows with
+// several items (first item, item count, slot) for combine_kernel.
+__global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, Item* ws_items,
+                                                            int4* ws_multi) {
   __shared__ int32_t scan[kMetaThreads];
+  __shared__ int32_t scan_multi[kMetaThreads];
   const int b = threadIdx.x;
   const int32_t n = b < a.batch ? a.lens[b] : 0;
-  const int32_t cnt = n > 0 ? (n + a.split) / a.split : 0;   // ceil((n + 1) / split)
+  const int32_t cnt = b < a.batch ? (n > 0 ? (n + a.split) / a.split : 1) : 0;  // ceil((n+1)/split)
   scan[b] = cnt;
+  scan_multi[b] = cnt > 1 ? 1 : 0;
   __syncthreads();
   for (int off = 1; off < kMetaThreads; off <<= 1) {
     const int32_t add = b >= off ? scan[b - off] : 0;
+    const int32_t add_m = b >= off ? scan_multi[b - off] : 0;
     __syncthreads();
     scan[b] += add;
+    scan_multi[b] += add_m;
     __syncthreads();
   }
-  const int32_t excl = scan[b] - cnt;
+  const int32_t first = scan[b] - cnt;
   if (b < a.batch) {
-    ws_lens[b] = n;
-    ws_item_start[b] = excl;
-    if (b == a.batch - 1) ws_item_start[a.batch] = scan[b];
-    for (int32_t c = 0; c < cnt; ++c) ws_items[excl + c] = make_int2(b, c);
+    for (int32_t c = 0; c < cnt; ++c) {
+      Item it;
+      it.span = n > 0 ? make_int4(b, c * a.split, min((c + 1) * a.split, n + 1), n)
+                      : make_int4(b, 0, 0, -1);
+      it.row = make_int4(first, cnt, 0, 0);
+      ws_items[first + c] = it;
+    }
+    if (cnt > 1) ws_multi[scan_multi[b] - 1] = make_int4(first, cnt, b, 0);
   }
 }
 
@@ -61,9 +86,8 @@ struct AttnArgs {
   const uint32_t* knew;      // [batch][n_kv_heads][D]
   const uint32_t* vnew;
   uint32_t* out;             // [batch][n_q_heads][D]
-  const int32_t* lens;       // workspace
-  const int32_t* item_start;
-  const int2* items;
+  const Item* items;         // workspace
+  const int4* multi;         // rows with several items: (first item, count, slot)
   float* partial;            // [n_kv_heads][n_items][G][D + 4]
   int64_t cap, base, L;
   int32_t layer, batch, n_kv_heads, split, n_items;
@@ -79,8 +103,127 @@ struct Geometry {
   static_assert(kLpt >= 4 && kLpt <= 32, "token row must span 4..32 lanes");
 };
 
+// Word 3 of a raw buffer resource on gfx9-family GPUs (no format conversion).
+constexpr int32_t kBufferWord3 = 0x00020000;
+
+__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  // aux bit 1: non-temporal (streamed once per layer and step)
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, BATON_ATTN_NT ? 2 : 0));
+}
+
+// Online-softmax update of one lane group with U token rows per lane group:
+// scores by a dot product over the group's lanes (DPP), running max m, sum l
+// and value accumulator acc rescaled by exp2(m_old - m_new).
+template <typename T, int G, int U, int EPL, int LPT>
+__device__ __forceinline__ void online_update(const u32x4 (&kw)[U], const u32x4 (&vw)[U],
+                                              const bool (&valid)[U], const float (&qf)[G][EPL],
+                                              float (&m)[G], float (&l)[G], float (&acc)[G][EPL]) {
+  float s[U][G];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float kf[EPL];
+    Lane16<T>::widen(kw[u], kf);
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      float d = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) d = fmaf(qf[gi][e], kf[e], d);
+      d = group_sum<LPT>(d);
+      s[u][gi] = valid[u] ? d : -INFINITY;
+    }
+  }
+#pragma unroll
+  for (int gi = 0; gi < G; ++gi) {
+    float mt = m[gi];
+#pragma unroll
+    for (int u = 0; u < U; ++u) mt = fmaxf(mt, s[u][gi]);
+    const float ref = mt == -INFINITY ? 0.f : mt;
+    const float alpha = exp2f(m[gi] - ref);
+    l[gi] *= alpha;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[gi][e] *= alpha;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float p = exp2f(s[u][gi] - ref);
+      l[gi] += p;
+      float vf[EPL];
+      Lane16<T>::widen(vw[u], vf);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[gi][e] = fmaf(p, vf[e], acc[gi][e]);
+    }
+    m[gi] = mt;
+  }
+}
+
+// Log-sum-exp merge of a row's partial records (m, l, acc[D]) for one query
+// head: lane i reads record i's m (64 at a time) and the wave reduces the max;
+// then every lane accumulates its D/64 elements over the records, eight
+// records' loads in flight at a time, with the weights broadcast from the
+// lanes that computed them.
+template <typename T, int D, int G>
+__device__ __forceinline__ void merge_row(const float* base, int32_t count, uint32_t* outw,
+                                          int lane) {
+  constexpr int REC = D + 4;
+  constexpr int PER = D / kWave;   // elements per lane (1 or 2)
+  constexpr int64_t STRIDE = (int64_t)G * REC;
+  float mm = -INFINITY;
+  for (int32_t i0 = 0; i0 < count; i0 += kWave) {
+    const int32_t i = i0 + lane;
+    mm = fmaxf(mm, i < count ? base[i * STRIDE + D] : -INFINITY);
+  }
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) mm = fmaxf(mm, __shfl_xor(mm, off, kWave));
+  float l = 0.f, o[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) o[e] = 0.f;
+  for (int32_t i0 = 0; i0 < count; i0 += kWave) {
+    const int32_t i = i0 + lane;
+    float w = 0.f;
+    if (i < count) {
+      const float mi = base[i * STRIDE + D];
+      w = mi == -INFINITY ? 0.f : exp2f(mi - mm);
+      l += w * base[i * STRIDE + D + 1];
+    }
+    const int32_t nrec = min(kWave, count - i0);
+    for (int32_t j0 = 0; j0 < nrec; j0 += 8) {
+      float v[8][PER];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float* rec = base + (int64_t)(i0 + min(j0 + j, nrec - 1)) * STRIDE;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) v[j][e] = rec[lane * PER + e];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float wj = j0 + j < nrec ? __shfl(w, j0 + j, kWave) : 0.f;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) o[e] = fmaf(wj, v[j][e], o[e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) l += __shfl_xor(l, off, kWave);
+  const float inv = 1.f / l;
+  if constexpr (T::kBytes == 4) {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) outw[lane * PER + e] = __float_as_uint(o[e] * inv);
+  } else {
+    uint16_t* out16 = reinterpret_cast<uint16_t*>(outw);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) out16[lane * PER + e] = (uint16_t)f32_to_bf16_rne(o[e] * inv);
+  }
+}
+
+#ifndef BATON_ATTN_WAVES_PER_EU
+#define BATON_ATTN_WAVES_PER_EU 0   // 0: compiler's choice
+#endif
+
 template <typename T, int D, int G, int U>
-__global__ void __launch_bounds__(kWave) attn_kernel(const AttnArgs a) {
+__global__ void __launch_bounds__(kWave)
+#if BATON_ATTN_WAVES_PER_EU > 0
+__attribute__((amdgpu_waves_per_eu(BATON_ATTN_WAVES_PER_EU)))
+#endif
+attn_kernel(const AttnArgs a) {
   using Geo = Geometry<T, D>;
   constexpr int EPL = Geo::kEpl, LPT = Geo::kLpt, TPI = Geo::kTpi, VPT = Geo::kVpt;
   constexpr int REC = D + 4;   // floats per partial record
@@ -90,17 +233,32 @@ __global__ void __launch_bounds__(kWave) attn_kernel(const AttnArgs a) {
   const int r = lane / LPT;        // token row within an instruction
   const int cl = lane % LPT;       // 16-byte slice of the row
 
-  const int2 bc = a.items[item];
-  const int b = bc.x, c = bc.y;
-  const int32_t n = a.lens[b];     // cached tokens; token n is the current one
-  const int32_t t_begin = c * a.split;
-  const int32_t t_end = min(t_begin + a.split, n + 1);
-  const bool whole_row = (t_begin == 0) && (t_end == n + 1);
+  const int4 it = a.items[item].span;
+  const int4 rw = a.items[item].row;
+  const int b = it.x;
+  const int32_t t_begin = it.y, t_end = it.z;
+  const int32_t n = it.w;          // cached tokens; token n is the current one
+  uint32_t* outw = a.out + (((int64_t)b * a.n_kv_heads + h) * G) * (D * T::kBytes / 4);
+  if (n < 0) {                     // free slot: the output rows are zero
+    if (r == 0) {
+#pragma unroll
+      for (int gi = 0; gi < G; ++gi)
+        reinterpret_cast<u32x4*>(outw)[gi * VPT + cl] = u32x4{0, 0, 0, 0};
+    }
+    return;
+  }
+  const bool whole_row = rw.y == 1;
 
   const int64_t row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
-  const u32x4* Krow = reinterpret_cast<const u32x4*>(a.k) + row * a.cap * VPT;
-  const u32x4* Vrow = reinterpret_cast<const u32x4*>(a.v) + row * a.cap * VPT;
-  const int64_t start = ring_add(a.base, a.L - n, a.cap);   // physical column of token 0
+  constexpr uint32_t ROWB = VPT * 16;                     // bytes per token row
+  const uint32_t ring_bytes = (uint32_t)a.cap * ROWB;
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.k) + row * a.cap * VPT * 4, 0,
+                                        ring_bytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc(a.v + row * a.cap * VPT * 4, 0, ring_bytes, kBufferWord3);
+  const uint32_t start = (uint32_t)ring_add(a.base, a.L - n, a.cap);   // ring column of token 0
+  const uint32_t cap = (uint32_t)a.cap;
   const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
   const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
 
@@ -123,68 +281,51 @@ __global__ void __launch_bounds__(kWave) attn_kernel(const AttnArgs a) {
     for (int e = 0; e < EPL; ++e) acc[gi][e] = 0.f;
   }
 
-  for (int32_t tt = t_begin; tt < t_end; tt += TPI * U) {
-    u32x4 kw[U], vw[U];
-    bool valid[U];
+  // Cached tokens of the item, software-pipelined: the 2U loads of the next
+  // iteration are in flight while the current one is computed.  A token past
+  // the end gets an offset beyond the buffer's range, which the hardware
+  // answers with zeros (its score is then set to -inf).
+  const int32_t c_end = min(t_end, n);
+  constexpr int32_t STEP = TPI * U;
+  auto issue = [&](int32_t tt, u32x4 (&kw)[U], u32x4 (&vw)[U], bool (&valid)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int32_t t = tt + u * TPI + r;
-      valid[u] = t < t_end;
-      kw[u] = u32x4{0, 0, 0, 0};
-      vw[u] = u32x4{0, 0, 0, 0};
-      if (valid[u]) {
-        if (t < n) {
-          const int64_t col = ring_add(start, t, a.cap);
-          kw[u] = __builtin_nontemporal_load(Krow + col * VPT + cl);
-          vw[u] = __builtin_nontemporal_load(Vrow + col * VPT + cl);
-        } else {
-          kw[u] = knew[cl];
-          vw[u] = vnew[cl];
-        }
-      }
+      valid[u] = t < c_end;
+      uint32_t col = start + (uint32_t)t;
+      col = col >= cap ? col - cap : col;
+      const uint32_t off = valid[u] ? col * ROWB + cl * 16u : 0x80000000u;
+      kw[u] = load16(rk, off);
+      vw[u] = load16(rv, off);
     }
-    float s[U][G];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float kf[EPL];
-      Lane16<T>::widen(kw[u], kf);
-#pragma unroll
-      for (int gi = 0; gi < G; ++gi) {
-        float d = 0.f;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) d = fmaf(qf[gi][e], kf[e], d);
-        d = group_sum<LPT>(d);
-        s[u][gi] = valid[u] ? d : -INFINITY;
-      }
-    }
-#pragma unroll
-    for (int gi = 0; gi < G; ++gi) {
-      float mt = m[gi];
-#pragma unroll
-      for (int u = 0; u < U; ++u) mt = fmaxf(mt, s[u][gi]);
-      const float ref = mt == -INFINITY ? 0.f : mt;
-      const float alpha = exp2f(m[gi] - ref);
-      l[gi] *= alpha;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[gi][e] *= alpha;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float p = exp2f(s[u][gi] - ref);
-        l[gi] += p;
-        float vf[EPL];
-        Lane16<T>::widen(vw[u], vf);
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[gi][e] = fmaf(p, vf[e], acc[gi][e]);
-      }
-      m[gi] = mt;
+  };
+  if (t_begin < c_end) {
+    u32x4 ka[U], va[U], kb[U], vb[U];
+    bool la[U], lb[U];
+    issue(t_begin, ka, va, la);
+    for (int32_t tt = t_begin;;) {
+      if (tt + STEP < c_end) issue(tt + STEP, kb, vb, lb);
+      online_update<T, G, U, EPL, LPT>(ka, va, la, qf, m, l, acc);
+      tt += STEP;
+      if (tt >= c_end) break;
+      if (tt + STEP < c_end) issue(tt + STEP, ka, va, la);
+      online_update<T, G, U, EPL, LPT>(kb, vb, lb, qf, m, l, acc);
+      tt += STEP;
+      if (tt >= c_end) break;
     }
   }
 
-  // The current token goes into the cache as column L (once per row).
-  if (n >= t_begin && n < t_end && (n - t_begin) % TPI == r) {
-    const int64_t col = ring_add(start, n, a.cap);
-    reinterpret_cast<u32x4*>(a.k_w)[row * a.cap * VPT + col * VPT + cl] = knew[cl];
-    reinterpret_cast<u32x4*>(a.v)[row * a.cap * VPT + col * VPT + cl] = vnew[cl];
+  // The current token: read from k_new / v_new by lane group 0, appended to
+  // the cache as column L by the item that holds it (once per row).
+  if (n >= t_begin && n < t_end) {
+    u32x4 kw[1] = {knew[cl]}, vw[1] = {vnew[cl]};
+    bool valid[1] = {r == 0};
+    online_update<T, G, 1, EPL, LPT>(kw, vw, valid, qf, m, l, acc);
+    if (r == 0) {
+      const uint32_t col = (uint32_t)ring_add(start, n, a.cap);
+      reinterpret_cast<u32x4*>(a.k_w)[row * a.cap * VPT + (int64_t)col * VPT + cl] = kw[0];
+      reinterpret_cast<u32x4*>(a.v)[row * a.cap * VPT + (int64_t)col * VPT + cl] = vw[0];
+    }
   }
 
   // Merge the TPI lane groups.
@@ -207,21 +348,24 @@ __global__ void __launch_bounds__(kWave) attn_kernel(const AttnArgs a) {
     }
   }
 
-  if (r != 0) return;
   if (whole_row) {
+    if (r == 0) {
 #pragma unroll
-    for (int gi = 0; gi < G; ++gi) {
-      const float inv = 1.f / l[gi];
-      float o[EPL];
+      for (int gi = 0; gi < G; ++gi) {
+        const float inv = 1.f / l[gi];
+        float o[EPL];
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) o[e] = acc[gi][e] * inv;
-      reinterpret_cast<u32x4*>(a.out)[(((int64_t)b * a.n_kv_heads + h) * G + gi) * VPT + cl] =
-          Lane16<T>::narrow(o);
+        for (int e = 0; e < EPL; ++e) o[e] = acc[gi][e] * inv;
+        reinterpret_cast<u32x4*>(outw)[gi * VPT + cl] = Lane16<T>::narrow(o);
+      }
     }
-  } else {
+    return;
+  }
+  float* part = a.partial + ((int64_t)h * a.n_items) * G * REC;
+  if (r == 0) {
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
-      float* rec = a.partial + (((int64_t)h * a.n_items + item) * G + gi) * REC;
+      float* rec = part + ((int64_t)item * G + gi) * REC;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) rec[cl * EPL + e] = acc[gi][e];
       if (cl == 0) {
@@ -232,45 +376,16 @@ __global__ void __launch_bounds__(kWave) attn_kernel(const AttnArgs a) {
   }
 }
 
-// One wave per (slot, kv-head): zeros for a free slot, nothing for a slot with
-// one item, the log-sum-exp merge of the partials otherwise.
+// One wave per (row with several items, query head): the log-sum-exp merge
+// of the row's partials.
 template <typename T, int D, int G>
 __global__ void __launch_bounds__(kWave) combine_kernel(const AttnArgs a) {
   constexpr int REC = D + 4;
-  constexpr int PER = D / kWave;   // elements per lane (1 or 2)
-  const int b = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-  const int32_t i0 = a.item_start[b], i1 = a.item_start[b + 1];
-  if (i1 - i0 == 1) return;
-  for (int gi = 0; gi < G; ++gi) {
-    float o[PER];
-#pragma unroll
-    for (int e = 0; e < PER; ++e) o[e] = 0.f;
-    if (i1 > i0) {
-      const float* base = a.partial + ((int64_t)h * a.n_items * G + gi) * REC;
-      float mm = -INFINITY;
-      for (int32_t i = i0; i < i1; ++i) mm = fmaxf(mm, base[(int64_t)i * G * REC + D]);
-      float l = 0.f;
-      for (int32_t i = i0; i < i1; ++i) {
-        const float* rec = base + (int64_t)i * G * REC;
-        const float w = rec[D] == -INFINITY ? 0.f : exp2f(rec[D] - mm);
-        l += w * rec[D + 1];
-#pragma unroll
-        for (int e = 0; e < PER; ++e) o[e] = fmaf(w, rec[lane * PER + e], o[e]);
-      }
-      const float inv = 1.f / l;
-#pragma unroll
-      for (int e = 0; e < PER; ++e) o[e] *= inv;
-    }
-    const int64_t obase = (((int64_t)b * a.n_kv_heads + h) * G + gi) * D + lane * PER;
-    if constexpr (T::kBytes == 4) {
-#pragma unroll
-      for (int e = 0; e < PER; ++e) a.out[obase + e] = __float_as_uint(o[e]);
-    } else {
-      uint16_t* out16 = reinterpret_cast<uint16_t*>(a.out);
-#pragma unroll
-      for (int e = 0; e < PER; ++e) out16[obase + e] = (uint16_t)f32_to_bf16_rne(o[e]);
-    }
-  }
+  const int4 mr = a.multi[blockIdx.x];
+  const int hq = blockIdx.y, h = hq / G, gi = hq % G;
+  uint32_t* outw = a.out + ((int64_t)mr.z * a.n_kv_heads * G + hq) * (D * T::kBytes / 4);
+  const float* base = a.partial + (((int64_t)h * a.n_items + mr.x) * G + gi) * REC;
+  merge_row<T, D, G>(base, mr.y, outw, threadIdx.x);
 }
 
 }  // namespace baton

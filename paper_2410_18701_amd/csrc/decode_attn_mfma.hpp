@@ -1,0 +1,240 @@
+// Grouped-query decode attention on the matrix cores (bf16, G = 2, 4 or 8
+// query heads per kv head).  With G query heads sharing a key row the work is
+// G times denser than multi-head attention, enough to make the VALU the
+// limiter; here QK^T and PV run as v_mfma_f32_16x16x32_bf16 tiles.
+//
+// Per iteration a wave takes 32 tokens of its work item as two 16-token tiles.
+//  * QK^T: A = 16 key rows x 32 d (lane l supplies row l%16, d-group l/16),
+//    B = the G query heads padded to 16 columns, D = head_dim/32 MFMAs.
+//    The A row of lane l is token tau(l%16) with tau(4g + r) = g + 4r, so the
+//    result row 4g + r (held by lane group g, register r) is token g + 4r.
+//  * softmax: lane l holds head l%16's scores of 8 tokens; the running max is
+//    shared by the four lane groups (all of them accumulate into the same
+//    output tile), exponentials are base 2, P is rounded to bf16.
+//  * PV: A = P (16 heads x 32 tokens, lane l: head l%16, its own 8 tokens as
+//    k = 8*(l/16) + e), B = V (32 tokens x 16 d) per 16-column slice of
+//    head_dim.  V is staged in LDS row by row (coalesced global loads) and read
+//    back transposed, 2 bytes per lane; the token order above makes the four
+//    lane groups of one read hit consecutive rows, i.e. disjoint banks.
+// The current token (k_new, v_new) is a one-token tile of its own.  Partial
+// records and outputs have the layout of the VALU kernel, so combine_kernel
+// merges both.
+#pragma once
+
+#include "common.hpp"
+#include "decode_attn.hpp"
+
+namespace baton {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& w) { return __builtin_bit_cast(bf16x8, w); }
+
+template <int D>
+struct MfmaGeo {
+  static constexpr int kVpt = D / 8;              // 16-byte vectors per token row
+  static constexpr int kTpiV = kWave / kVpt;      // token rows per V load instruction
+  static constexpr int kVLoads = 32 / kTpiV;      // V loads per lane per 32 tokens
+  static constexpr int kKk = D / 32;              // QK MFMAs per tile
+  static constexpr int kDt = D / 16;              // PV MFMAs (16-column slices)
+  static constexpr int kLdsRow = D * 2 + 32;      // padded LDS row (bank spread)
+};
+
+// One 32-token block: scores, online softmax, PV.  kA/kB: the two key tiles
+// (A operands), vw: this lane's V vectors, valid_mask: bit t set when token t
+// (0..31) of the block takes part.
+template <int D, int G>
+__device__ __forceinline__ void mfma_block(const u32x4 (&kA)[D / 32], const u32x4 (&kB)[D / 32],
+                                           const u32x4 (&vw)[MfmaGeo<D>::kVLoads],
+                                           const bf16x8 (&qb)[D / 32], uint32_t valid_mask,
+                                           float qscale, uint8_t* lds, float& m, float& lsum,
+                                           f32x4 (&o)[D / 16], int lane) {
+  using Geo = MfmaGeo<D>;
+  const int g4 = lane / 16, c16 = lane % 16;
+  // Stage V rows in LDS (row t holds token t of the block).
+#pragma unroll
+  for (int u = 0; u < Geo::kVLoads; ++u) {
+    const int t = u * Geo::kTpiV + lane / Geo::kVpt;
+    *reinterpret_cast<u32x4*>(lds + t * Geo::kLdsRow + (lane % Geo::kVpt) * 16) = vw[u];
+  }
+  // Scores of the two tiles: s[r] for token g4 + 4r, s[4 + r] for token 16 + g4 + 4r.
+  f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < Geo::kKk; ++kk) {
+    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kA[kk]), qb[kk], sa, 0, 0, 0);
+    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kB[kk]), qb[kk], sb, 0, 0, 0);
+  }
+  float s[8];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    s[r] = ((valid_mask >> (g4 + 4 * r)) & 1u) ? sa[r] * qscale : -INFINITY;
+    s[4 + r] = ((valid_mask >> (16 + g4 + 4 * r)) & 1u) ? sb[r] * qscale : -INFINITY;
+  }
+  float mx = s[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  const float mn = fmaxf(m, mx);
+  const float ref = mn == -INFINITY ? 0.f : mn;
+  const float alpha = exp2f(m - ref);
+  bf16x8 pa;
+  float psum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 pb = (__bf16)exp2f(s[e] - ref);
+    pa[e] = pb;
+    psum += (float)pb;
+  }
+  lsum = lsum * alpha + psum;
+  m = mn;
+  // Rescale the output rows this lane holds (heads 4*g4 + r).
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float ar = __shfl(alpha, 4 * g4 + r, kWave);
+#pragma unroll
+    for (int dt = 0; dt < Geo::kDt; ++dt) o[dt][r] *= ar;
+  }
+  // PV: B operand = V[token(k)][16*dt + c16], k = 8*g4 + e.
+#pragma unroll
+  for (int dt = 0; dt < Geo::kDt; ++dt) {
+    bf16x8 vb;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int t = e < 4 ? g4 + 4 * e : 16 + g4 + 4 * (e - 4);
+      vb[e] = *reinterpret_cast<const __bf16*>(lds + t * Geo::kLdsRow + (16 * dt + c16) * 2);
+    }
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
+  }
+}
+
+#ifndef BATON_MFMA_WAVES_PER_EU
+#define BATON_MFMA_WAVES_PER_EU 0   // 0: compiler's choice
+#endif
+
+template <int D, int G>
+__global__ void __launch_bounds__(kWave)
+#if BATON_MFMA_WAVES_PER_EU > 0
+__attribute__((amdgpu_waves_per_eu(BATON_MFMA_WAVES_PER_EU)))
+#endif
+attn_mfma_kernel(const AttnArgs a) {
+  using Geo = MfmaGeo<D>;
+  constexpr int VPT = Geo::kVpt, KK = Geo::kKk, DT = Geo::kDt, REC = D + 4;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[32 * Geo::kLdsRow];
+  const int item = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int g4 = lane / 16, c16 = lane % 16;
+
+  const int4 it = a.items[item].span;
+  const int4 rw = a.items[item].row;
+  const int b = it.x;
+  const int32_t t_begin = it.y, t_end = it.z, n = it.w;
+  uint32_t* outw = a.out + (((int64_t)b * a.n_kv_heads + h) * G) * (D / 2);
+  if (n < 0) {                       // free slot: zero output rows
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi)
+      if (lane < VPT) reinterpret_cast<u32x4*>(outw)[gi * VPT + lane] = u32x4{0, 0, 0, 0};
+    return;
+  }
+  const int64_t row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
+  constexpr uint32_t ROWB = VPT * 16;
+  const uint32_t ring_bytes = (uint32_t)a.cap * ROWB;
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.k) + row * a.cap * VPT * 4, 0,
+                                        ring_bytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc(a.v + row * a.cap * VPT * 4, 0, ring_bytes, kBufferWord3);
+  const uint32_t start = (uint32_t)ring_add(a.base, a.L - n, a.cap);
+  const uint32_t cap = (uint32_t)a.cap;
+
+  // Query heads as the B operand: column c16 = head c16 (zero beyond G).
+  bf16x8 qb[KK];
+  const u32x4* qrow = reinterpret_cast<const u32x4*>(a.q) + (((int64_t)b * a.n_kv_heads + h) * G) * VPT;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    const u32x4 w = c16 < G ? qrow[c16 * VPT + kk * 4 + g4] : u32x4{0, 0, 0, 0};
+    qb[kk] = as_bf16x8(w);
+  }
+
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int32_t c_end = min(t_end, n);
+  const int tau = (c16 / 4) + 4 * (c16 % 4);   // token of this lane's key row in a tile
+  auto koff = [&](int32_t t, int kk) -> uint32_t {
+    if (t >= c_end) return 0x80000000u;           // out of range: zeros
+    uint32_t col = start + (uint32_t)t;
+    col = col >= cap ? col - cap : col;
+    return col * ROWB + (uint32_t)(kk * 4 + g4) * 16u;
+  };
+  for (int32_t tt = t_begin; tt < c_end; tt += 32) {
+    u32x4 kA[KK], kB[KK], vw[Geo::kVLoads];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      kA[kk] = load16(rk, koff(tt + tau, kk));
+      kB[kk] = load16(rk, koff(tt + 16 + tau, kk));
+    }
+#pragma unroll
+    for (int u = 0; u < Geo::kVLoads; ++u) {
+      const int32_t t = tt + u * Geo::kTpiV + lane / VPT;
+      uint32_t col = start + (uint32_t)t;
+      col = col >= cap ? col - cap : col;
+      vw[u] = load16(rv, t < c_end ? col * ROWB + (lane % VPT) * 16u : 0x80000000u);
+    }
+    const int32_t nvalid = min(32, c_end - tt);
+    const uint32_t mask = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+    mfma_block<D, G>(kA, kB, vw, qb, mask, a.qscale, lds, m, lsum, o, lane);
+  }
+
+  // The current token, a one-token tile read from k_new / v_new, and its append.
+  if (n >= t_begin && n < t_end) {
+    const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
+    const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
+    u32x4 kA[KK], kB[KK], vw[Geo::kVLoads];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      kA[kk] = tau == 0 ? knew[kk * 4 + g4] : u32x4{0, 0, 0, 0};
+      kB[kk] = u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < Geo::kVLoads; ++u)
+      vw[u] = (u == 0 && lane < VPT) ? vnew[lane] : u32x4{0, 0, 0, 0};
+    mfma_block<D, G>(kA, kB, vw, qb, 1u, a.qscale, lds, m, lsum, o, lane);
+    if (lane < VPT) {
+      const uint32_t col = (uint32_t)ring_add(start, n, a.cap);
+      reinterpret_cast<u32x4*>(a.k_w)[row * a.cap * VPT + (int64_t)col * VPT + lane] = knew[lane];
+      reinterpret_cast<u32x4*>(a.v)[row * a.cap * VPT + (int64_t)col * VPT + lane] = vnew[lane];
+    }
+  }
+
+  // Row sums over the four lane groups; lane l's output rows are heads 4*g4 + r.
+  lsum += __shfl_xor(lsum, 16, kWave);
+  lsum += __shfl_xor(lsum, 32, kWave);
+  const bool whole_row = rw.y == 1;
+  float* part = a.partial + ((int64_t)h * a.n_items) * G * REC;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int head = 4 * g4 + r;
+    const float lr = __shfl(lsum, head, kWave);
+    const float mr = __shfl(m, head, kWave);
+    if (head >= G) continue;
+    if (whole_row) {
+      const float inv = 1.f / lr;
+      uint16_t* out16 = reinterpret_cast<uint16_t*>(outw) + head * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) out16[16 * dt + c16] = (uint16_t)f32_to_bf16_rne(o[dt][r] * inv);
+    } else {
+      float* rec = part + ((int64_t)item * G + head) * REC;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) rec[16 * dt + c16] = o[dt][r];
+      if (c16 == 0) {
+        rec[D] = mr;
+        rec[D + 1] = lr;
+      }
+    }
+  }
+}
+
+}  // namespace baton
