@@ -40,11 +40,13 @@ def parse():
                    help="resident layers (config 4's 80-layer padded cache exceeds HBM; default 24 there)")
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=16, help="layers of step 0 the oracle runs")
+    p.add_argument("--cpu-layers", type=int, default=20, help="layers of step 0 the oracle runs")
     p.add_argument("--copy-bytes", type=int, default=2 << 30,
                    help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
-    p.add_argument("--traffic", default=None,
-                   help="JSON file with rocprofv3-derived HBM bytes per attention launch")
+    p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "decode_attn_cfg3_traffic.json"),
+                   help="rocprofv3-derived HBM bytes per decode_attn launch (FETCH_SIZE/WRITE_SIZE, "
+                        "scaled by a copy of known size); used only for the workload it was measured "
+                        "on and while the kernel sources are unchanged")
     return p.parse_args()
 
 
@@ -115,6 +117,17 @@ def cpu_baseline(w, n_layers):
             "sample": f"step 0 of {w.name} (evict, embed, mask, attention, advance) for layers "
                       f"0..{n_layers - 1}, one layer at a time, numpy float64 on 1 thread; "
                       f"{elapsed:.1f} s measured, scaled by {w.n_layers}/{n_layers} layers"}
+
+
+def kernel_sources_sha256():
+    """Hash of the decode-attention kernel sources: counters taken on other
+    sources do not describe this kernel."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("common.hpp", "decode_attn.hpp", "decode_attn_mfma.hpp", "baton.hip"):
+        with open(os.path.join(ROOT, "paper_2410_18701_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def copy_probe(nbytes, reps=5):
@@ -249,9 +262,12 @@ def main():
     value = live_tokens / (total_ms * 1e-3)
 
     traffic = None
-    if args.traffic and os.path.exists(args.traffic):
+    if args.traffic and os.path.exists(args.traffic) and args.config == "cfg3" and args.split is None \
+            and (args.steps, args.warmup) == (60, 4):
         with open(args.traffic) as f:
-            traffic = json.load(f).get("bytes_per_launch")
+            rec = json.load(f)
+        if rec.get("kernel_sources_sha256") == kernel_sources_sha256():
+            traffic = rec.get("bytes_per_launch")
 
     result = {
         "metric": "decode-attention query-tokens/s + achieved HBM GB/s (attn, kv_embed) at 1 GPU",

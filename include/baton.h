@@ -142,7 +142,8 @@ baton_status baton_kv_embed(baton_cache* cache, const int32_t* slots, int32_t n,
 baton_status baton_build_mask(const baton_cache* cache, uint8_t* mask, int64_t ld,
                               hipStream_t stream);
 
-/* Bytes of device workspace baton_decode_attn needs for this cache (fixed for its lifetime). */
+/* Bytes of device workspace baton_decode_attn needs for this cache (fixed until
+   baton_set_split_tokens changes the split setting). */
 size_t baton_decode_attn_workspace_bytes(const baton_cache* cache);
 
 /*
@@ -188,7 +189,9 @@ baton_status baton_cache_query(const baton_cache* cache, int64_t* L, int64_t* ba
 
 /*
  * Tuning: tokens per split of a row in baton_decode_attn (a multiple of 64,
- * 64 .. 4096).  Changes baton_decode_attn_workspace_bytes; only between steps.
+ * 64 .. 4096), or 0 (the default) to let each step choose from its total
+ * number of cached tokens (256 .. 1024).  Changes
+ * baton_decode_attn_workspace_bytes; only between steps.
  * Errors: EINVAL (out of range), ESTATE (inside a decode step).
  */
 baton_status baton_set_split_tokens(baton_cache* cache, int32_t tokens);

@@ -25,7 +25,8 @@ struct baton_cache {
   int32_t esz;             // bytes per element
   int32_t vpt;             // 16-byte vectors per token row
   int32_t group;           // q-heads per kv-head
-  int32_t split;           // tokens per attention work item
+  int32_t split;           // tokens per attention work item; 0: chosen per step
+  int32_t step_split = 0;  // the split of the current step's work list
   int64_t L = 0;           // padded length
   int64_t base = 0;        // physical column of logical column 0
   std::vector<int32_t> lens;
@@ -57,6 +58,11 @@ int64_t ring(int64_t x, int64_t cap) {
   return x < 0 ? x + cap : x;
 }
 
+// Automatic split: enough items to fill the GPU about twice over at the
+// occupancy of these kernels, never smaller than 256 tokens (per-item set-up
+// and partial records) nor larger than 1024 (the merge and the tail).
+constexpr int64_t kAutoSplitMin = 256, kAutoSplitMax = 1024, kAutoItems = 8192;
+
 // Workspace layout: [items: max_items] [rows with several items: batch]
 // [partials: n_kv_heads][max_items][group][head_dim + 4] fp32.
 struct WsLayout {
@@ -67,7 +73,8 @@ struct WsLayout {
 WsLayout ws_layout(const baton_cache* c) {
   WsLayout w;
   const int64_t B = c->d.batch;
-  w.max_items = B * ((c->d.capacity + c->split - 1) / c->split);
+  const int64_t smin = c->split > 0 ? c->split : kAutoSplitMin;   // most items a row can have
+  w.max_items = B * ((c->d.capacity + smin - 1) / smin);
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   w.items_off = 0;
   w.multi_off = up(w.items_off + sizeof(baton::Item) * w.max_items);
@@ -179,7 +186,16 @@ bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, hipStream_t s) 
   return launch_attn_d<baton::BF16Tag, 128>(c->group, a, I, M, H, s);
 }
 
-int default_split(const baton_cache_desc& d) { return d.dtype == BATON_F32 ? 128 : 256; }
+
+int32_t auto_split(const baton_cache* c) {
+  int64_t rows_tokens = 0;
+  for (int32_t b = 0; b < c->d.batch; ++b)
+    if (c->lens[b] > 0) rows_tokens += c->lens[b] + 1;
+  rows_tokens *= c->d.n_kv_heads;
+  int64_t s = (rows_tokens + kAutoItems - 1) / kAutoItems;
+  s = (s + 63) / 64 * 64;
+  return (int32_t)std::min(kAutoSplitMax, std::max(kAutoSplitMin, s));
+}
 
 }  // namespace
 
@@ -220,7 +236,7 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   c->esz = d.dtype == BATON_F32 ? 4 : 2;
   c->vpt = d.head_dim * c->esz / 16;
   c->group = g;
-  c->split = default_split(d);
+  c->split = 0;
   c->lens.assign(d.batch, 0);
   c->layer_done.assign(d.n_layers, 0);
   if (!(flags & BATON_CREATE_ASSUME_FILLED)) {
@@ -349,11 +365,12 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     baton::MetaArgs m;
     std::memset(&m, 0, sizeof(m));
     m.batch = c->d.batch;
-    m.split = c->split;
+    c->step_split = c->split > 0 ? c->split : auto_split(c);
+    m.split = c->step_split;
     int64_t items = 0, multi = 0;   // as meta_kernel counts them: one item for a free slot
     for (int32_t b = 0; b < c->d.batch; ++b) {
       m.lens[b] = c->lens[b];
-      const int64_t cnt = c->lens[b] > 0 ? (c->lens[b] + c->split) / c->split : 1;
+      const int64_t cnt = c->lens[b] > 0 ? (c->lens[b] + m.split) / m.split : 1;
       items += cnt;
       multi += cnt > 1;
     }
@@ -385,7 +402,7 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.layer = layer;
   a.batch = c->d.batch;
   a.n_kv_heads = c->d.n_kv_heads;
-  a.split = c->split;
+  a.split = c->step_split;
   a.n_items = c->n_items;
   const float sc = scale == 0.f ? 1.0f / std::sqrt((float)c->d.head_dim) : scale;
   a.qscale = sc * 1.4426950408889634f;
@@ -418,7 +435,7 @@ baton_status baton_cache_query(const baton_cache* c, int64_t* L, int64_t* base, 
 }
 
 baton_status baton_set_split_tokens(baton_cache* c, int32_t tokens) {
-  if (!c || tokens < 64 || tokens > 4096 || tokens % 64) return BATON_EINVAL;
+  if (!c || (tokens != 0 && (tokens < 64 || tokens > 4096 || tokens % 64))) return BATON_EINVAL;
   if (c->n_done) return BATON_ESTATE;
   c->split = tokens;
   c->meta_valid = false;
