@@ -17,6 +17,9 @@
 #ifndef BATON_GQA_MFMA
 #define BATON_GQA_MFMA 1   // grouped-query bf16 attention on the matrix cores
 #endif
+#ifndef BATON_MFMA_MIN_GROUP
+#define BATON_MFMA_MIN_GROUP 2   // smallest q-heads per kv-head that takes the matrix-core kernel
+#endif
 
 static_assert(BATON_MAX_BATCH == baton::kMetaThreads, "meta kernel covers every slot");
 
@@ -153,7 +156,7 @@ baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hip
 template <typename T, int D, int G>
 void launch_attn_t(const baton::AttnArgs& a, int n_items, int n_multi, int hkv, hipStream_t s) {
   constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
-  if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= 2)
+  if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= BATON_MFMA_MIN_GROUP)
     hipLaunchKernelGGL((baton::attn_mfma_kernel<D, G>), dim3(n_items, hkv), dim3(baton::kWave), 0,
                        s, a);
   else
