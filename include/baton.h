@@ -131,6 +131,24 @@ baton_status baton_kv_embed(baton_cache* cache, const int32_t* slots, int32_t n,
                             const void* const* k_src, const void* const* v_src, hipStream_t stream);
 
 /*
+ * Copy live queries' cached keys/values out of the batch (sec. 4.3: preemptive
+ * scheduling stores the lowest-priority query's keys and values aside and
+ * re-inserts it later; batch-size scaling moves queries' keys and values to
+ * host memory and back).  slots: host array of n distinct live slots; k_dst,
+ * v_dst: host arrays of n device pointers, each receiving
+ * [n_layers][n_kv_heads][len][head_dim] contiguous elements (len = the slot's
+ * current length, baton_cache_query), 16-byte aligned -- the layout
+ * baton_kv_embed takes, so baton_kv_embed(slot', len, k_dst, v_dst) re-inserts
+ * the query into any free slot with its cache bit for bit.  The batch is not
+ * changed; preempting a query is extract, then baton_kv_evict.
+ * Errors: EINVAL (n < 0, null arrays or pointers, misaligned pointer, slot out
+ * of range, duplicate), ESLOT (a slot is free), ESTATE (inside a decode step),
+ * EHIP.
+ */
+baton_status baton_kv_extract(const baton_cache* cache, const int32_t* slots, int32_t n,
+                              void* const* k_dst, void* const* v_dst, hipStream_t stream);
+
+/*
  * The 0-1 attention mask of the current step (sec. 2.1, "Batch-wise inference";
  * sec. 4.1: a column of ones for the current token, zero rows for finished
  * queries; sec. 4.2: zeros over the grown front of existing rows).  Writes

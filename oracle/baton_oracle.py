@@ -200,6 +200,21 @@ class PaddedBatch:
                 self.hist_k[s] = np.array(ks, copy=True)
                 self.hist_v[s] = np.array(vs, copy=True)
 
+    def extract(self, slots):
+        """A live query's keys and values read off its aligned row (the columns
+        after its placeholders), to be stored aside and re-embedded later
+        (sec. 4.3, preemptive scheduling and batch-size scaling).  Changes nothing."""
+        self._check_between_steps()
+        if len(set(slots)) != len(slots) or any(not 0 <= s < self.B for s in slots):
+            raise ValueError("bad slot list")
+        if any(self.lens[s] == 0 for s in slots):
+            raise LookupError("extracting a free slot")
+        out = []
+        for s in slots:
+            n = self.lens[s]
+            out.append((self.K[:, s, :, self.L - n:].copy(), self.V[:, s, :, self.L - n:].copy()))
+        return out
+
     def mask(self):
         return build_mask(self.L, self.lens)
 

@@ -54,6 +54,7 @@ def lib():
         L.baton_cache_destroy.argtypes = [vp]
         L.baton_kv_evict.argtypes = [vp, P(i32), i32, u32, vp]
         L.baton_kv_embed.argtypes = [vp, P(i32), i32, P(i32), P(vp), P(vp), vp]
+        L.baton_kv_extract.argtypes = [vp, P(i32), i32, P(vp), P(vp), vp]
         L.baton_build_mask.argtypes = [vp, vp, i64, vp]
         L.baton_decode_attn_workspace_bytes.argtypes = [vp]
         L.baton_decode_attn_workspace_bytes.restype = ctypes.c_size_t
@@ -64,6 +65,7 @@ def lib():
         L.baton_status_string.argtypes = [st]
         L.baton_status_string.restype = ctypes.c_char_p
         for name in ("baton_cache_create", "baton_cache_destroy", "baton_kv_evict", "baton_kv_embed",
+                     "baton_kv_extract",
                      "baton_build_mask", "baton_decode_attn", "baton_step_advance",
                      "baton_cache_query", "baton_set_split_tokens"):
             getattr(L, name).restype = st
@@ -126,6 +128,15 @@ def baton_kv_embed(cache, slots, lens, k_src, v_src, stream=None):
     ks = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in k_src])
     vs = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in v_src])
     _check(lib().baton_kv_embed(cache, s_arr, n, l_arr, ks, vs, _stream(stream)), "baton_kv_embed")
+
+
+def baton_kv_extract(cache, slots, k_dst, v_dst, stream=None):
+    s_arr, n = _i32s(slots)
+    if len(k_dst) != n or len(v_dst) != n:
+        raise ValueError("slots, k_dst and v_dst must have the same length")
+    ks = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in k_dst])
+    vs = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in v_dst])
+    _check(lib().baton_kv_extract(cache, s_arr, n, ks, vs, _stream(stream)), "baton_kv_extract")
 
 
 def baton_build_mask(cache, mask, ld, stream=None):

@@ -64,6 +64,18 @@ class BatonCache:
         B.baton_kv_embed(self.handle, slots, lens, k_src, v_src,
                          stream if stream is not None else _cur_stream())
 
+    def extract(self, slots, stream=None):
+        """The slots' cached K and V as new device tensors [n_layers][n_kv_heads][len][head_dim]."""
+        import torch
+        lens = self.query()[2]
+        ks, vs = [], []
+        for s in slots:
+            shape = (self.n_layers, self.n_kv_heads, max(lens[s], 0), self.head_dim)
+            ks.append(torch.empty(shape, dtype=self.k.dtype, device=self.k.device))
+            vs.append(torch.empty(shape, dtype=self.k.dtype, device=self.k.device))
+        B.baton_kv_extract(self.handle, slots, ks, vs, stream if stream is not None else _cur_stream())
+        return ks, vs
+
     def build_mask(self, out=None, stream=None):
         import torch
         L = self.query()[0]

@@ -91,12 +91,13 @@ WsLayout ws_layout(const baton_cache* c) {
 struct Seg {
   int32_t slot, len;
   int64_t col0;
-  const void* ks;
+  const void* ks;   // contiguous side (null: placeholders)
   const void* vs;
 };
 
 template <int VPT>
-baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs, hipStream_t s) {
+baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs, bool extract,
+                             hipStream_t s) {
   constexpr int TT = baton::kCopyThreads * baton::kCopyVecs / VPT;
   for (size_t off = 0; off < segs.size(); off += baton::kMaxSegs) {
     SegArgs a;
@@ -108,6 +109,7 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
     a.batch = c->d.batch;
     a.n_kv_heads = c->d.n_kv_heads;
     a.fill_word = fill_word(c);
+    a.extract = extract ? 1 : 0;
     const size_t n = std::min<size_t>(baton::kMaxSegs, segs.size() - off);
     int64_t tiles = 0;
     int32_t used = 0;
@@ -119,8 +121,8 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
       a.len[used] = g.len;
       a.col0[used] = g.col0;
       a.tiles_per_row[used] = tpr;
-      a.ksrc[used] = static_cast<const uint32_t*>(g.ks);
-      a.vsrc[used] = static_cast<const uint32_t*>(g.vs);
+      a.kext[used] = static_cast<uint32_t*>(const_cast<void*>(g.ks));
+      a.vext[used] = static_cast<uint32_t*>(const_cast<void*>(g.vs));
       tiles += (int64_t)tpr * 2 * c->d.n_layers * c->d.n_kv_heads;
       a.tile_end[used] = tiles;
       ++used;
@@ -136,11 +138,12 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
   return BATON_OK;
 }
 
-baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hipStream_t s) {
+baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hipStream_t s,
+                         bool extract = false) {
   switch (c->vpt) {
-    case 8: return launch_segs_vpt<8>(c, segs, s);
-    case 16: return launch_segs_vpt<16>(c, segs, s);
-    case 32: return launch_segs_vpt<32>(c, segs, s);
+    case 8: return launch_segs_vpt<8>(c, segs, extract, s);
+    case 16: return launch_segs_vpt<16>(c, segs, extract, s);
+    case 32: return launch_segs_vpt<32>(c, segs, extract, s);
     default: return BATON_EDTYPE;
   }
 }
@@ -330,6 +333,29 @@ baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, con
   for (int32_t i = 0; i < n; ++i) c->lens[slots[i]] = lens[i];
   c->meta_valid = false;
   return BATON_OK;
+}
+
+baton_status baton_kv_extract(const baton_cache* c, const int32_t* slots, int32_t n, void* const* k_dst,
+                              void* const* v_dst, hipStream_t stream) {
+  if (!c || n < 0) return BATON_EINVAL;
+  if (n > 0 && (!slots || !k_dst || !v_dst)) return BATON_EINVAL;
+  if (c->n_done) return BATON_ESTATE;
+  std::vector<uint8_t> seen(c->d.batch, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = slots[i];
+    if (s < 0 || s >= c->d.batch || seen[s]) return BATON_EINVAL;
+    if (!k_dst[i] || !v_dst[i] || !aligned16(k_dst[i]) || !aligned16(v_dst[i])) return BATON_EINVAL;
+    seen[s] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i)
+    if (c->lens[slots[i]] == 0) return BATON_ESLOT;
+  std::vector<Seg> segs;
+  segs.reserve(n);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = slots[i], len = c->lens[s];
+    segs.push_back({s, len, ring(c->base + c->L - len, c->d.capacity), k_dst[i], v_dst[i]});
+  }
+  return launch_segs(c, segs, stream, /*extract=*/true);
 }
 
 baton_status baton_build_mask(const baton_cache* c, uint8_t* mask, int64_t ld, hipStream_t stream) {

@@ -1,5 +1,5 @@
-// KV-cache shaping kernels: placeholder fill, end-aligned embed / evict scrub,
-// attention-mask build.  Pure data movement: every kernel streams 16-byte
+// KV-cache shaping kernels: placeholder fill, end-aligned embed / evict scrub /
+// extract, attention-mask build.  Pure data movement: every kernel streams 16-byte
 // vectors per lane with non-temporal stores (the data is not re-read before it
 // leaves the caches).
 #pragma once
@@ -14,22 +14,25 @@ constexpr int kCopyVecs = 4;   // 16-byte vectors per thread per tile
 
 // Work of one launch: up to kMaxSegs row sets.  Segment i covers, in every
 // layer and kv-head and for both K and V, `len[i]` tokens of slot `slot[i]`
-// starting at physical ring column `col0[i]`; with a source it copies
-// src[i][layer][head][0:len][:] there, without one it writes the placeholder.
+// starting at physical ring column `col0[i]`.  With `extract` clear, it copies
+// the contiguous buffer ext[i][layer][head][0:len][:] there, or writes the
+// placeholder when ext[i] is null; with `extract` set it copies those ring
+// columns out into ext[i].
 struct SegArgs {
   uint32_t* k;              // ring buffers, viewed as 32-bit words
   uint32_t* v;
   int64_t cap;              // ring columns
   int32_t n_layers, batch, n_kv_heads;
   int32_t n_segs;
+  int32_t extract;          // 1: ring -> ext, 0: ext (or placeholder) -> ring
   uint32_t fill_word;       // placeholder bits replicated to a 32-bit word
   int32_t slot[kMaxSegs];
   int32_t len[kMaxSegs];
   int32_t tiles_per_row[kMaxSegs];
   int64_t col0[kMaxSegs];
   int64_t tile_end[kMaxSegs];           // inclusive prefix of tiles over segments
-  const uint32_t* ksrc[kMaxSegs];       // null: write placeholders
-  const uint32_t* vsrc[kMaxSegs];
+  uint32_t* kext[kMaxSegs];             // contiguous side; null: placeholders
+  uint32_t* vext[kMaxSegs];
 };
 
 // VPT = 16-byte vectors per token row (head_dim * elem_bytes / 16).  One block
@@ -52,21 +55,35 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
   const int32_t t0 = tile * TT;
   const int32_t nt = min(TT, len - t0);
 
-  u32x4* dst = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
+  u32x4* ring = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
                (((int64_t)layer * a.batch + a.slot[i]) * a.n_kv_heads + h) * a.cap * VPT;
-  const uint32_t* srcw = which ? a.vsrc[i] : a.ksrc[i];
-  const u32x4* src = srcw ? reinterpret_cast<const u32x4*>(srcw) +
-                                (((int64_t)layer * a.n_kv_heads + h) * len + t0) * VPT
-                          : nullptr;
+  u32x4* ext = reinterpret_cast<u32x4*>(which ? a.vext[i] : a.kext[i]);
+  if (ext) ext += (((int64_t)layer * a.n_kv_heads + h) * len + t0) * VPT;
   const int64_t c0 = ring_add(a.col0[i], t0, a.cap);
 
   u32x4 val[kCopyVecs];
   const u32x4 fill = {a.fill_word, a.fill_word, a.fill_word, a.fill_word};
+  if (a.extract) {
+#pragma unroll
+    for (int r = 0; r < kCopyVecs; ++r) {
+      const int idx = threadIdx.x + r * kCopyThreads;
+      if (idx < nt * VPT) {
+        const int t = idx / VPT, e = idx - (idx / VPT) * VPT;
+        val[r] = __builtin_nontemporal_load(ring + ring_add(c0, t, a.cap) * VPT + e);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kCopyVecs; ++r) {
+      const int idx = threadIdx.x + r * kCopyThreads;
+      if (idx < nt * VPT) __builtin_nontemporal_store(val[r], ext + idx);
+    }
+    return;
+  }
 #pragma unroll
   for (int r = 0; r < kCopyVecs; ++r) {
     const int idx = threadIdx.x + r * kCopyThreads;
     val[r] = fill;
-    if (src && idx < nt * VPT) val[r] = __builtin_nontemporal_load(src + idx);
+    if (ext && idx < nt * VPT) val[r] = __builtin_nontemporal_load(ext + idx);
   }
 #pragma unroll
   for (int r = 0; r < kCopyVecs; ++r) {
@@ -74,7 +91,7 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
     if (idx < nt * VPT) {
       const int t = idx / VPT, e = idx - (idx / VPT) * VPT;
       const int64_t col = ring_add(c0, t, a.cap);
-      __builtin_nontemporal_store(val[r], dst + col * VPT + e);
+      __builtin_nontemporal_store(val[r], ring + col * VPT + e);
     }
   }
 }

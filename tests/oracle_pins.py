@@ -367,3 +367,37 @@ ALL_PINS = [pin_attention_worked, pin_attention_closed_forms, pin_attention_sdpa
             pin_attention_permutation, pin_insertion_replay, pin_gqa_mapping,
             pin_isolation_invariant, pin_layout_invariants, pin_embed_order_and_release,
             pin_brute_force_small, pin_placeholder_poison, pin_error_paths]
+
+
+def pin_preemption_round_trip(O):
+    """Sec. 4.3 preemption: a query stored aside (extract), evicted, and embedded
+    again into another slot later computes what it would have computed in place:
+    same inputs, bit-identical output; and what extract returns is its own history."""
+    import copy
+    rng = np.random.default_rng(31)
+    NL, B, Hq, Hkv, D = 2, 4, 4, 2, 8
+
+    def bits(shape):
+        return rng.standard_normal(shape).astype(np.float32).view(np.uint32)
+
+    pb = O.PaddedBatch(NL, B, Hq, Hkv, D, O.F32)
+    lens = [5, 9, 3]
+    pb.embed([0, 1, 2], lens, [bits((NL, Hkv, n, D)) for n in lens], [bits((NL, Hkv, n, D)) for n in lens])
+    for _ in range(2):
+        for layer in range(NL):
+            pb.decode_layer(layer, bits((B, Hq, D)), bits((B, Hkv, D)), bits((B, Hkv, D)))
+        pb.advance()
+    q, kn, vn = bits((B, Hq, D)), bits((B, Hkv, D)), bits((B, Hkv, D))
+    stay = copy.deepcopy(pb)
+    want = stay.decode_layer(0, q, kn, vn)[1]
+    (k1, v1), = pb.extract([1])
+    assert np.array_equal(k1, pb.hist_k[1]) and np.array_equal(v1, pb.hist_v[1])
+    pb.evict([1], release=True)
+    pb.embed([3], [k1.shape[2]], [k1], [v1])
+    q2, kn2, vn2 = q.copy(), kn.copy(), vn.copy()
+    q2[3], kn2[3], vn2[3] = q[1], kn[1], vn[1]
+    got = pb.decode_layer(0, q2, kn2, vn2)[3]
+    assert np.array_equal(got, want)
+
+
+ALL_PINS.append(pin_preemption_round_trip)

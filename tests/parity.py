@@ -234,3 +234,74 @@ def run_sampled(w, sample_steps, sample_layers, n_slots=4, seed=0, split=None, c
     check_placeholders_outside_live(cache, cache.fill_bits)
     cache.close()
     return worst, checked
+
+
+# ---------------------------------------------------------- scripted mode --
+def run_script(shape, ops, seed=3, capacity=64, split=None):
+    """A scripted sequence on a small batch, GPU and materialized oracle in
+    lockstep, everything compared after every operation.
+
+    shape: (dtype, n_layers, batch, n_q_heads, n_kv_heads, head_dim).  ops:
+      ("embed", slots, lens, qids)   prefilled queries from the generator
+      ("evict", slots)               with release
+      ("extract", slots, tag)        store the slots' K/V aside (GPU and oracle)
+      ("embed_saved", slots, tag)    re-insert stored queries into these slots
+      ("step", s)                    mask, every layer with step-s inputs, advance
+    """
+    dtype, NL, B, Hq, Hkv, D = shape
+    from workload.configs import Workload
+    w = Workload("script", dtype, NL, B, Hq, Hkv, D, 1, 0, seed=seed)
+    cache = driver.BatonCache(NL, B, Hq, Hkv, D, capacity, dtype=dtype)
+    if split is not None:
+        cache.set_split_tokens(split)
+    dev = driver.DeviceInputs(w)
+    pb = O.PaddedBatch(NL, B, Hq, Hkv, D, dtype, fill_bits=cache.fill_bits)
+    saved_gpu, saved_cpu = {}, {}
+    worst = 0.0
+    for op in ops:
+        kind = op[0]
+        if kind == "embed":
+            _, slots, lens, qids = op
+            srcs = [dev.prefill(q, n) for q, n in zip(qids, lens)]
+            cache.embed(slots, lens, [x[0] for x in srcs], [x[1] for x in srcs])
+            hs = [(gen.prefill_host(w.seed, "k", q, NL, Hkv, n, D, dtype),
+                   gen.prefill_host(w.seed, "v", q, NL, Hkv, n, D, dtype)) for q, n in zip(qids, lens)]
+            pb.embed(slots, lens, [h[0] for h in hs], [h[1] for h in hs])
+        elif kind == "evict":
+            cache.evict(op[1], release=True)
+            pb.evict(op[1], release=True)
+        elif kind == "extract":
+            _, slots, tag = op
+            ks, vs = cache.extract(slots)
+            want = pb.extract(slots)
+            for (kw, vw), kg, vg in zip(want, ks, vs):
+                assert np.array_equal(host_bits(kg), kw) and np.array_equal(host_bits(vg), vw), \
+                    f"extract {slots}: bits differ"
+            saved_gpu[tag], saved_cpu[tag] = (ks, vs), want
+        elif kind == "embed_saved":
+            _, slots, tag = op
+            ks, vs = saved_gpu[tag]
+            cache.embed(slots, [k.shape[2] for k in ks], ks, vs)
+            pb.embed(slots, [k.shape[2] for k, _ in saved_cpu[tag]], [k for k, _ in saved_cpu[tag]],
+                     [v for _, v in saved_cpu[tag]])
+        elif kind == "step":
+            s = op[1]
+            m = cache.build_mask()
+            assert np.array_equal(m.cpu().numpy(), pb.mask()), f"{op}: mask"
+            for layer in range(NL):
+                q, kn, vn = dev.decode(s, layer)
+                out = cache.decode_attn(layer, q, kn, vn)
+                hq = [gen.decode_host(w.seed, sid, s, layer, NL, B, h, D, dtype)
+                      for sid, h in ((gen.S_Q, Hq), (gen.S_KNEW, Hkv), (gen.S_VNEW, Hkv))]
+                want = pb.decode_layer(layer, *hq)
+                err = max_err(out, want, dtype)
+                worst = max(worst, err)
+                assert err <= TOL[dtype], f"{op} layer {layer}: {err}"
+            cache.advance()
+            pb.advance()
+        else:
+            raise ValueError(kind)
+        torch.cuda.synchronize()
+        check_ring(cache, pb, str(op))
+    cache.close()
+    return worst

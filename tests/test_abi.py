@@ -75,6 +75,10 @@ def test_host_checks_leave_state_unchanged():
         assert status(B.baton_kv_embed, h, [0, 0], [3, 3], [FAKE_K] * 2, [FAKE_V] * 2) == B.BATON_EINVAL
         assert status(B.baton_kv_embed, h, [0], [3], [0], [FAKE_V]) == B.BATON_EINVAL      # null source
         assert status(B.baton_kv_embed, h, [0], [3], [FAKE_K + 4], [FAKE_V]) == B.BATON_EINVAL  # misaligned
+        assert status(B.baton_kv_extract, h, [0], [FAKE_K], [FAKE_V]) == B.BATON_ESLOT   # free slot
+        assert status(B.baton_kv_extract, h, [0, 0], [FAKE_K] * 2, [FAKE_V] * 2) == B.BATON_EINVAL
+        assert status(B.baton_kv_extract, h, [0], [FAKE_K + 8], [FAKE_V]) == B.BATON_EINVAL
+        B.baton_kv_extract(h, [], [], [])                                  # nothing to do
         assert status(B.baton_step_advance, h) == B.BATON_ESTATE          # no layer decoded
         ws = B.baton_decode_attn_workspace_bytes(h)
         assert status(B.baton_decode_attn, h, 2, FAKE_K, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws) == B.BATON_EINVAL

@@ -1,0 +1,68 @@
+"""Preemption and batch-size scaling on the GPU (sec. 4.3): a query's keys and
+values stored aside with baton_kv_extract, the query evicted, other queries
+taking and leaving its slot, and the stored query re-inserted later into a
+different slot -- bit-exact against the oracle after every operation, and the
+re-inserted query decoding as the oracle says it must."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2410_18701_amd import baton as B
+from paper_2410_18701_amd.cache import BatonCache
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("shape", [("bf16", 2, 4, 8, 2, 128), ("f32", 1, 4, 4, 4, 64), ("bf16", 1, 5, 8, 8, 64)],
+                         ids=lambda s: f"{s[0]}-{s[1]}x{s[2]}-{s[3]}/{s[4]}x{s[5]}")
+def test_preempt_and_resume(shape):
+    ops = [
+        ("embed", [0, 1, 2], [37, 90, 12], [0, 1, 2]),
+        ("step", 0), ("step", 1),
+        ("extract", [1], "low"),                 # the lowest-priority query is stored aside
+        ("evict", [1]),                          # ... and leaves its slot
+        ("embed", [1], [50], [3]),               # the high-priority query takes it
+        ("step", 2), ("step", 3),
+        ("evict", [0]),                          # some query finishes
+        ("embed_saved", [3], "low"),             # the stored one comes back, in another slot
+        ("step", 4),
+        ("extract", [3, 2], "pair"),             # batch-size scaling: two queries leave ...
+        ("evict", [2, 3]),
+        ("step", 5),
+        ("embed_saved", [0, 2], "pair"),         # ... and return
+        ("step", 6), ("step", 7),
+    ]
+    err = parity.run_script(shape, ops, capacity=256, split=64)
+    print(f"[preempt] {shape}: max abs error {err:.3g}", flush=True)
+
+
+def test_host_round_trip():
+    """Batch-size scaling through host memory: extract, copy to pinned host
+    memory, evict, copy back, re-embed -- the cache returns bit for bit."""
+    cache = BatonCache(2, 3, 4, 2, 64, capacity=128, dtype="bf16")
+    from workload import driver
+    from workload.configs import Workload
+    dev = driver.DeviceInputs(Workload("h", "bf16", 2, 3, 4, 2, 64, 1, 0, seed=4))
+    srcs = [dev.prefill(q, n) for q, n in zip([0, 1, 2], [20, 33, 7])]
+    cache.embed([0, 1, 2], [20, 33, 7], [s[0] for s in srcs], [s[1] for s in srcs])
+    torch.cuda.synchronize()
+    before = (parity.host_bits(cache.k).copy(), parity.host_bits(cache.v).copy(), cache.query())
+    ks, vs = cache.extract([1])
+    hk = torch.empty(ks[0].shape, dtype=ks[0].dtype, pin_memory=True)
+    hv = torch.empty(vs[0].shape, dtype=vs[0].dtype, pin_memory=True)
+    hk.copy_(ks[0])
+    hv.copy_(vs[0])
+    cache.evict([1], release=True)
+    del ks, vs
+    dk, dv = hk.cuda(), hv.cuda()
+    cache.embed([1], [dk.shape[2]], [dk], [dv])
+    torch.cuda.synchronize()
+    assert cache.query() == before[2]
+    assert np.array_equal(parity.host_bits(cache.k), before[0])
+    assert np.array_equal(parity.host_bits(cache.v), before[1])
+    with pytest.raises(B.BatonError) as e:
+        cache.extract([2])[0]                     # live: fine
+        B.baton_kv_extract(cache.handle, [1, 1], [dk, dk], [dv, dv])
+    assert e.value.status == B.BATON_EINVAL
+    cache.close()
