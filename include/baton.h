@@ -32,8 +32,10 @@
  * column j of the aligned cache (0 <= j < L) lives at physical column
  * (base + j) mod capacity, where base is reported by baton_cache_query.  Every
  * physical position that is not a live token holds the placeholder bits
- * (fill_bits) at every call boundary -- free rows, the placeholder fronts of
- * live rows and the capacity - L unused columns alike.
+ * (fill_bits) -- free rows, the placeholder fronts of live rows and the
+ * capacity - L unused columns alike -- except the tokens of slots evicted since
+ * the last decode step began, whose placeholder write is deferred (see
+ * baton_kv_evict).
  */
 #ifndef BATON_H
 #define BATON_H
@@ -103,13 +105,17 @@ baton_status baton_cache_destroy(baton_cache* cache);
  * Finished queries leave their slots (sec. 4.1, Attention_mask and KV_Cache
  * paragraphs: the finished query's cached keys/values are overwritten with the
  * placeholder and its mask row zeroed).  slots: host array of n distinct live
- * slot indices (n may be 0).  Enqueues the placeholder write over each slot's
- * live tokens in every layer and head; the slot becomes free.  With
- * BATON_RELEASE, the columns [0 : min over live rows of (L - len)] are then
- * released (sec. 4.1, "Resources releasing"): L becomes the longest live
- * length (0 when no slot is live).  Release itself moves no data.
+ * slot indices (n may be 0); the slots become free.  The placeholder write over
+ * each finished query's tokens (every layer and head) is owed, not enqueued
+ * here: the next baton_kv_embed into the slot performs it over the columns in
+ * front of its new query (the new query overwrites the rest), and the first
+ * baton_decode_attn of the next step, or baton_cache_flush, performs whatever
+ * is still owed.  With BATON_RELEASE, the columns [0 : min over live rows of
+ * (L - len)] are then released (sec. 4.1, "Resources releasing"): L becomes
+ * the longest live length (0 when no slot is live).  Release moves no data.
+ * Nothing is enqueued.
  * Errors: EINVAL (n < 0, null slots with n > 0, index out of range, duplicate,
- * unknown flag), ESLOT (a slot is free), ESTATE (inside a decode step), EHIP.
+ * unknown flag), ESLOT (a slot is free), ESTATE (inside a decode step).
  */
 baton_status baton_kv_evict(baton_cache* cache, const int32_t* slots, int32_t n, uint32_t flags,
                             hipStream_t stream);
@@ -122,7 +128,8 @@ baton_status baton_kv_evict(baton_cache* cache, const int32_t* slots, int32_t n,
  * batch first grows on the left to that length, every other row's new front
  * being placeholders; then each query's keys/values are copied end-aligned into
  * its slot, placeholders in front (the case l_q <= l_kv).  Growth moves no
- * data: the new front columns already hold placeholders.
+ * data: the new front columns already hold placeholders.  The same launch writes
+ * the placeholders an embedded slot still owes from its eviction.
  * Errors: EINVAL (n < 0, null arrays or pointers, slot out of range, duplicate,
  * lens[i] < 1), ESLOT (a slot is live), ECAPACITY (max(L, max lens) + 1 >
  * capacity), ESTATE (inside a decode step), EHIP.
@@ -188,6 +195,14 @@ size_t baton_decode_attn_workspace_bytes(const baton_cache* cache);
 baton_status baton_decode_attn(baton_cache* cache, int32_t layer, const void* q, const void* k_new,
                                const void* v_new, void* out, float scale, void* ws, size_t ws_bytes,
                                hipStream_t stream);
+
+/*
+ * Enqueue the placeholder writes evictions still owe (see baton_kv_evict), so
+ * that every non-live position holds the placeholder now.  Never needed for
+ * correct results; for callers that read the ring directly.
+ * Errors: EINVAL (null cache), EHIP.
+ */
+baton_status baton_cache_flush(baton_cache* cache, hipStream_t stream);
 
 /*
  * Close the decode step once every layer has been decoded: L += 1 and every

@@ -60,6 +60,7 @@ def lib():
         L.baton_decode_attn_workspace_bytes.restype = ctypes.c_size_t
         L.baton_decode_attn.argtypes = [vp, i32, vp, vp, vp, vp, ctypes.c_float, vp, ctypes.c_size_t, vp]
         L.baton_step_advance.argtypes = [vp]
+        L.baton_cache_flush.argtypes = [vp, vp]
         L.baton_cache_query.argtypes = [vp, P(i64), P(i64), P(i32)]
         L.baton_set_split_tokens.argtypes = [vp, i32]
         L.baton_status_string.argtypes = [st]
@@ -67,7 +68,7 @@ def lib():
         for name in ("baton_cache_create", "baton_cache_destroy", "baton_kv_evict", "baton_kv_embed",
                      "baton_kv_extract",
                      "baton_build_mask", "baton_decode_attn", "baton_step_advance",
-                     "baton_cache_query", "baton_set_split_tokens"):
+                     "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush"):
             getattr(L, name).restype = st
         _lib = L
     return _lib
@@ -151,6 +152,10 @@ def baton_decode_attn(cache, layer, q, k_new, v_new, out, scale, ws, ws_bytes, s
     _check(lib().baton_decode_attn(cache, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
                                    float(scale), _ptr(ws), ws_bytes, _stream(stream)),
            "baton_decode_attn")
+
+
+def baton_cache_flush(cache, stream=None):
+    _check(lib().baton_cache_flush(cache, _stream(stream)), "baton_cache_flush")
 
 
 def baton_step_advance(cache):

@@ -93,6 +93,10 @@ class BatonCache:
                             stream if stream is not None else _cur_stream())
         return out
 
+    def flush(self, stream=None):
+        """Enqueue the placeholder writes evictions still owe."""
+        B.baton_cache_flush(self.handle, stream if stream is not None else _cur_stream())
+
     def advance(self):
         B.baton_step_advance(self.handle)
 

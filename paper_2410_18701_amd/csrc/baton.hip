@@ -33,6 +33,9 @@ struct baton_cache {
   int64_t L = 0;           // padded length
   int64_t base = 0;        // physical column of logical column 0
   std::vector<int32_t> lens;
+  // Placeholder writes still owed by evictions: pending[s] tokens of slot s,
+  // ending at ring column base + L (which neither release nor growth moves).
+  std::vector<int32_t> pending;
   std::vector<uint8_t> layer_done;
   int32_t n_done = 0;      // layers decoded in the current step
   // Work list of the current step as last written into a workspace.
@@ -203,6 +206,20 @@ int32_t auto_split(const baton_cache* c) {
   return (int32_t)std::min(kAutoSplitMax, std::max(kAutoSplitMin, s));
 }
 
+// Enqueues the placeholder writes evictions still owe.
+baton_status flush_pending(baton_cache* c, hipStream_t stream) {
+  const int64_t end = ring(c->base + c->L, c->d.capacity);
+  std::vector<Seg> segs;
+  for (int32_t b = 0; b < c->d.batch; ++b)
+    if (c->pending[b] > 0)
+      segs.push_back({b, c->pending[b], ring(end - c->pending[b], c->d.capacity), nullptr, nullptr});
+  if (segs.empty()) return BATON_OK;
+  const baton_status st = launch_segs(c, segs, stream);
+  if (st != BATON_OK) return st;
+  std::fill(c->pending.begin(), c->pending.end(), 0);
+  return BATON_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -244,6 +261,7 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   c->group = g;
   c->split = 0;
   c->lens.assign(d.batch, 0);
+  c->pending.assign(d.batch, 0);
   c->layer_done.assign(d.n_layers, 0);
   if (!(flags & BATON_CREATE_ASSUME_FILLED)) {
     const int64_t n_vec = (int64_t)d.n_layers * d.batch * d.n_kv_heads * d.capacity * c->vpt;
@@ -278,16 +296,14 @@ baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uin
   }
   for (int32_t i = 0; i < n; ++i)
     if (c->lens[slots[i]] == 0) return BATON_ESLOT;
-  // The finished queries' tokens become placeholders (the rest of their rows already is).
-  std::vector<Seg> segs;
-  segs.reserve(n);
+  // The finished queries' tokens are owed placeholders (the rest of their rows
+  // already holds them); the write is left to the next embed into the slot,
+  // which skips the columns its own query overwrites, or to the next step.
+  (void)stream;
   for (int32_t i = 0; i < n; ++i) {
-    const int32_t s = slots[i], len = c->lens[s];
-    segs.push_back({s, len, ring(c->base + c->L - len, c->d.capacity), nullptr, nullptr});
+    c->pending[slots[i]] = c->lens[slots[i]];
+    c->lens[slots[i]] = 0;
   }
-  const baton_status st = launch_segs(c, segs, stream);
-  if (st != BATON_OK) return st;
-  for (int32_t i = 0; i < n; ++i) c->lens[slots[i]] = 0;
   if (flags & BATON_RELEASE) {
     int64_t r = c->L;
     for (int32_t b = 0; b < c->d.batch; ++b)
@@ -321,16 +337,26 @@ baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, con
   // Growth on the left: the new front columns come out of the unused part of
   // the ring, which holds placeholders in every row already.
   const int64_t base_new = ring(c->base - (L_new - c->L), c->d.capacity);
+  // One launch: each query's copy, and the placeholders its slot still owes
+  // over the columns in front of the new query (both end at base + L).
+  const int64_t end = ring(c->base + c->L, c->d.capacity);
   std::vector<Seg> segs;
-  segs.reserve(n);
-  for (int32_t i = 0; i < n; ++i)
+  segs.reserve(2 * n);
+  for (int32_t i = 0; i < n; ++i) {
     segs.push_back({slots[i], lens[i], ring(base_new + L_new - lens[i], c->d.capacity), k_src[i],
                     v_src[i]});
+    const int32_t owed = c->pending[slots[i]];
+    if (owed > lens[i])
+      segs.push_back({slots[i], owed - lens[i], ring(end - owed, c->d.capacity), nullptr, nullptr});
+  }
   const baton_status st = launch_segs(c, segs, stream);
   if (st != BATON_OK) return st;
   c->base = base_new;
   c->L = L_new;
-  for (int32_t i = 0; i < n; ++i) c->lens[slots[i]] = lens[i];
+  for (int32_t i = 0; i < n; ++i) {
+    c->lens[slots[i]] = lens[i];
+    c->pending[slots[i]] = 0;
+  }
   c->meta_valid = false;
   return BATON_OK;
 }
@@ -389,6 +415,10 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   if (ws_bytes < w.total) return BATON_EINVAL;
   if (c->layer_done[layer]) return BATON_ESTATE;
   if (c->L + 1 > c->d.capacity) return BATON_ECAPACITY;
+  if (c->n_done == 0) {
+    const baton_status st = flush_pending(c, stream);
+    if (st != BATON_OK) return st;
+  }
   char* wsb = static_cast<char*>(ws);
   if (!c->meta_valid || c->meta_ws != ws) {
     baton::MetaArgs m;
@@ -441,6 +471,11 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   c->layer_done[layer] = 1;
   ++c->n_done;
   return BATON_OK;
+}
+
+baton_status baton_cache_flush(baton_cache* c, hipStream_t stream) {
+  if (!c) return BATON_EINVAL;
+  return flush_pending(c, stream);
 }
 
 baton_status baton_step_advance(baton_cache* c) {

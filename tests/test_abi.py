@@ -79,6 +79,7 @@ def test_host_checks_leave_state_unchanged():
         assert status(B.baton_kv_extract, h, [0, 0], [FAKE_K] * 2, [FAKE_V] * 2) == B.BATON_EINVAL
         assert status(B.baton_kv_extract, h, [0], [FAKE_K + 8], [FAKE_V]) == B.BATON_EINVAL
         B.baton_kv_extract(h, [], [], [])                                  # nothing to do
+        B.baton_cache_flush(h)                                             # nothing owed
         assert status(B.baton_step_advance, h) == B.BATON_ESTATE          # no layer decoded
         ws = B.baton_decode_attn_workspace_bytes(h)
         assert status(B.baton_decode_attn, h, 2, FAKE_K, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws) == B.BATON_EINVAL
