@@ -27,6 +27,14 @@ Efficiency for Large Language Models via Dynamic Re-batching", 2024):
   (sec. 2.1, "General architecture").
 * The paper's correctness claim: shaping, padding and placeholders do not change
   any query's result (sec. 4.1, the paragraphs closing the insertion example).
+* Without prefill/decode separation (sec. 4.1, the Input_token, Attention_mask
+  and KV_Cache paragraphs of the insertion example), a new query is prefilled
+  inside the batch: the step's input has T = l_q positions per row, the other
+  queries' latest token padded behind to T; their mask rows keep their old
+  values, 1 for the latest token, 0 for the padding; the new query's row is 0
+  over the old columns and 1 over its own tokens; the cache grows by T columns,
+  and the padding columns stay in the other rows as holes that are never
+  attended to.
 
 Two formulations are kept and must agree: the padded batch (PaddedBatch, the
 paper's tensors) and each query's own unpadded history (hist_k / hist_v);
@@ -45,7 +53,15 @@ the design notes of the repository):
 * scale defaults to 1/sqrt(head_dim);
 * grouped-query attention maps q-head hq to kv-head hq // (n_q_heads // n_kv_heads);
 * several evictions/insertions in one step: evictions (ascending), release,
-  then insertions in the given order.
+  then insertions in the given order;
+* in-batch prefill of several queries in one step: T = the longest of them,
+  a shorter prompt sits at the end of the T new columns with zeros in front
+  (the batch's left padding of prompts, sec. 2.1); outputs at positions that
+  hold no token are not defined (NaN here), except that a free row's first
+  position is 0 as in a decode step; the padding columns hold placeholders;
+* a row's length (lens) is its span: columns from its first token to the end
+  of the cache, holes included; release drops [0 : min over live rows of the
+  first token column].
 """
 import math
 
@@ -93,6 +109,16 @@ def build_mask(L, lens):
     return M
 
 
+def expected_row_masked(mask_row, hist_row, fill_bits, dtype):
+    """A row of the aligned cache whose tokens sit where mask_row (its cached
+    columns) is 1, in order; placeholders elsewhere."""
+    keep = np.asarray(mask_row).astype(bool)
+    hist_row = np.asarray(hist_row)
+    out = np.full((len(keep), hist_row.shape[-1]), fill_bits, dtype=STORAGE[dtype])
+    out[keep] = hist_row
+    return out
+
+
 def expected_row(L, n, hist_row, fill_bits, dtype):
     """A live row of the aligned cache: L - n placeholders, then the n history rows."""
     hist_row = np.asarray(hist_row)
@@ -128,9 +154,11 @@ class PaddedBatch:
         self.V = np.zeros(shape, st) if materialize else None
         self.hist_k = [None] * batch   # per slot: [layer][head][n][dim] bits of its query
         self.hist_v = [None] * batch
-        self._new_k = None             # column being appended this step, per layer
+        self.M = np.zeros((batch, 0), np.uint8)   # attention_mask over the cached columns
+        self._new_k = None             # columns being appended this step, per layer
         self._new_v = None
         self._layers_done = set()
+        self._shape = None             # pending in-batch prefill: {slot: prompt length}
 
     # -- helpers --
     def _placeholders(self, n_cols, rows=None):
@@ -143,6 +171,12 @@ class PaddedBatch:
     def _check_between_steps(self):
         if self._layers_done:
             raise RuntimeError("a decode step is in progress")
+        if self._shape is not None:
+            raise RuntimeError("an in-batch prefill is registered for the next step")
+
+    def step_width(self):
+        """Positions per row in the next step's input: 1, or T with an in-batch prefill."""
+        return max(self._shape.values()) if self._shape else 1
 
     # -- the method's steps --
     def evict(self, slots, release=True):
@@ -158,6 +192,7 @@ class PaddedBatch:
             if self.materialize:
                 self.K[:, s] = self.fill
                 self.V[:, s] = self.fill
+            self.M[s] = 0
             self.lens[s] = 0
             self.hist_k[s] = self.hist_v[s] = None
         if release:
@@ -171,6 +206,7 @@ class PaddedBatch:
         if self.materialize:
             self.K = self.K[:, :, :, r:]
             self.V = self.V[:, :, :, r:]
+        self.M = self.M[:, r:]
         self.L -= r
         return r
 
@@ -189,7 +225,10 @@ class PaddedBatch:
                 if self.materialize:
                     self.K = np.concatenate([self._placeholders(grow), self.K], axis=3)
                     self.V = np.concatenate([self._placeholders(grow), self.V], axis=3)
+                self.M = np.concatenate([np.zeros((self.B, grow), np.uint8), self.M], axis=1)
                 self.L = n
+            self.M[s] = 0
+            self.M[s, self.L - n:] = 1
             if self.materialize:                    # case l_q <= l_kv: end-aligned
                 self.K[:, s] = self.fill
                 self.V[:, s] = self.fill
@@ -211,19 +250,57 @@ class PaddedBatch:
             raise LookupError("extracting a free slot")
         out = []
         for s in slots:
-            n = self.lens[s]
-            out.append((self.K[:, s, :, self.L - n:].copy(), self.V[:, s, :, self.L - n:].copy()))
+            keep = self.M[s].astype(bool)
+            out.append((self.K[:, s][:, :, keep].copy(), self.V[:, s][:, :, keep].copy()))
         return out
 
+    def shape_insert(self, slots, lens):
+        """Register new queries to be prefilled inside the batch in the next step
+        (no prefill/decode separation, sec. 4.1): slots must be free, lens are
+        their prompt lengths.  The step's input then has T = max(lens) positions
+        per row."""
+        self._check_between_steps()
+        if not slots or len(set(slots)) != len(slots) or any(not 0 <= s < self.B for s in slots):
+            raise ValueError("bad slot list")
+        if len(lens) != len(slots) or any(n < 1 for n in lens):
+            raise ValueError("a prompt has at least one token")
+        if any(self.lens[s] != 0 for s in slots):
+            raise LookupError("shaping into a live slot")
+        self._shape = {s: int(n) for s, n in zip(slots, lens)}
+
     def mask(self):
-        return build_mask(self.L, self.lens)
+        """attention_mask of the next step: the cached columns, then the step's
+        own input columns (one, or T with an in-batch prefill)."""
+        if not self._shape:
+            cur = np.array([[1 if n > 0 else 0] for n in self.lens], np.uint8).reshape(self.B, 1)
+            return np.concatenate([self.M, cur], axis=1)
+        T = self.step_width()
+        M = np.zeros((self.B, self.L + T), np.uint8)
+        for b in range(self.B):
+            if b in self._shape:                 # old columns 0, its own tokens 1
+                M[b, self.L + T - self._shape[b]:] = 1
+            elif self.lens[b] > 0:               # old values, latest token 1, padding 0
+                M[b, :self.L] = self.M[b]
+                M[b, self.L] = 1
+        return M
+
+    def _positions(self, b):
+        """Input positions of row b that hold a token in the next step."""
+        T = self.step_width()
+        if self._shape and b in self._shape:
+            return list(range(T - self._shape[b], T))
+        return [0] if self.lens[b] > 0 else []
 
     def decode_layer(self, layer, q, k_new, v_new, scale=None):
-        """One layer of the decode step.
+        """One layer of the step.
 
-        q: bits [batch][n_q_heads][dim]; k_new, v_new: bits [batch][n_kv_heads][dim].
-        Appends column L of this layer (placeholders in free rows) and returns the
-        attention output float64 [batch][n_q_heads][dim], 0 for free rows.
+        Decode step: q bits [batch][n_q_heads][dim]; k_new, v_new bits
+        [batch][n_kv_heads][dim].  With an in-batch prefill registered, every
+        input has a position axis after the batch: [batch][T][...][dim].
+        Appends this layer's new columns (placeholders where no token is) and
+        returns the attention output float64 in q's shape, computed from each
+        query's own tokens: 0 for a free row's first position, NaN at positions
+        that hold no token.
         """
         if layer in self._layers_done:
             raise RuntimeError("layer already decoded this step")
@@ -232,52 +309,95 @@ class PaddedBatch:
             return None
         scale = 1.0 / math.sqrt(self.D) if scale is None else scale
         st = STORAGE[self.dtype]
+        T = self.step_width()
+        shaped = self._shape is not None
+        if not shaped:                           # one position: add the axis
+            q, k_new, v_new = q[:, None], k_new[:, None], v_new[:, None]
+        if q.shape[1] != T or k_new.shape[1] != T or v_new.shape[1] != T:
+            raise ValueError("inputs must have one position per column of the step")
         if self._new_k is None:
-            self._new_k = np.full((self.NL, self.B, self.Hkv, 1, self.D), self.fill, st)
-            self._new_v = np.full((self.NL, self.B, self.Hkv, 1, self.D), self.fill, st)
+            self._new_k = np.full((self.NL, self.B, self.Hkv, T, self.D), self.fill, st)
+            self._new_v = np.full((self.NL, self.B, self.Hkv, T, self.D), self.fill, st)
         g = self.Hq // self.Hkv
-        out = np.zeros((self.B, self.Hq, self.D))
-        for b in self.live():
-            self._new_k[layer, b, :, 0] = k_new[b]
-            self._new_v[layer, b, :, 0] = v_new[b]
-            for hq in range(self.Hq):
-                h = hq // g
-                K = widen(np.concatenate([self.hist_k[b][layer, h], k_new[b][h][None]]), self.dtype)
-                V = widen(np.concatenate([self.hist_v[b][layer, h], v_new[b][h][None]]), self.dtype)
-                out[b, hq] = attend(widen(q[b, hq], self.dtype), K, V, scale)
+        out = np.full((self.B, T, self.Hq, self.D), np.nan)
+        for b in range(self.B):
+            pos = self._positions(b)
+            if not pos:
+                out[b, 0] = 0.0
+                continue
+            for t in pos:
+                self._new_k[layer, b, :, t] = k_new[b, t]
+                self._new_v[layer, b, :, t] = v_new[b, t]
+            for t in pos:
+                for hq in range(self.Hq):
+                    h = hq // g
+                    if shaped and b in self._shape:      # the new query: its prompt up to t
+                        K = widen(k_new[b, pos[0]:t + 1, h], self.dtype)
+                        V = widen(v_new[b, pos[0]:t + 1, h], self.dtype)
+                    else:                                # its history and the latest token
+                        K = widen(np.concatenate([self.hist_k[b][layer, h], k_new[b, t, h][None]]), self.dtype)
+                        V = widen(np.concatenate([self.hist_v[b][layer, h], v_new[b, t, h][None]]), self.dtype)
+                    out[b, t, hq] = attend(widen(q[b, t, hq], self.dtype), K, V, scale)
         self._layers_done.add(layer)
-        return out
+        return out if shaped else out[:, 0]
 
     def decode_layer_padded(self, layer, q, scale=None):
         """The batched formulation of the same layer: masked attention over the
-        padded rows (after decode_layer appended this layer's column)."""
+        padded rows (after decode_layer appended this layer's columns); the query
+        at input position t sees the mask's columns up to L + t."""
         if layer not in self._layers_done or not self.materialize:
             raise RuntimeError("decode_layer first, on a materialized batch")
         scale = 1.0 / math.sqrt(self.D) if scale is None else scale
+        shaped = self._shape is not None
+        if not shaped:
+            q = q[:, None]
+        T = self.step_width()
         g = self.Hq // self.Hkv
         M = self.mask()
         K = np.concatenate([self.K[layer], self._new_k[layer]], axis=2)
         V = np.concatenate([self.V[layer], self._new_v[layer]], axis=2)
-        out = np.zeros((self.B, self.Hq, self.D))
-        for b in self.live():
-            for hq in range(self.Hq):
-                h = hq // g
-                out[b, hq] = attend_masked(widen(q[b, hq], self.dtype), widen(K[b, h], self.dtype),
-                                           widen(V[b, h], self.dtype), M[b], scale)
-        return out
+        out = np.full((self.B, T, self.Hq, self.D), np.nan)
+        for b in range(self.B):
+            pos = self._positions(b)
+            if not pos:
+                out[b, 0] = 0.0
+            for t in pos:
+                c = self.L + t + 1
+                for hq in range(self.Hq):
+                    h = hq // g
+                    out[b, t, hq] = attend_masked(widen(q[b, t, hq], self.dtype),
+                                                  widen(K[b, h, :c], self.dtype),
+                                                  widen(V[b, h, :c], self.dtype), M[b, :c], scale)
+        return out if shaped else out[:, 0]
 
     def advance(self):
-        """Close the step: every layer appended its column; lengths grow by one."""
+        """Close the step: every layer appended its columns; the mask takes the
+        step's columns; rows that decoded grow by one token."""
         if len(self._layers_done) != self.NL:
             raise RuntimeError("every layer must be decoded before the step advances")
+        T = self.step_width()
+        M_step = self.mask()[:, self.L:]
         if self.materialize:
             self.K = np.concatenate([self.K, self._new_k], axis=3)
             self.V = np.concatenate([self.V, self._new_v], axis=3)
-        for b in self.live():
+        for b in range(self.B):
+            pos = self._positions(b)
+            if not pos:
+                continue
             if self.materialize:
-                self.hist_k[b] = np.concatenate([self.hist_k[b], self._new_k[:, b]], axis=2)
-                self.hist_v[b] = np.concatenate([self.hist_v[b], self._new_v[:, b]], axis=2)
-            self.lens[b] += 1
-        self.L += 1
+                k_tok = self._new_k[:, b][:, :, pos]
+                v_tok = self._new_v[:, b][:, :, pos]
+                if self._shape and b in self._shape:
+                    self.hist_k[b], self.hist_v[b] = k_tok, v_tok
+                else:
+                    self.hist_k[b] = np.concatenate([self.hist_k[b], k_tok], axis=2)
+                    self.hist_v[b] = np.concatenate([self.hist_v[b], v_tok], axis=2)
+            if self._shape and b in self._shape:
+                self.lens[b] = self._shape[b]
+            else:
+                self.lens[b] += T
+        self.M = np.concatenate([self.M, M_step], axis=1)
+        self.L += T
         self._new_k = self._new_v = None
         self._layers_done = set()
+        self._shape = None

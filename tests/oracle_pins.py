@@ -243,6 +243,8 @@ def pin_layout_invariants(O):
             if n:
                 want[pb.L - n:] = 1
             assert np.array_equal(m, want)
+        # the mask the batch built step by step is the closed form of its lengths
+        assert np.array_equal(pb.mask(), O.build_mask(pb.L, pb.lens))
         if op[0] == "evict":
             assert pb.L == max(pb.lens)
         elif op[0] == "embed":
@@ -401,3 +403,205 @@ def pin_preemption_round_trip(O):
 
 
 ALL_PINS.append(pin_preemption_round_trip)
+
+
+# ------------------------------------- in-batch prefill (no P&D separation) --
+_PAD_CODE = 999999.0
+
+
+def pin_inbatch_prefill_replay(O):
+    """Replay of the sec. 4.1 insertion story without prefill/decode separation
+    against hand-derived states (tests/golden/inbatch_prefill_replay.json): L,
+    cells (holes included), masks (the l_am + l_q - 1 wide mask of a prefill
+    step), and the outputs of zero queries (means of the attended values)."""
+    g = _load("inbatch_prefill_replay.json")
+    B = g["batch"]
+    pb = O.PaddedBatch(1, B, 1, 1, 1, O.F32)
+    slot_qid = [None] * B
+    count = [0] * B          # tokens in each query's own history
+    for op in g["ops"]:
+        if op["op"] == "embed":
+            srcs = [_src(q, n) for q, n in zip(op["qids"], op["lens"])]
+            pb.embed(op["slots"], op["lens"], srcs, srcs)
+            for s, q, n in zip(op["slots"], op["qids"], op["lens"]):
+                slot_qid[s], count[s] = q, n
+        elif op["op"] == "evict":
+            pb.evict(op["slots"], release=True)
+            for s in op["slots"]:
+                slot_qid[s], count[s] = None, 0
+        elif op["op"] == "shape":
+            l_am = pb.L + 1
+            pb.shape_insert(op["slots"], op["lens"])
+            shaped = {s: (q, n) for s, q, n in zip(op["slots"], op["qids"], op["lens"])}
+            assert pb.mask().shape[1] == l_am + max(op["lens"]) - 1
+        elif op["op"] == "step":
+            T = pb.step_width()
+            pending = pb._shape or {}
+            kn = np.full((B, T, 1, 1), _PAD_CODE, np.float32)
+            for b in range(B):
+                if b in pending:
+                    q, n = shaped[b]
+                    for p in range(n):
+                        kn[b, T - n + p] = _code(q, p)
+                elif slot_qid[b] is not None:
+                    kn[b, 0] = _code(slot_qid[b], count[b])
+            kn = kn.view(np.uint32)
+            q0 = np.zeros((B, T, 1, 1), np.uint32)
+            if pending:
+                out = pb.decode_layer(0, q0, kn, kn)
+            else:
+                out = pb.decode_layer(0, q0[:, 0], kn[:, 0], kn[:, 0])[:, None]
+            for b in range(B):
+                for t in range(T):
+                    want = op["out"][b][t]
+                    got = out[b, t, 0, 0]
+                    if want is None:
+                        assert math.isnan(got), (op, b, t, got)
+                    else:
+                        assert abs(got - want) < 1e-9, (op, b, t, got, want)
+            pb.advance()
+            for b in range(B):
+                if b in pending:
+                    slot_qid[b], count[b] = shaped[b][0], shaped[b][1]
+                elif slot_qid[b] is not None:
+                    count[b] += 1
+        assert pb.L == op["L"], (op, pb.L)
+        cells = pb.K[0, :, 0, :, 0].view(np.float32)
+        for b in range(B):
+            got = " ".join(_decode_cell(x) for x in cells[b])
+            assert got == op["rows"][b], (op["op"], b, got, op["rows"][b])
+        want_mask = np.array([[int(x) for x in r.split()] for r in op["mask"]], np.uint8)
+        assert np.array_equal(pb.mask(), want_mask), (op["op"], pb.mask(), want_mask)
+
+
+def pin_inbatch_prefill_sdpa(O):
+    """The new query's outputs in a prefill step are causal self-attention over
+    its prompt: torch's scaled_dot_product_attention(is_causal=True) in float64
+    on the CPU, per q-head with the grouped kv-head; and its cached keys/values
+    afterwards are exactly its prompt's."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(41)
+    NL, B, Hq, Hkv, D = 1, 3, 4, 2, 16
+
+    def bits(shape):
+        return rng.standard_normal(shape).astype(np.float32).view(np.uint32)
+
+    pb = O.PaddedBatch(NL, B, Hq, Hkv, D, O.F32)
+    pb.embed([0, 2], [5, 3], [bits((NL, Hkv, 5, D)), bits((NL, Hkv, 3, D))],
+             [bits((NL, Hkv, 5, D)), bits((NL, Hkv, 3, D))])
+    l_new = 7
+    pb.shape_insert([1], [l_new])
+    T = pb.step_width()
+    q, kn, vn = bits((B, T, Hq, D)), bits((B, T, Hkv, D)), bits((B, T, Hkv, D))
+    out = pb.decode_layer(0, q, kn, vn)
+    g = Hq // Hkv
+    for hq in range(Hq):
+        h = hq // g
+        Q = torch.tensor(O.widen(q[1, :, hq], O.F32))[None, None]
+        K = torch.tensor(O.widen(kn[1, :, h], O.F32))[None, None]
+        V = torch.tensor(O.widen(vn[1, :, h], O.F32))[None, None]
+        ref = F.scaled_dot_product_attention(Q, K, V, is_causal=True).numpy()[0, 0]
+        assert np.allclose(out[1, :, hq], ref, rtol=0, atol=1e-12), hq
+    pb.advance()
+    assert np.array_equal(pb.K[0, 1][:, pb.L - l_new:], kn[1].transpose(1, 0, 2))
+    assert np.array_equal(pb.hist_v[1][0], vn[1].transpose(1, 0, 2))
+
+
+def _random_ops_shaped(rng, B, steps, max_len):
+    """Random sequences that also prefill new queries inside the batch."""
+    ops = []
+    live = set()
+    for _ in range(steps):
+        free = [b for b in range(B) if b not in live]
+        r = rng.random()
+        if live and r < 0.25:
+            k = int(rng.integers(1, len(live) + 1))
+            ev = sorted(rng.choice(sorted(live), k, replace=False).tolist())
+            ops.append(("evict", ev))
+            live -= set(ev)
+        elif free and r < 0.45:
+            k = int(rng.integers(1, len(free) + 1))
+            ins = rng.choice(free, k, replace=False).tolist()
+            ops.append(("embed", ins, [int(rng.integers(1, max_len + 1)) for _ in ins]))
+            live |= set(ins)
+        elif free and r < 0.7:
+            k = int(rng.integers(1, len(free) + 1))
+            ins = rng.choice(free, k, replace=False).tolist()
+            ops.append(("shape", ins, [int(rng.integers(1, max_len + 1)) for _ in ins]))
+            live |= set(ins)
+        else:
+            ops.append(("decode",))
+    return ops
+
+
+def _run_shaped(O, ops, NL, B, Hq, Hkv, D, dtype, seed, fill=None, check=None):
+    """Like _run; a ("shape", slots, lens) op registers the prefill and runs its step."""
+    rng = np.random.default_rng(seed)
+    pb = O.PaddedBatch(NL, B, Hq, Hkv, D, dtype, fill_bits=fill)
+
+    def rand_bits(shape):
+        x = rng.standard_normal(shape).astype(np.float32)
+        if dtype == O.BF16:
+            return (x.view(np.uint32) >> 16).astype(np.uint16)
+        return x.view(np.uint32)
+
+    for op in ops:
+        outs = None
+        if op[0] == "evict":
+            pb.evict(op[1], release=True)
+        elif op[0] == "embed":
+            ks = [rand_bits((NL, Hkv, n, D)) for n in op[2]]
+            vs = [rand_bits((NL, Hkv, n, D)) for n in op[2]]
+            pb.embed(op[1], op[2], ks, vs)
+        else:
+            if op[0] == "shape":
+                pb.shape_insert(op[1], op[2])
+            T = pb.step_width()
+            pre = (B, T) if op[0] == "shape" else (B,)
+            outs = []
+            for layer in range(NL):
+                q = rand_bits(pre + (Hq, D))
+                kn = rand_bits(pre + (Hkv, D))
+                vn = rand_bits(pre + (Hkv, D))
+                o = pb.decode_layer(layer, q, kn, vn)
+                outs.append((q, o, pb.decode_layer_padded(layer, q)))
+            pb.advance()
+        if check is not None:
+            check(pb, op, outs)
+    return pb
+
+
+def pin_inbatch_prefill_isolation(O):
+    """Sec. 4.1's correctness claim with prefills inside the batch: every query's
+    output over the holey, masked rows equals its output over its own tokens
+    (the new query's: causal over its prompt), and positions without a token
+    are the same ones in both; rows are placeholders except where the mask is 1,
+    where they hold the query's own history in order; the mask has L + 1
+    columns and a row's span reaches its first token."""
+    rng = np.random.default_rng(43)
+
+    def check(pb, op, outs):
+        for _, iso, batched in outs or []:
+            assert np.array_equal(np.isnan(iso), np.isnan(batched))
+            assert np.allclose(np.nan_to_num(iso), np.nan_to_num(batched), rtol=0, atol=1e-12)
+        M = pb.mask()
+        assert M.shape == (pb.B, pb.L + 1)
+        for b in range(pb.B):
+            live = pb.lens[b] > 0
+            assert M[b, pb.L] == (1 if live else 0)
+            ones = np.flatnonzero(M[b, :pb.L])
+            if not live:
+                assert len(ones) == 0 and np.all(pb.K[:, b] == pb.fill)
+                continue
+            assert ones[0] == pb.L - pb.lens[b]
+            want = np.stack([np.stack([O.expected_row_masked(M[b, :pb.L], pb.hist_k[b][l, h], pb.fill, pb.dtype)
+                                       for h in range(pb.Hkv)]) for l in range(pb.NL)])
+            assert np.array_equal(pb.K[:, b], want)
+
+    for trial in range(6):
+        ops = _random_ops_shaped(rng, B=4, steps=14, max_len=6)
+        _run_shaped(O, ops, 2, 4, 4, 2, 8, O.BF16 if trial % 2 else O.F32, seed=200 + trial, check=check)
+
+
+ALL_PINS += [pin_inbatch_prefill_replay, pin_inbatch_prefill_sdpa, pin_inbatch_prefill_isolation]

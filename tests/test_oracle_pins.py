@@ -82,6 +82,20 @@ def _mask_start_aligned(L, lens):
     return M
 
 
+def _pb_mask_no_current_column(self):
+    M = O.PaddedBatch.mask(self)
+    if not self._shape:
+        M[:, -1] = 0
+    return M
+
+
+def _embed_mask_start_aligned(self, slots, lens, k_src, v_src):
+    O.PaddedBatch.embed(self, slots, lens, k_src, v_src)
+    for s, n in zip(slots, lens):
+        self.M[s] = 0
+        self.M[s, :n] = 1
+
+
 def _release_max(self):
     live = self.live()
     r = max(self.L - self.lens[b] for b in live) if live else self.L
@@ -139,6 +153,48 @@ def _decode_gqa_modulo(self, layer, q, k_new, v_new, scale=None):
     return out
 
 
+def _decode_prefill_not_causal(self, layer, q, k_new, v_new, scale=None):
+    # the new query's positions attend over its whole prompt
+    shape = dict(self._shape or {})
+    out = O.PaddedBatch.decode_layer(self, layer, q, k_new, v_new, scale)
+    sc = 1.0 / np.sqrt(self.D) if scale is None else scale
+    g = self.Hq // self.Hkv
+    T = self.step_width()
+    for b, n in shape.items():
+        for t in range(T - n, T):
+            for hq in range(self.Hq):
+                h = hq // g
+                out[b, t, hq] = O.attend(O.widen(q[b, t, hq], self.dtype),
+                                         O.widen(k_new[b, T - n:, h], self.dtype),
+                                         O.widen(v_new[b, T - n:, h], self.dtype), sc)
+    return out
+
+
+def _mask_padding_in_front(self):
+    M = O.PaddedBatch.mask(self)
+    if self._shape:
+        T = self.step_width()
+        for b in range(self.B):
+            if b not in self._shape and self.lens[b] > 0:
+                M[b, self.L], M[b, self.L + T - 1] = M[b, self.L + T - 1], M[b, self.L]
+    return M
+
+
+def _positions_start_aligned(self, b):
+    if self._shape and b in self._shape:
+        return list(range(self._shape[b]))
+    return [0] if self.lens[b] > 0 else []
+
+
+def _advance_span_by_one(self):
+    T = self.step_width()
+    shape = dict(self._shape or {})
+    live = [b for b in range(self.B) if self.lens[b] > 0 and b not in shape]
+    O.PaddedBatch.advance(self)
+    for b in live:
+        self.lens[b] -= T - 1
+
+
 MUTANTS = {
     "scale dropped": dict(attend=_attend_no_scale),
     "keys and values swapped": dict(attend=_attend_kv_swapped),
@@ -147,12 +203,18 @@ MUTANTS = {
     "current token skipped": dict(attend=_attend_drop_last),
     "mask without current column": dict(build_mask=_mask_no_current_column),
     "mask start-aligned": dict(build_mask=_mask_start_aligned),
+    "stateful mask without current column": dict(PB_mask=_pb_mask_no_current_column),
+    "stateful mask start-aligned": dict(PB_embed=_embed_mask_start_aligned),
     "release takes max": dict(PB_release=_release_max),
     "release never drops": dict(PB_release=_release_none),
     "embed start-aligned": dict(PB_embed=_embed_start_aligned),
     "growth on the right": dict(PB_embed=_embed_grow_right),
     "evicted row keeps its values": dict(PB_evict=_evict_no_placeholder),
     "GQA heads interleaved": dict(PB_decode_layer=_decode_gqa_modulo),
+    "prefill not causal": dict(PB_decode_layer=_decode_prefill_not_causal),
+    "padding in front of the latest token": dict(PB_mask=_mask_padding_in_front),
+    "shorter prompt start-aligned": dict(PB__positions=_positions_start_aligned),
+    "span grows by one in a prefill step": dict(PB_advance=_advance_span_by_one),
 }
 
 
