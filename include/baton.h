@@ -12,6 +12,15 @@
  * then runs masked attention for one new token per query (baton_decode_attn)
  * and appends that token's key/value as column L (sec. 4.1, second iteration).
  *
+ * Without prefill/decode separation (sec. 4.1, the Input_token, Attention_mask
+ * and KV_Cache paragraphs), a new query is instead prefilled inside the batch
+ * (baton_shape_insert): that step's input has T positions per row, T the
+ * longest new prompt, the other queries' latest token padded behind to T, and
+ * the cache grows by T columns.  The padding columns stay in the other rows as
+ * holes: placeholders inside a live row that its mask zeroes and attention
+ * skips.  A row's length (its span) then counts the holes between its first
+ * token and the end of the cache; baton_cache_tokens gives its token count.
+ *
  * Conventions
  *  - Every call returns a baton_status.  Arguments and state are checked on the
  *    host before anything is enqueued; on any error nothing is enqueued and the
@@ -53,7 +62,8 @@ typedef enum baton_status {
   BATON_OK = 0,
   BATON_EINVAL = 1,    /* malformed argument: null pointer, size or index out of range, duplicate slot */
   BATON_ESLOT = 2,     /* evicting a free slot, or embedding into a live one */
-  BATON_ECAPACITY = 3, /* the padded length plus the next appended column would exceed capacity */
+  BATON_ECAPACITY = 3, /* the padded length plus the next appended columns would exceed capacity,
+                          or a prefill step would leave more than BATON_MAX_HOLES holes */
   BATON_EDTYPE = 4,    /* unsupported element type, head_dim or head grouping */
   BATON_ESTATE = 5,    /* call out of order with the decode step in progress */
   BATON_EHIP = 6       /* the HIP runtime refused a launch */
@@ -66,6 +76,8 @@ typedef enum baton_dtype { BATON_F32 = 0, BATON_BF16 = 1 } baton_dtype;
 #define BATON_FILL_NEG_INF_BF16 0xFF80u
 
 #define BATON_MAX_BATCH 512
+#define BATON_MAX_PREFILL 64 /* queries prefilled inside the batch in one step */
+#define BATON_MAX_HOLES 64   /* prefill steps whose padding columns are still inside live rows */
 
 /* baton_cache_create flags */
 #define BATON_CREATE_ASSUME_FILLED 1u /* K and V already hold fill_bits everywhere: enqueue nothing */
@@ -112,7 +124,7 @@ baton_status baton_cache_destroy(baton_cache* cache);
  * baton_decode_attn of the next step, or baton_cache_flush, performs whatever
  * is still owed.  With BATON_RELEASE, the columns [0 : min over live rows of
  * (L - len)] are then released (sec. 4.1, "Resources releasing"): L becomes
- * the longest live length (0 when no slot is live).  Release moves no data.
+ * the longest live span (0 when no slot is live).  Release moves no data.
  * Nothing is enqueued.
  * Errors: EINVAL (n < 0, null slots with n > 0, index out of range, duplicate,
  * unknown flag), ESLOT (a slot is free), ESTATE (inside a decode step).
@@ -144,10 +156,10 @@ baton_status baton_kv_embed(baton_cache* cache, const int32_t* slots, int32_t n,
  * host memory and back).  slots: host array of n distinct live slots; k_dst,
  * v_dst: host arrays of n device pointers, each receiving
  * [n_layers][n_kv_heads][len][head_dim] contiguous elements (len = the slot's
- * current length, baton_cache_query), 16-byte aligned -- the layout
- * baton_kv_embed takes, so baton_kv_embed(slot', len, k_dst, v_dst) re-inserts
- * the query into any free slot with its cache bit for bit.  The batch is not
- * changed; preempting a query is extract, then baton_kv_evict.
+ * token count, baton_cache_tokens; holes are skipped), 16-byte aligned -- the
+ * layout baton_kv_embed takes, so baton_kv_embed(slot', len, k_dst, v_dst)
+ * re-inserts the query into any free slot with its tokens bit for bit.  The
+ * batch is not changed; preempting a query is extract, then baton_kv_evict.
  * Errors: EINVAL (n < 0, null arrays or pointers, misaligned pointer, slot out
  * of range, duplicate), ESLOT (a slot is free), ESTATE (inside a decode step),
  * EHIP.
@@ -156,19 +168,46 @@ baton_status baton_kv_extract(const baton_cache* cache, const int32_t* slots, in
                               void* const* k_dst, void* const* v_dst, hipStream_t stream);
 
 /*
+ * Prefill new queries inside the batch in the next step (sec. 4.1, without
+ * prefill/decode separation).  slots, lens: host arrays of n >= 1 entries:
+ * distinct free slots and their prompt lengths.  The next step's input has
+ * T = max(lens) positions per row: a new query's prompt at the last lens[i]
+ * positions, every other live query's latest token at position 0 and padding
+ * behind it.  That step's baton_decode_attn calls take q, k_new, v_new and out
+ * with a position axis of T after the batch axis; baton_build_mask returns
+ * L + T columns; baton_step_advance then grows L by T, leaves a hole of T - 1
+ * columns behind the latest token of every other live row, and makes the new
+ * queries live with lens[i] tokens.  Host metadata only; replaces a previous
+ * registration for the same step.
+ * Errors: EINVAL (n < 1 or > BATON_MAX_PREFILL, null arrays, slot out of range,
+ * duplicate, lens[i] < 1), ESLOT (a slot is live), ECAPACITY (L + T >
+ * capacity, or more than BATON_MAX_HOLES holes would remain), ESTATE (inside a
+ * decode step).
+ */
+baton_status baton_shape_insert(baton_cache* cache, const int32_t* slots, int32_t n,
+                                const int32_t* lens);
+
+/*
  * The 0-1 attention mask of the current step (sec. 2.1, "Batch-wise inference";
  * sec. 4.1: a column of ones for the current token, zero rows for finished
  * queries; sec. 4.2: zeros over the grown front of existing rows).  Writes
- * mask[b * ld + j] for 0 <= j <= L: 1 when slot b is live and j >= L - len_b,
- * else 0.  Column L is the token being decoded.  mask: device uint8, >= batch
- * rows of ld bytes.  Bytes at j > L are not touched.
- * Errors: EINVAL (null mask, ld < L + 1), EHIP.
+ * mask[b * ld + j] for 0 <= j < L + T (T = 1, or the prefill width after
+ * baton_shape_insert): for a live slot, 1 on its own tokens' columns and on
+ * column L (its token being decoded), 0 on its holes, in front of its first
+ * token and after column L; for a slot being prefilled, 1 on its prompt's
+ * columns (the last lens[i] ones), else 0; 0 for a free slot.  This is the
+ * paper's mask: with a prefill it is l_am + l_q - 1 wide, l_am = L + 1.
+ * mask: device uint8, >= batch rows of ld bytes.  Bytes at j >= L + T are
+ * not touched.
+ * Errors: EINVAL (null mask, ld < L + T), EHIP.
  */
 baton_status baton_build_mask(const baton_cache* cache, uint8_t* mask, int64_t ld,
                               hipStream_t stream);
 
-/* Bytes of device workspace baton_decode_attn needs for this cache (fixed until
-   baton_set_split_tokens changes the split setting). */
+/* Bytes of device workspace baton_decode_attn needs for this cache in its
+   current state.  Fixed while no prefill step has left holes; otherwise it
+   grows with their number, so query it again after baton_step_advance and
+   baton_kv_evict. */
 size_t baton_decode_attn_workspace_bytes(const baton_cache* cache);
 
 /*
@@ -182,8 +221,18 @@ size_t baton_decode_attn_workspace_bytes(const baton_cache* cache);
  * are skipped, never read into arithmetic.  Free slots: nothing appended, out
  * rows set to 0.  Arithmetic in fp32; out rounded to nearest-even in the
  * cache's dtype.
+ * Live rows' holes are skipped like placeholders.
  * q, out: device [batch][n_q_heads][head_dim]; k_new, v_new: device
- * [batch][n_kv_heads][head_dim]; all 16-byte aligned.  scale = 0 selects
+ * [batch][n_kv_heads][head_dim]; all 16-byte aligned.
+ * In a step registered by baton_shape_insert, q and out are
+ * [batch][T][n_q_heads][head_dim] and k_new, v_new [batch][T][n_kv_heads]
+ * [head_dim]: a live slot's position 0 is decoded as above (positions 1 .. T-1
+ * are padding; only position 0 is appended); a slot being prefilled attends
+ * causally over its own prompt -- its position T - l + i over prompt positions
+ * T - l .. T - l + i -- and all l prompt positions are appended as columns
+ * L + T - l .. L + T - 1.  out is written at positions that hold a token and at
+ * position 0 of free slots (zeros); other positions are not touched.
+ * scale = 0 selects
  * 1/sqrt(head_dim).  ws: device workspace of >= baton_decode_attn_workspace_bytes
  * bytes, 16-byte aligned, used by one cache at a time; its contents are the
  * library's between calls.  Call once per layer per step, then
@@ -207,18 +256,29 @@ baton_status baton_cache_flush(baton_cache* cache, hipStream_t stream);
 /*
  * Close the decode step once every layer has been decoded: L += 1 and every
  * live slot's length += 1 (sec. 4.1: cache and mask grow by one column per
- * iteration).  Host metadata only.
+ * iteration); after a prefill step L += T, every other live slot's length
+ * += T (its new hole included) and the prefilled slots become live.  Host
+ * metadata only.
  * Errors: ESTATE (some layer not decoded this step).
  */
 baton_status baton_step_advance(baton_cache* cache);
 
 /*
  * Current metadata: padded length L, ring base (physical column of logical
- * column 0), and per-slot lengths (host array of batch entries, 0 = free).
- * Any output pointer may be NULL.  A caller applying rotary position
- * embeddings uses position len_b for slot b's next token.
+ * column 0), and per-slot lengths (host array of batch entries, 0 = free): a
+ * live slot's span L - (column of its first token), holes included.  Any
+ * output pointer may be NULL.
  */
 baton_status baton_cache_query(const baton_cache* cache, int64_t* L, int64_t* base, int32_t* lens);
+
+/*
+ * Per-slot token counts (host array of batch entries, 0 = free): the span
+ * without its holes, i.e. the length of the query's own history.  A caller
+ * applying rotary position embeddings uses position tokens[b] for slot b's
+ * next token.
+ * Errors: EINVAL (null pointer).
+ */
+baton_status baton_cache_tokens(const baton_cache* cache, int32_t* tokens);
 
 /*
  * Tuning: tokens per split of a row in baton_decode_attn (a multiple of 64,

@@ -19,6 +19,8 @@ BATON_F32, BATON_BF16 = 0, 1
 BATON_FILL_NEG_INF_F32 = 0xFF800000
 BATON_FILL_NEG_INF_BF16 = 0xFF80
 BATON_MAX_BATCH = 512
+BATON_MAX_PREFILL = 64
+BATON_MAX_HOLES = 64
 BATON_CREATE_ASSUME_FILLED = 1
 BATON_RELEASE = 1
 
@@ -55,6 +57,8 @@ def lib():
         L.baton_kv_evict.argtypes = [vp, P(i32), i32, u32, vp]
         L.baton_kv_embed.argtypes = [vp, P(i32), i32, P(i32), P(vp), P(vp), vp]
         L.baton_kv_extract.argtypes = [vp, P(i32), i32, P(vp), P(vp), vp]
+        L.baton_shape_insert.argtypes = [vp, P(i32), i32, P(i32)]
+        L.baton_cache_tokens.argtypes = [vp, P(i32)]
         L.baton_build_mask.argtypes = [vp, vp, i64, vp]
         L.baton_decode_attn_workspace_bytes.argtypes = [vp]
         L.baton_decode_attn_workspace_bytes.restype = ctypes.c_size_t
@@ -68,7 +72,8 @@ def lib():
         for name in ("baton_cache_create", "baton_cache_destroy", "baton_kv_evict", "baton_kv_embed",
                      "baton_kv_extract",
                      "baton_build_mask", "baton_decode_attn", "baton_step_advance",
-                     "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush"):
+                     "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
+                     "baton_shape_insert", "baton_cache_tokens"):
             getattr(L, name).restype = st
         _lib = L
     return _lib
@@ -138,6 +143,21 @@ def baton_kv_extract(cache, slots, k_dst, v_dst, stream=None):
     ks = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in k_dst])
     vs = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in v_dst])
     _check(lib().baton_kv_extract(cache, s_arr, n, ks, vs, _stream(stream)), "baton_kv_extract")
+
+
+def baton_shape_insert(cache, slots, lens):
+    s_arr, n = _i32s(slots)
+    l_arr, nl = _i32s(lens)
+    if nl != n:
+        raise ValueError("slots and lens must have the same length")
+    _check(lib().baton_shape_insert(cache, s_arr, n, l_arr), "baton_shape_insert")
+
+
+def baton_cache_tokens(cache, batch):
+    """Per-slot token counts (list)."""
+    out = (ctypes.c_int32 * batch)()
+    _check(lib().baton_cache_tokens(cache, out), "baton_cache_tokens")
+    return list(out)
 
 
 def baton_build_mask(cache, mask, ld, stream=None):

@@ -43,6 +43,7 @@ class BatonCache:
         flags = B.BATON_CREATE_ASSUME_FILLED if assume_filled else 0
         self.handle = B.baton_cache_create(desc, flags, _cur_stream())
         self._ws = None
+        self.step_width = 1   # input positions per row of the next step
 
     # -- workspace --
     def workspace(self):
@@ -64,10 +65,21 @@ class BatonCache:
         B.baton_kv_embed(self.handle, slots, lens, k_src, v_src,
                          stream if stream is not None else _cur_stream())
 
+    def shape_insert(self, slots, lens):
+        """Prefill these queries inside the batch in the next step (no prefill/decode
+        separation); that step's inputs and outputs have a position axis of
+        max(lens) after the batch axis."""
+        B.baton_shape_insert(self.handle, slots, lens)
+        self.step_width = max(int(x) for x in lens)
+
+    def tokens(self):
+        """Per-slot token counts (spans without holes)."""
+        return B.baton_cache_tokens(self.handle, self.batch)
+
     def extract(self, slots, stream=None):
         """The slots' cached K and V as new device tensors [n_layers][n_kv_heads][len][head_dim]."""
         import torch
-        lens = self.query()[2]
+        lens = self.tokens()
         ks, vs = [], []
         for s in slots:
             shape = (self.n_layers, self.n_kv_heads, max(lens[s], 0), self.head_dim)
@@ -80,14 +92,24 @@ class BatonCache:
         import torch
         L = self.query()[0]
         if out is None:
-            out = torch.empty((self.batch, L + 1), dtype=torch.uint8, device=self.k.device)
+            out = torch.empty((self.batch, L + self.step_width), dtype=torch.uint8, device=self.k.device)
         B.baton_build_mask(self.handle, out, out.stride(0), stream if stream is not None else _cur_stream())
         return out
 
     def decode_attn(self, layer, q, k_new, v_new, out=None, scale=0.0, stream=None):
+        """q, out: [batch][n_q_heads][head_dim] ([batch][T][...] in a prefill step);
+        k_new, v_new: the same with n_kv_heads."""
         import torch
         if out is None:
             out = torch.empty_like(q)
+        T = self.step_width
+        want_q = self.batch * T * self.n_q_heads * self.head_dim
+        want_kv = self.batch * T * self.n_kv_heads * self.head_dim
+        for name, t, n in (("q", q, want_q), ("k_new", k_new, want_kv), ("v_new", v_new, want_kv),
+                           ("out", out, want_q)):
+            if t.dtype != self.k.dtype or not t.is_contiguous() or t.numel() != n:
+                raise ValueError(f"{name}: expected {n} contiguous {self.k.dtype} elements, "
+                                 f"got {t.numel()} {t.dtype}")
         ws = self.workspace()
         B.baton_decode_attn(self.handle, layer, q, k_new, v_new, out, scale, ws, ws.numel(),
                             stream if stream is not None else _cur_stream())
@@ -99,6 +121,7 @@ class BatonCache:
 
     def advance(self):
         B.baton_step_advance(self.handle)
+        self.step_width = 1
 
     def query(self):
         """(L, base, lens)."""

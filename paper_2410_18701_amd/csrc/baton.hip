@@ -13,6 +13,7 @@
 #include "decode_attn.hpp"
 #include "decode_attn_mfma.hpp"
 #include "kv_ops.hpp"
+#include "prefill_attn.hpp"
 
 #ifndef BATON_GQA_MFMA
 #define BATON_GQA_MFMA 1   // grouped-query bf16 attention on the matrix cores
@@ -21,7 +22,20 @@
 #define BATON_MFMA_MIN_GROUP 2   // smallest q-heads per kv-head that takes the matrix-core kernel
 #endif
 
+#ifndef BATON_PREFILL_MFMA
+#define BATON_PREFILL_MFMA 1   // bf16 prefill attention on the matrix cores
+#endif
+
 static_assert(BATON_MAX_BATCH == baton::kMetaThreads, "meta kernel covers every slot");
+static_assert(BATON_MAX_HOLES == baton::kMaxHoles, "hole list size");
+static_assert(BATON_MAX_PREFILL == baton::kMaxPrefill, "prefill list size");
+
+// A hole: the padding columns a prefill step inside the batch left behind the
+// latest token of the rows live at that time, as absolute columns [a0, a1)
+// (absolute column of logical column j: j + vend - L).
+struct baton_hole {
+  int64_t a0, a1, id;
+};
 
 struct baton_cache {
   baton_cache_desc d;
@@ -38,6 +52,15 @@ struct baton_cache {
   std::vector<int32_t> pending;
   std::vector<uint8_t> layer_done;
   int32_t n_done = 0;      // layers decoded in the current step
+  // Columns appended since creation; the absolute column of logical column L.
+  int64_t vend = 0;
+  std::vector<baton_hole> holes;   // by id, which is also column order
+  int64_t next_hole = 0;
+  std::vector<int64_t> epoch;      // per slot: the holes with id >= epoch lie in its row
+  // Prefill registered for the next step: prompt length per slot (0: none).
+  std::vector<int32_t> plen;
+  int32_t n_prefill = 0;
+  int32_t step_T = 1;              // input positions per row in the next step
   // Work list of the current step as last written into a workspace.
   const void* meta_ws = nullptr;
   bool meta_valid = false;
@@ -64,6 +87,47 @@ int64_t ring(int64_t x, int64_t cap) {
   return x < 0 ? x + cap : x;
 }
 
+// Index in c->holes of slot b's first hole.
+int32_t first_hole(const baton_cache* c, int32_t b) {
+  int32_t k = 0;
+  while (k < (int32_t)c->holes.size() && c->holes[k].id < c->epoch[b]) ++k;
+  return k;
+}
+
+// The holes in logical columns of the current step.
+baton::HoleList hole_list(const baton_cache* c) {
+  baton::HoleList hl;
+  std::memset(&hl, 0, sizeof(hl));
+  hl.n = (int32_t)c->holes.size();
+  const int64_t shift = c->vend - c->L;
+  for (int32_t k = 0; k < hl.n; ++k) {
+    hl.col[k][0] = (int32_t)(c->holes[k].a0 - shift);
+    hl.col[k][1] = (int32_t)(c->holes[k].a1 - shift);
+  }
+  return hl;
+}
+
+// Cached tokens of a live slot: its span without its holes.
+int32_t row_tokens(const baton_cache* c, int32_t b, const baton::HoleList& hl) {
+  const int32_t n = c->lens[b];
+  if (n <= 0) return 0;
+  int32_t cnt = 0;
+  baton::row_runs(hl, first_hole(c, b), c->L, n, [&](int32_t t0, int32_t t1) { cnt += t1 - t0; });
+  return cnt - 1;   // without the current token
+}
+
+// Forget holes that no live row holds: those released from the front, or
+// older than every live row's first hole.
+void drop_holes(baton_cache* c) {
+  int64_t min_epoch = INT64_MAX;
+  for (int32_t b = 0; b < c->d.batch; ++b)
+    if (c->lens[b] > 0) min_epoch = std::min(min_epoch, c->epoch[b]);
+  const int64_t shift = c->vend - c->L;
+  size_t k = 0;
+  while (k < c->holes.size() && (c->holes[k].id < min_epoch || c->holes[k].a1 - shift <= 0)) ++k;
+  c->holes.erase(c->holes.begin(), c->holes.begin() + k);
+}
+
 // Automatic split: enough items to fill the GPU about twice over at the
 // occupancy of these kernels, never smaller than 256 tokens (per-item set-up
 // and partial records) nor larger than 1024 (the merge and the tail).
@@ -79,8 +143,9 @@ struct WsLayout {
 WsLayout ws_layout(const baton_cache* c) {
   WsLayout w;
   const int64_t B = c->d.batch;
-  const int64_t smin = c->split > 0 ? c->split : kAutoSplitMin;   // most items a row can have
-  w.max_items = B * ((c->d.capacity + smin - 1) / smin);
+  // Most items a row can have: its tokens cut at every split and every hole.
+  const int64_t smin = c->split > 0 ? c->split : kAutoSplitMin;
+  w.max_items = B * ((c->d.capacity + smin - 1) / smin + (int64_t)c->holes.size() + 1);
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   w.items_off = 0;
   w.multi_off = up(w.items_off + sizeof(baton::Item) * w.max_items);
@@ -96,6 +161,8 @@ struct Seg {
   int64_t col0;
   const void* ks;   // contiguous side (null: placeholders)
   const void* vs;
+  int32_t ext_len = 0;   // tokens per (layer, head) of the contiguous side; 0: len
+  int32_t ext_t0 = 0;    // the segment's first token there
 };
 
 template <int VPT>
@@ -124,6 +191,8 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
       a.len[used] = g.len;
       a.col0[used] = g.col0;
       a.tiles_per_row[used] = tpr;
+      a.ext_len[used] = g.ext_len > 0 ? g.ext_len : g.len;
+      a.ext_t0[used] = g.ext_t0;
       a.kext[used] = static_cast<uint32_t*>(const_cast<void*>(g.ks));
       a.vext[used] = static_cast<uint32_t*>(const_cast<void*>(g.vs));
       tiles += (int64_t)tpr * 2 * c->d.n_layers * c->d.n_kv_heads;
@@ -195,6 +264,33 @@ bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, hipStream_t s) 
   return launch_attn_d<baton::BF16Tag, 128>(c->group, a, I, M, H, s);
 }
 
+template <int D, int G>
+void launch_prefill_g(const baton_cache* c, baton::PrefillArgs& a, hipStream_t s) {
+  const bool mfma = BATON_PREFILL_MFMA && c->d.dtype == BATON_BF16;
+  const int32_t per_tile = mfma ? 16 : baton::kWave / (D * c->esz / 16);
+  int32_t tiles = 0;
+  for (int32_t i = 0; i < a.n_ins; ++i) {
+    tiles += (a.plen[i] + per_tile - 1) / per_tile;
+    a.tile_end[i] = tiles;
+  }
+  const dim3 grid((unsigned)tiles, (unsigned)(c->d.n_kv_heads * G));
+  if (mfma)
+    hipLaunchKernelGGL((baton::prefill_mfma_kernel<D, G>), grid, dim3(baton::kWave), 0, s, a);
+  else if (c->d.dtype == BATON_BF16)
+    hipLaunchKernelGGL((baton::prefill_valu_kernel<baton::BF16Tag, D, G>), grid, dim3(baton::kWave), 0, s, a);
+  else
+    hipLaunchKernelGGL((baton::prefill_valu_kernel<baton::F32Tag, D, G>), grid, dim3(baton::kWave), 0, s, a);
+}
+
+template <int D>
+void launch_prefill_d(const baton_cache* c, baton::PrefillArgs& a, hipStream_t s) {
+  switch (c->group) {
+    case 1: launch_prefill_g<D, 1>(c, a, s); break;
+    case 2: launch_prefill_g<D, 2>(c, a, s); break;
+    case 4: launch_prefill_g<D, 4>(c, a, s); break;
+    default: launch_prefill_g<D, 8>(c, a, s); break;
+  }
+}
 
 int32_t auto_split(const baton_cache* c) {
   int64_t rows_tokens = 0;
@@ -262,6 +358,8 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   c->split = 0;
   c->lens.assign(d.batch, 0);
   c->pending.assign(d.batch, 0);
+  c->epoch.assign(d.batch, 0);
+  c->plen.assign(d.batch, 0);
   c->layer_done.assign(d.n_layers, 0);
   if (!(flags & BATON_CREATE_ASSUME_FILLED)) {
     const int64_t n_vec = (int64_t)d.n_layers * d.batch * d.n_kv_heads * d.capacity * c->vpt;
@@ -287,7 +385,7 @@ baton_status baton_cache_destroy(baton_cache* c) {
 baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uint32_t flags,
                             hipStream_t stream) {
   if (!c || n < 0 || (n > 0 && !slots) || (flags & ~BATON_RELEASE)) return BATON_EINVAL;
-  if (c->n_done) return BATON_ESTATE;
+  if (c->n_done || c->n_prefill) return BATON_ESTATE;
   std::vector<uint8_t> seen(c->d.batch, 0);
   for (int32_t i = 0; i < n; ++i) {
     const int32_t s = slots[i];
@@ -311,6 +409,7 @@ baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uin
     c->base = ring(c->base + r, c->d.capacity);
     c->L -= r;
   }
+  drop_holes(c);
   c->meta_valid = false;
   return BATON_OK;
 }
@@ -320,7 +419,7 @@ baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, con
                             hipStream_t stream) {
   if (!c || n < 0) return BATON_EINVAL;
   if (n > 0 && (!slots || !lens || !k_src || !v_src)) return BATON_EINVAL;
-  if (c->n_done) return BATON_ESTATE;
+  if (c->n_done || c->n_prefill) return BATON_ESTATE;
   std::vector<uint8_t> seen(c->d.batch, 0);
   int64_t longest = 0;
   for (int32_t i = 0; i < n; ++i) {
@@ -356,6 +455,7 @@ baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, con
   for (int32_t i = 0; i < n; ++i) {
     c->lens[slots[i]] = lens[i];
     c->pending[slots[i]] = 0;
+    c->epoch[slots[i]] = c->next_hole;   // no earlier hole lies in its row
   }
   c->meta_valid = false;
   return BATON_OK;
@@ -365,7 +465,7 @@ baton_status baton_kv_extract(const baton_cache* c, const int32_t* slots, int32_
                               void* const* v_dst, hipStream_t stream) {
   if (!c || n < 0) return BATON_EINVAL;
   if (n > 0 && (!slots || !k_dst || !v_dst)) return BATON_EINVAL;
-  if (c->n_done) return BATON_ESTATE;
+  if (c->n_done || c->n_prefill) return BATON_ESTATE;
   std::vector<uint8_t> seen(c->d.batch, 0);
   for (int32_t i = 0; i < n; ++i) {
     const int32_t s = slots[i];
@@ -375,26 +475,68 @@ baton_status baton_kv_extract(const baton_cache* c, const int32_t* slots, int32_
   }
   for (int32_t i = 0; i < n; ++i)
     if (c->lens[slots[i]] == 0) return BATON_ESLOT;
+  // One segment per run of consecutive tokens, packed end to end in the buffer.
+  const baton::HoleList hl = hole_list(c);
   std::vector<Seg> segs;
   segs.reserve(n);
   for (int32_t i = 0; i < n; ++i) {
     const int32_t s = slots[i], len = c->lens[s];
-    segs.push_back({s, len, ring(c->base + c->L - len, c->d.capacity), k_dst[i], v_dst[i]});
+    const int32_t ntok = row_tokens(c, s, hl);
+    int32_t done = 0;
+    baton::row_runs(hl, first_hole(c, s), c->L, len, [&](int32_t t0, int32_t t1) {
+      t1 = std::min(t1, len);   // the current token is not cached yet
+      if (t1 <= t0) return;
+      Seg g{s, t1 - t0, ring(c->base + c->L - len + t0, c->d.capacity), k_dst[i], v_dst[i]};
+      g.ext_len = ntok;
+      g.ext_t0 = done;
+      segs.push_back(g);
+      done += t1 - t0;
+    });
   }
   return launch_segs(c, segs, stream, /*extract=*/true);
 }
 
+baton_status baton_shape_insert(baton_cache* c, const int32_t* slots, int32_t n, const int32_t* lens) {
+  if (!c || n < 1 || n > BATON_MAX_PREFILL || !slots || !lens) return BATON_EINVAL;
+  if (c->n_done) return BATON_ESTATE;
+  std::vector<uint8_t> seen(c->d.batch, 0);
+  int32_t T = 1;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = slots[i];
+    if (s < 0 || s >= c->d.batch || seen[s] || lens[i] < 1) return BATON_EINVAL;
+    seen[s] = 1;
+    T = std::max(T, lens[i]);
+  }
+  for (int32_t i = 0; i < n; ++i)
+    if (c->lens[slots[i]] != 0) return BATON_ESLOT;
+  if (c->L + T > c->d.capacity) return BATON_ECAPACITY;
+  bool others = false;
+  for (int32_t b = 0; b < c->d.batch; ++b) others |= c->lens[b] > 0;
+  if (T > 1 && others && (int32_t)c->holes.size() + 1 > BATON_MAX_HOLES) return BATON_ECAPACITY;
+  std::fill(c->plen.begin(), c->plen.end(), 0);
+  for (int32_t i = 0; i < n; ++i) c->plen[slots[i]] = lens[i];
+  c->n_prefill = n;
+  c->step_T = T;
+  c->meta_valid = false;
+  return BATON_OK;
+}
+
 baton_status baton_build_mask(const baton_cache* c, uint8_t* mask, int64_t ld, hipStream_t stream) {
-  if (!c || !mask || ld < c->L + 1) return BATON_EINVAL;
+  if (!c || !mask || ld < c->L + c->step_T) return BATON_EINVAL;
   baton::MaskArgs a;
   std::memset(&a, 0, sizeof(a));
   a.mask = mask;
   a.ld = ld;
   a.L = c->L;
+  a.T = c->step_T;
   a.batch = c->d.batch;
-  for (int32_t b = 0; b < c->d.batch; ++b) a.lens[b] = c->lens[b];
+  a.holes = hole_list(c);
+  for (int32_t b = 0; b < c->d.batch; ++b) {
+    a.lens[b] = c->plen[b] > 0 ? -c->plen[b] : c->lens[b];
+    a.first[b] = (uint8_t)first_hole(c, b);
+  }
   const int64_t per_block = 256 * 4;
-  const int64_t bx = std::min<int64_t>((c->L + 1 + per_block - 1) / per_block, 1024);
+  const int64_t bx = std::min<int64_t>((c->L + c->step_T + per_block - 1) / per_block, 1024);
   hipLaunchKernelGGL(baton::mask_kernel, dim3((unsigned)bx, c->d.batch), dim3(256), 0, stream, a);
   return hip_status(hipGetLastError());
 }
@@ -414,7 +556,7 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   const WsLayout w = ws_layout(c);
   if (ws_bytes < w.total) return BATON_EINVAL;
   if (c->layer_done[layer]) return BATON_ESTATE;
-  if (c->L + 1 > c->d.capacity) return BATON_ECAPACITY;
+  if (c->L + c->step_T > c->d.capacity) return BATON_ECAPACITY;
   if (c->n_done == 0) {
     const baton_status st = flush_pending(c, stream);
     if (st != BATON_OK) return st;
@@ -423,16 +565,20 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   if (!c->meta_valid || c->meta_ws != ws) {
     baton::MetaArgs m;
     std::memset(&m, 0, sizeof(m));
+    m.L = c->L;
     m.batch = c->d.batch;
     c->step_split = c->split > 0 ? c->split : auto_split(c);
     m.split = c->step_split;
-    int64_t items = 0, multi = 0;   // as meta_kernel counts them: one item for a free slot
+    m.holes = hole_list(c);
+    int64_t items = 0, multi = 0;   // as meta_kernel counts them
     for (int32_t b = 0; b < c->d.batch; ++b) {
-      m.lens[b] = c->lens[b];
-      const int64_t cnt = c->lens[b] > 0 ? (c->lens[b] + m.split) / m.split : 1;
+      m.lens[b] = c->plen[b] > 0 ? -1 : c->lens[b];   // a row prefilled this step has no item
+      m.first[b] = (uint8_t)first_hole(c, b);
+      const int64_t cnt = baton::row_items(m, b);
       items += cnt;
       multi += cnt > 1;
     }
+    if (items > w.max_items) return BATON_EINVAL;   // cannot happen: the layout bounds every row
     hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, m,
                        reinterpret_cast<baton::Item*>(wsb + w.items_off),
                        reinterpret_cast<int4*>(wsb + w.multi_off));
@@ -463,11 +609,40 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.n_kv_heads = c->d.n_kv_heads;
   a.split = c->step_split;
   a.n_items = c->n_items;
+  a.tw = c->step_T;
   const float sc = scale == 0.f ? 1.0f / std::sqrt((float)c->d.head_dim) : scale;
   a.qscale = sc * 1.4426950408889634f;
-  if (!launch_attn(c, a, stream)) return BATON_EDTYPE;
-  const baton_status st = hip_status(hipGetLastError());
+  if (c->n_items > 0 && !launch_attn(c, a, stream)) return BATON_EDTYPE;
+  baton_status st = hip_status(hipGetLastError());
   if (st != BATON_OK) return st;
+  if (c->n_prefill > 0) {
+    baton::PrefillArgs p;
+    std::memset(&p, 0, sizeof(p));
+    p.k = static_cast<uint32_t*>(c->d.k);
+    p.v = static_cast<uint32_t*>(c->d.v);
+    p.q = a.q;
+    p.knew = a.knew;
+    p.vnew = a.vnew;
+    p.out = a.out;
+    p.cap = c->d.capacity;
+    p.base = c->base;
+    p.L = c->L;
+    p.T = c->step_T;
+    p.layer = layer;
+    p.batch = c->d.batch;
+    p.n_kv_heads = c->d.n_kv_heads;
+    p.qscale = a.qscale;
+    for (int32_t b = 0; b < c->d.batch; ++b)
+      if (c->plen[b] > 0) {
+        p.slot[p.n_ins] = b;
+        p.plen[p.n_ins] = c->plen[b];
+        ++p.n_ins;
+      }
+    if (c->d.head_dim == 64) launch_prefill_d<64>(c, p, stream);
+    else launch_prefill_d<128>(c, p, stream);
+    st = hip_status(hipGetLastError());
+    if (st != BATON_OK) return st;
+  }
   c->layer_done[layer] = 1;
   ++c->n_done;
   return BATON_OK;
@@ -481,9 +656,29 @@ baton_status baton_cache_flush(baton_cache* c, hipStream_t stream) {
 baton_status baton_step_advance(baton_cache* c) {
   if (!c) return BATON_EINVAL;
   if (c->n_done != c->d.n_layers) return BATON_ESTATE;
-  c->L += 1;
-  for (int32_t b = 0; b < c->d.batch; ++b)
-    if (c->lens[b] > 0) c->lens[b] += 1;
+  const int32_t T = c->step_T;
+  if (c->n_prefill > 0) {
+    // The other live rows keep padding columns L + 1 .. L + T - 1 as a hole.
+    bool others = false;
+    for (int32_t b = 0; b < c->d.batch; ++b) others |= c->lens[b] > 0 && c->plen[b] == 0;
+    if (T > 1 && others) c->holes.push_back({c->vend + 1, c->vend + T, c->next_hole++});
+    for (int32_t b = 0; b < c->d.batch; ++b) {
+      if (c->plen[b] > 0) {
+        c->lens[b] = c->plen[b];
+        c->epoch[b] = c->next_hole;
+        c->plen[b] = 0;
+      } else if (c->lens[b] > 0) {
+        c->lens[b] += T;
+      }
+    }
+    c->n_prefill = 0;
+    c->step_T = 1;
+  } else {
+    for (int32_t b = 0; b < c->d.batch; ++b)
+      if (c->lens[b] > 0) c->lens[b] += 1;
+  }
+  c->L += T;
+  c->vend += T;
   std::fill(c->layer_done.begin(), c->layer_done.end(), 0);
   c->n_done = 0;
   c->meta_valid = false;
@@ -495,6 +690,13 @@ baton_status baton_cache_query(const baton_cache* c, int64_t* L, int64_t* base, 
   if (L) *L = c->L;
   if (base) *base = c->base;
   if (lens) std::copy(c->lens.begin(), c->lens.end(), lens);
+  return BATON_OK;
+}
+
+baton_status baton_cache_tokens(const baton_cache* c, int32_t* tokens) {
+  if (!c || !tokens) return BATON_EINVAL;
+  const baton::HoleList hl = hole_list(c);
+  for (int32_t b = 0; b < c->d.batch; ++b) tokens[b] = row_tokens(c, b, hl);
   return BATON_OK;
 }
 

@@ -108,4 +108,32 @@ __device__ __forceinline__ int64_t ring_add(int64_t a, int64_t b, int64_t cap) {
   return s >= cap ? s - cap : s;
 }
 
+constexpr int kMaxHoles = 64;       // == BATON_MAX_HOLES
+
+// Holes of live rows: the padding columns a prefill step inside the batch
+// leaves behind the latest token of the other rows.  Hole k covers the
+// logical columns [col0[k], col1[k]); holes are sorted by column, and a row's
+// holes are a suffix of the list, from index first[b].
+struct HoleList {
+  int32_t n;
+  int32_t col[kMaxHoles][2];
+};
+
+// Calls f(t0, t1) for each run of consecutive tokens of a live row with n
+// cached tokens (token t is logical column L - n + t; token n is the current
+// one): [0, n + 1) without the row's holes.
+template <typename F>
+__host__ __device__ __forceinline__ void row_runs(const HoleList& hl, int32_t first, int64_t L,
+                                                  int32_t n, F&& f) {
+  const int64_t c0 = L - n;
+  int32_t t = 0;
+  for (int k = first; k < hl.n; ++k) {
+    const int32_t h0 = (int32_t)(hl.col[k][0] - c0), h1 = (int32_t)(hl.col[k][1] - c0);
+    if (h1 <= 0 || h0 > n) continue;   // outside the row (never for a row's own holes)
+    if (h0 > t) f(t, h0);
+    t = h1 > t ? h1 : t;
+  }
+  if (t < n + 1) f(t, n + 1);
+}
+
 }  // namespace baton

@@ -1,11 +1,11 @@
 // Masked batched decode attention over the aligned ring cache, split over the
 // sequence ("split-K") so that long and skewed rows spread over all CUs.
 //
-// Work item = (slot b, split c) x kv-head h: the tokens t in
-// [c*S, min((c+1)*S, len_b+1)) of row (layer, b, h), where token t < len_b is
-// cache column L - len_b + t and token len_b is the current token (k_new/v_new,
-// appended to the cache by the item that holds it).  Placeholder columns are
-// never addressed.  One wave per item: a token row of D elements is spread
+// Work item = (slot b, split c) x kv-head h: a range of at most S tokens t of
+// row (layer, b, h) inside one run of consecutive tokens, where token t <
+// len_b is cache column L - len_b + t and token len_b is the current token
+// (k_new/v_new, appended to the cache by the item that holds it).  Placeholder
+// columns, holes included, are never addressed.  One wave per item: a token row of D elements is spread
 // over LPT = D*elem/16 lanes (16 bytes each), so one wave instruction reads
 // TPI = 64/LPT whole token rows; each of those TPI lane groups keeps its own
 // online-softmax state (max m, sum l, weighted values acc) over the tokens it
@@ -29,11 +29,13 @@ namespace baton {
 
 constexpr int kMetaThreads = 512;   // == BATON_MAX_BATCH
 
-
 struct MetaArgs {
+  int64_t L;
   int32_t batch;
   int32_t split;                    // tokens per item
-  int32_t lens[kMetaThreads];
+  int32_t lens[kMetaThreads];       // cached tokens (span); 0 free; -1 prefilled this step (no item)
+  uint8_t first[kMetaThreads];      // index of the row's first hole
+  HoleList holes;
 };
 
 // One work item: the tokens [t_begin, t_end) of slot b's row (n = len_b
@@ -44,6 +46,17 @@ struct Item {
   int4 row;      // (first item of the row, items of the row, 0, 0)
 };
 
+// Items of a live row: each run of tokens cut into pieces of at most `split`.
+__host__ __device__ __forceinline__ int32_t row_items(const MetaArgs& a, int b) {
+  const int32_t n = a.lens[b];
+  if (n < 0) return 0;
+  if (n == 0) return 1;
+  int32_t cnt = 0;
+  row_runs(a.holes, a.first[b], a.L, n,
+           [&](int32_t t0, int32_t t1) { cnt += (t1 - t0 + a.split - 1) / a.split; });
+  return cnt;
+}
+
 // Builds the per-step work list in the workspace: one descriptor per item, so
 // that an item needs a single load to start, and the list of rows with
 // several items (first item, item count, slot) for combine_kernel.
@@ -53,7 +66,7 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   __shared__ int32_t scan_multi[kMetaThreads];
   const int b = threadIdx.x;
   const int32_t n = b < a.batch ? a.lens[b] : 0;
-  const int32_t cnt = b < a.batch ? (n > 0 ? (n + a.split) / a.split : 1) : 0;  // ceil((n+1)/split)
+  const int32_t cnt = b < a.batch ? row_items(a, b) : 0;
   scan[b] = cnt;
   scan_multi[b] = cnt > 1 ? 1 : 0;
   __syncthreads();
@@ -66,13 +79,16 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
     __syncthreads();
   }
   const int32_t first = scan[b] - cnt;
-  if (b < a.batch) {
-    for (int32_t c = 0; c < cnt; ++c) {
-      Item it;
-      it.span = n > 0 ? make_int4(b, c * a.split, min((c + 1) * a.split, n + 1), n)
-                      : make_int4(b, 0, 0, -1);
-      it.row = make_int4(first, cnt, 0, 0);
-      ws_items[first + c] = it;
+  if (b < a.batch && cnt > 0) {
+    const int4 row = make_int4(first, cnt, 0, 0);
+    if (n == 0) {
+      ws_items[first] = Item{make_int4(b, 0, 0, -1), row};
+    } else {
+      int32_t c = first;
+      row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
+        for (int32_t t = t0; t < t1; t += a.split)
+          ws_items[c++] = Item{make_int4(b, t, min(t + a.split, t1), n), row};
+      });
     }
     if (cnt > 1) ws_multi[scan_multi[b] - 1] = make_int4(first, cnt, b, 0);
   }
@@ -82,15 +98,16 @@ struct AttnArgs {
   const uint32_t* k;         // ring buffers (whole cache), 32-bit words
   uint32_t* v;
   uint32_t* k_w;             // same as k, writable (append)
-  const uint32_t* q;         // [batch][n_q_heads][D]
-  const uint32_t* knew;      // [batch][n_kv_heads][D]
+  const uint32_t* q;         // [batch][tw][n_q_heads][D], position 0 decoded
+  const uint32_t* knew;      // [batch][tw][n_kv_heads][D]
   const uint32_t* vnew;
-  uint32_t* out;             // [batch][n_q_heads][D]
+  uint32_t* out;             // [batch][tw][n_q_heads][D]
   const Item* items;         // workspace
   const int4* multi;         // rows with several items: (first item, count, slot)
   float* partial;            // [n_kv_heads][n_items][G][D + 4]
   int64_t cap, base, L;
   int32_t layer, batch, n_kv_heads, split, n_items;
+  int32_t tw;                // input positions per row (1; T in a prefill step)
   float qscale;              // scale * log2(e)
 };
 
@@ -238,7 +255,8 @@ attn_kernel(const AttnArgs a) {
   const int b = it.x;
   const int32_t t_begin = it.y, t_end = it.z;
   const int32_t n = it.w;          // cached tokens; token n is the current one
-  uint32_t* outw = a.out + (((int64_t)b * a.n_kv_heads + h) * G) * (D * T::kBytes / 4);
+  const int64_t bt = (int64_t)b * a.tw;   // input row of the slot's position 0
+  uint32_t* outw = a.out + ((bt * a.n_kv_heads + h) * G) * (D * T::kBytes / 4);
   if (n < 0) {                     // free slot: the output rows are zero
     if (r == 0) {
 #pragma unroll
@@ -259,14 +277,14 @@ attn_kernel(const AttnArgs a) {
       __builtin_amdgcn_make_buffer_rsrc(a.v + row * a.cap * VPT * 4, 0, ring_bytes, kBufferWord3);
   const uint32_t start = (uint32_t)ring_add(a.base, a.L - n, a.cap);   // ring column of token 0
   const uint32_t cap = (uint32_t)a.cap;
-  const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
-  const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
+  const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + (bt * a.n_kv_heads + h) * VPT;
+  const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + (bt * a.n_kv_heads + h) * VPT;
 
   // Query slices of the G heads that share kv-head h, pre-scaled.
   float qf[G][EPL];
 #pragma unroll
   for (int gi = 0; gi < G; ++gi) {
-    const u32x4 w = reinterpret_cast<const u32x4*>(a.q)[(((int64_t)b * a.n_kv_heads + h) * G + gi) * VPT + cl];
+    const u32x4 w = reinterpret_cast<const u32x4*>(a.q)[((bt * a.n_kv_heads + h) * G + gi) * VPT + cl];
     Lane16<T>::widen(w, qf[gi]);
 #pragma unroll
     for (int e = 0; e < EPL; ++e) qf[gi][e] *= a.qscale;
@@ -383,7 +401,7 @@ __global__ void __launch_bounds__(kWave) combine_kernel(const AttnArgs a) {
   constexpr int REC = D + 4;
   const int4 mr = a.multi[blockIdx.x];
   const int hq = blockIdx.y, h = hq / G, gi = hq % G;
-  uint32_t* outw = a.out + ((int64_t)mr.z * a.n_kv_heads * G + hq) * (D * T::kBytes / 4);
+  uint32_t* outw = a.out + ((int64_t)mr.z * a.tw * a.n_kv_heads * G + hq) * (D * T::kBytes / 4);
   const float* base = a.partial + (((int64_t)h * a.n_items + mr.x) * G + gi) * REC;
   merge_row<T, D, G>(base, mr.y, outw, threadIdx.x);
 }

@@ -129,7 +129,8 @@ attn_mfma_kernel(const AttnArgs a) {
   const int4 rw = a.items[item].row;
   const int b = it.x;
   const int32_t t_begin = it.y, t_end = it.z, n = it.w;
-  uint32_t* outw = a.out + (((int64_t)b * a.n_kv_heads + h) * G) * (D / 2);
+  const int64_t bt = (int64_t)b * a.tw;   // input row of the slot's position 0
+  uint32_t* outw = a.out + ((bt * a.n_kv_heads + h) * G) * (D / 2);
   if (n < 0) {                       // free slot: zero output rows
 #pragma unroll
     for (int gi = 0; gi < G; ++gi)
@@ -149,7 +150,7 @@ attn_mfma_kernel(const AttnArgs a) {
 
   // Query heads as the B operand: column c16 = head c16 (zero beyond G).
   bf16x8 qb[KK];
-  const u32x4* qrow = reinterpret_cast<const u32x4*>(a.q) + (((int64_t)b * a.n_kv_heads + h) * G) * VPT;
+  const u32x4* qrow = reinterpret_cast<const u32x4*>(a.q) + ((bt * a.n_kv_heads + h) * G) * VPT;
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     const u32x4 w = c16 < G ? qrow[c16 * VPT + kk * 4 + g4] : u32x4{0, 0, 0, 0};
@@ -190,8 +191,8 @@ attn_mfma_kernel(const AttnArgs a) {
 
   // The current token, a one-token tile read from k_new / v_new, and its append.
   if (n >= t_begin && n < t_end) {
-    const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
-    const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + ((int64_t)b * a.n_kv_heads + h) * VPT;
+    const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + (bt * a.n_kv_heads + h) * VPT;
+    const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + (bt * a.n_kv_heads + h) * VPT;
     u32x4 kA[KK], kB[KK], vw[Geo::kVLoads];
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {

@@ -14,10 +14,11 @@ constexpr int kCopyVecs = 4;   // 16-byte vectors per thread per tile
 
 // Work of one launch: up to kMaxSegs row sets.  Segment i covers, in every
 // layer and kv-head and for both K and V, `len[i]` tokens of slot `slot[i]`
-// starting at physical ring column `col0[i]`.  With `extract` clear, it copies
-// the contiguous buffer ext[i][layer][head][0:len][:] there, or writes the
-// placeholder when ext[i] is null; with `extract` set it copies those ring
-// columns out into ext[i].
+// starting at physical ring column `col0[i]`.  The contiguous side ext[i] is
+// [layer][head][ext_len[i]][D] and the segment maps to its tokens
+// ext_t0[i] .. ext_t0[i] + len[i] - 1.  With `extract` clear, the segment is
+// copied from ext[i] into the ring, or the placeholder is written when ext[i]
+// is null; with `extract` set the ring columns are copied out into ext[i].
 struct SegArgs {
   uint32_t* k;              // ring buffers, viewed as 32-bit words
   uint32_t* v;
@@ -31,6 +32,8 @@ struct SegArgs {
   int32_t tiles_per_row[kMaxSegs];
   int64_t col0[kMaxSegs];
   int64_t tile_end[kMaxSegs];           // inclusive prefix of tiles over segments
+  int32_t ext_len[kMaxSegs];            // tokens per (layer, head) of the contiguous side
+  int32_t ext_t0[kMaxSegs];             // its first token of this segment
   uint32_t* kext[kMaxSegs];             // contiguous side; null: placeholders
   uint32_t* vext[kMaxSegs];
 };
@@ -58,7 +61,7 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
   u32x4* ring = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
                (((int64_t)layer * a.batch + a.slot[i]) * a.n_kv_heads + h) * a.cap * VPT;
   u32x4* ext = reinterpret_cast<u32x4*>(which ? a.vext[i] : a.kext[i]);
-  if (ext) ext += (((int64_t)layer * a.n_kv_heads + h) * len + t0) * VPT;
+  if (ext) ext += (((int64_t)layer * a.n_kv_heads + h) * a.ext_len[i] + a.ext_t0[i] + t0) * VPT;
   const int64_t c0 = ring_add(a.col0[i], t0, a.cap);
 
   u32x4 val[kCopyVecs];
@@ -107,26 +110,45 @@ __global__ void __launch_bounds__(256) fill_kernel(u32x4* __restrict__ k, u32x4*
   }
 }
 
-// mask[b * ld + j] = (len_b > 0 && j >= L - len_b) for j in [0, L]; one block
-// row per slot, 4 bytes per thread.
+// The step's mask, mask[b * ld + j] for j in [0, L + T): a live row (span n)
+// is 1 on [L - n, L] outside its holes, a row prefilled this step (prompt p)
+// on [L + T - p, L + T), a free row nowhere.  One block row per slot, 4 bytes
+// per thread.
 struct MaskArgs {
   uint8_t* mask;
   int64_t ld, L;
-  int32_t batch;
-  int32_t lens[512];
+  int32_t batch, T;
+  int32_t lens[512];      // span; 0 free; -p prefilled this step with a prompt of p tokens
+  uint8_t first[512];     // index of the row's first hole
+  HoleList holes;
 };
 
 __global__ void __launch_bounds__(256) mask_kernel(const MaskArgs a) {
   const int b = blockIdx.y;
-  const int64_t n = a.lens[b];
-  const int64_t first = n > 0 ? a.L - n : a.L + 1;   // first column that is 1
+  const int32_t n = a.lens[b];
+  const int64_t W = a.L + a.T;
+  int64_t lo, hi;                                   // the ones before holes: [lo, hi)
+  if (n > 0) {
+    lo = a.L - n;
+    hi = a.L + 1;
+  } else if (n < 0) {
+    lo = W + n;
+    hi = W;
+  } else {
+    lo = hi = 0;
+  }
+  const int k0 = n > 0 ? a.first[b] : a.holes.n;
   uint8_t* row = a.mask + (int64_t)b * a.ld;
-  for (int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; j0 <= a.L;
+  for (int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; j0 < W;
        j0 += (int64_t)gridDim.x * blockDim.x * 4) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int64_t j = j0 + e;
-      if (j <= a.L) row[j] = (uint8_t)(j >= first);
+      if (j >= W) break;
+      bool one = j >= lo && j < hi;
+      for (int k = k0; one && k < a.holes.n; ++k)
+        one = !(j >= a.holes.col[k][0] && j < a.holes.col[k][1]);
+      row[j] = (uint8_t)one;
     }
   }
 }

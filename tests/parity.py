@@ -256,6 +256,7 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
       ("evict", slots)               with release
       ("extract", slots, tag)        store the slots' K/V aside (GPU and oracle)
       ("embed_saved", slots, tag)    re-insert stored queries into these slots
+      ("shape", slots, lens, qids)   prefill new queries inside the batch in the next step
       ("step", s)                    mask, every layer with step-s inputs, advance
       ("flush",)                     the placeholder writes evictions still owe
     After a step or a flush the whole ring is compared; after the other
@@ -270,6 +271,7 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
     dev = driver.DeviceInputs(w)
     pb = O.PaddedBatch(NL, B, Hq, Hkv, D, dtype, fill_bits=cache.fill_bits)
     saved_gpu, saved_cpu = {}, {}
+    shaped = []
     worst = 0.0
     for op in ops:
         kind = op[0]
@@ -297,26 +299,48 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
             cache.embed(slots, [k.shape[2] for k in ks], ks, vs)
             pb.embed(slots, [k.shape[2] for k, _ in saved_cpu[tag]], [k for k, _ in saved_cpu[tag]],
                      [v for _, v in saved_cpu[tag]])
+        elif kind == "shape":
+            _, slots, lens, qids = op
+            cache.shape_insert(slots, lens)
+            pb.shape_insert(slots, lens)
+            shaped = list(zip(slots, qids, lens))
         elif kind == "step":
             s = op[1]
             m = cache.build_mask()
             assert np.array_equal(m.cpu().numpy(), pb.mask()), f"{op}: mask"
             for layer in range(NL):
-                q, kn, vn = dev.decode(s, layer)
-                out = cache.decode_attn(layer, q, kn, vn)
-                hq = [gen.decode_host(w.seed, sid, s, layer, NL, B, h, D, dtype)
-                      for sid, h in ((gen.S_Q, Hq), (gen.S_KNEW, Hkv), (gen.S_VNEW, Hkv))]
-                want = pb.decode_layer(layer, *hq)
-                err = max_err(out, want, dtype)
+                if shaped:
+                    T = pb.step_width()
+                    q, kn, vn = dev.prefill_step(s, layer, T, shaped)
+                    out = torch.full_like(q, float("nan"))   # positions without a token stay NaN
+                    cache.decode_attn(layer, q, kn, vn, out=out)
+                    hq = [gen.prefill_step_host(w.seed, which, s, layer, NL, B, T, h, D, dtype, shaped)
+                          for which, h in (("q", Hq), ("k", Hkv), ("v", Hkv))]
+                    assert np.array_equal(host_bits(kn), hq[1]), "device and host generators disagree"
+                    want = pb.decode_layer(layer, *hq)
+                    got = O.widen(host_bits(out), dtype)
+                    hole = np.isnan(want)
+                    assert np.all(np.isnan(got[hole])), f"{op} layer {layer}: a position without a token was written"
+                    err = float(np.max(np.abs(got[~hole] - want[~hole]))) if (~hole).any() else 0.0
+                else:
+                    q, kn, vn = dev.decode(s, layer)
+                    out = cache.decode_attn(layer, q, kn, vn)
+                    hq = [gen.decode_host(w.seed, sid, s, layer, NL, B, h, D, dtype)
+                          for sid, h in ((gen.S_Q, Hq), (gen.S_KNEW, Hkv), (gen.S_VNEW, Hkv))]
+                    want = pb.decode_layer(layer, *hq)
+                    err = max_err(out, want, dtype)
                 worst = max(worst, err)
                 assert err <= TOL[dtype], f"{op} layer {layer}: {err}"
             cache.advance()
             pb.advance()
+            shaped = []
         elif kind == "flush":
             cache.flush()
         else:
             raise ValueError(kind)
         torch.cuda.synchronize()
-        check_ring(cache, pb, str(op), live_only=kind in ("evict", "embed", "embed_saved", "extract"))
+        check_ring(cache, pb, str(op), live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape"))
+        want_tok = [pb.hist_k[b].shape[2] if pb.lens[b] > 0 else 0 for b in range(B)]
+        assert cache.tokens() == want_tok, (op, cache.tokens(), want_tok)
     cache.close()
     return worst

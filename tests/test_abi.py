@@ -90,6 +90,20 @@ def test_host_checks_leave_state_unchanged():
         assert status(B.baton_build_mask, h, FAKE_K, 0) == B.BATON_EINVAL   # ld < L + 1
         assert status(B.baton_set_split_tokens, h, 100) == B.BATON_EINVAL
         assert B.baton_cache_query(h, 4) == (0, 0, [0, 0, 0, 0])
+        # in-batch prefill registration (host metadata only)
+        assert status(B.baton_shape_insert, h, [], []) == B.BATON_EINVAL          # nothing to insert
+        assert status(B.baton_shape_insert, h, [1, 1], [3, 3]) == B.BATON_EINVAL  # duplicate
+        assert status(B.baton_shape_insert, h, [1], [0]) == B.BATON_EINVAL        # empty prompt
+        assert status(B.baton_shape_insert, h, [5], [3]) == B.BATON_EINVAL        # out of range
+        assert status(B.baton_shape_insert, h, [1], [301]) == B.BATON_ECAPACITY   # L + T > capacity
+        assert status(B.baton_shape_insert, h, list(range(4)) * 17, [1] * 68) == B.BATON_EINVAL  # > max
+        B.baton_shape_insert(h, [1, 3], [7, 300])
+        assert status(B.baton_kv_evict, h, []) == B.BATON_ESTATE                   # prefill registered
+        assert status(B.baton_kv_embed, h, [], [], [], []) == B.BATON_ESTATE
+        assert status(B.baton_build_mask, h, FAKE_K, 299) == B.BATON_EINVAL       # ld < L + T
+        assert B.baton_cache_tokens(h, 4) == [0, 0, 0, 0]
+        B.baton_shape_insert(h, [2], [1])                                          # replaces it
+        assert status(B.baton_kv_evict, h, []) == B.BATON_ESTATE
         B.baton_set_split_tokens(h, 64)
         assert B.baton_decode_attn_workspace_bytes(h) > ws                # more, smaller splits
     finally:

@@ -1,0 +1,98 @@
+"""Baton without prefill/decode separation on the GPU (sec. 4.1): new queries
+prefilled inside the batch (baton_shape_insert), holes left in the other rows,
+the holey mask, causal prefill attention and later decode steps over holey
+rows -- in lockstep with the materialized oracle: ring bit for bit, mask bit
+for bit, token counts, every output within tolerance, and positions that hold
+no token left untouched."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from tests import oracle_pins, parity
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [("f32", 1, 4, 4, 4, 64), ("f32", 2, 5, 8, 2, 128), ("bf16", 2, 6, 8, 8, 128),
+          ("bf16", 1, 5, 16, 2, 128), ("bf16", 1, 4, 4, 2, 64)]
+
+
+def _sid(s):
+    return f"{s[0]}-{s[1]}x{s[2]}-{s[3]}/{s[4]}x{s[5]}"
+
+
+def _golden_ops():
+    """The hand-derived replay's operations (tests/golden/inbatch_prefill_replay.json)."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "inbatch_prefill_replay.json")
+    ops, s = [], 0
+    for op in json.load(open(path))["ops"]:
+        if op["op"] in ("embed", "shape"):
+            ops.append((op["op"], op["slots"], op["lens"], op["qids"]))
+        elif op["op"] == "evict":
+            ops.append(("evict", op["slots"]))
+        else:
+            ops.append(("step", s))
+            s += 1
+    return ops
+
+
+def _random_ops(seed, B, steps, max_len):
+    rng = np.random.default_rng(seed)
+    ops, qid, s = [], 0, 0
+    for op in oracle_pins._random_ops_shaped(rng, B, steps, max_len):
+        if op[0] in ("embed", "shape"):
+            qids = list(range(qid, qid + len(op[1])))
+            qid += len(op[1])
+            ops.append((op[0], op[1], op[2], qids))
+            if op[0] == "shape":
+                ops.append(("step", s))
+                s += 1
+        elif op[0] == "evict":
+            ops.append(op)
+        else:
+            ops.append(("step", s))
+            s += 1
+    return ops
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_sid)
+def test_golden_story(shape):
+    dtype, NL, _, Hq, Hkv, D = shape
+    err = parity.run_script((dtype, NL, 3, Hq, Hkv, D), _golden_ops(), capacity=64)
+    print(f"[inbatch golden] {shape}: max abs error {err:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_sid)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_random_sequences(shape, seed):
+    dtype, NL, B, Hq, Hkv, D = shape
+    ops = _random_ops(seed * 10 + len(shape[0]), B, steps=14, max_len=70)
+    err = parity.run_script(shape, ops, capacity=2048, split=64)
+    print(f"[inbatch random] {shape} seed {seed}: {len(ops)} ops, max abs error {err:.3g}", flush=True)
+
+
+def test_long_prompts_and_wrap():
+    """Prompts spanning many tiles and key blocks (up to 300 tokens), several
+    prefills in one step with different lengths, a ring that wraps."""
+    ops = [("embed", [0, 1, 2], [100, 40, 7], [0, 1, 2]), ("step", 0),
+           ("evict", [1]), ("shape", [1], [300], [3]), ("step", 1), ("step", 2),
+           ("evict", [0, 2]), ("shape", [2, 0], [129, 33], [4, 5]), ("step", 3),
+           ("evict", [1]), ("embed", [1], [60], [6]), ("step", 4),
+           ("evict", [2]), ("shape", [2], [250], [7]), ("step", 5), ("step", 6)]
+    for shape in (("bf16", 1, 3, 8, 8, 128), ("bf16", 1, 3, 16, 2, 64), ("f32", 1, 3, 4, 2, 128)):
+        err = parity.run_script(shape, ops, capacity=800, split=64)
+        print(f"[inbatch long] {shape}: max abs error {err:.3g}", flush=True)
+
+
+def test_extract_with_holes():
+    """A query with holes stored aside and re-inserted: its tokens come back in
+    order without the holes, and it decodes on as the oracle says."""
+    ops = [("embed", [0, 1], [20, 9], [0, 1]), ("step", 0),
+           ("shape", [2], [12], [2]), ("step", 1), ("step", 2),
+           ("evict", [1]), ("shape", [1], [5], [3]), ("step", 3),
+           ("extract", [0, 2], "holey"), ("evict", [0, 2]), ("step", 4),
+           ("embed_saved", [3, 0], "holey"), ("step", 5), ("step", 6)]
+    for shape in (("bf16", 2, 4, 8, 2, 128), ("f32", 1, 4, 4, 4, 64)):
+        err = parity.run_script(shape, ops, capacity=256, split=64)
+        print(f"[inbatch extract] {shape}: max abs error {err:.3g}", flush=True)

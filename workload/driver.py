@@ -49,6 +49,24 @@ class DeviceInputs:
         return out
 
 
+    def prefill_step(self, step, layer, T, inserted=()):
+        """(q, k_new, v_new) of one layer of a step that prefills queries inside
+        the batch: [batch][T][heads][head_dim]; inserted as in gen.prefill_step_host."""
+        w = self.w
+        out = []
+        for sid, psid, heads in ((gen.S_QW, None, w.n_q_heads), (gen.S_KW, gen.S_PREFILL_K, w.n_kv_heads),
+                                 (gen.S_VW, gen.S_PREFILL_V, w.n_kv_heads)):
+            t = torch.empty((w.batch, T, heads, w.head_dim), dtype=self.tdt, device=self.device)
+            c0, st = gen.wide_counter(step, layer, w.n_layers, w.batch, heads, w.head_dim)
+            self._fill(t, sid, (w.batch, T, heads, w.head_dim), c0, st)
+            if psid is not None:
+                for slot, qid, n in inserted:
+                    c0, st = gen.prompt_counter(qid, layer, w.n_layers, heads, w.head_dim)
+                    self._fill(t[slot, T - n:], psid, (1, n, heads, w.head_dim), c0, st)
+            out.append(t)
+        return out
+
+
 def prefill_bytes(w, length):
     return 2 * w.n_layers * w.n_kv_heads * length * w.head_dim * w.elem_bytes
 

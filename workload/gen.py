@@ -32,6 +32,9 @@ S_PREFILL_V = 4   # values a prefill instance produced for a query
 S_Q = 5           # decode-step queries
 S_KNEW = 6        # decode-step keys of the current token
 S_VNEW = 7        # decode-step values of the current token
+S_QW = 8          # queries of a step that prefills new queries inside the batch
+S_KW = 9          # its keys (positions that hold no prompt token)
+S_VW = 10         # its values
 
 # Token radix of the prefill counter: prefilled lengths stay below this.
 TMAX = 1 << 16
@@ -81,6 +84,21 @@ def decode_counter(step, layer, n_layers, batch, n_heads, head_dim):
     """(c0, strides) of a decode-step tensor laid out [1][batch][head][d]."""
     c0 = ((step * n_layers + layer) * batch) * n_heads * head_dim
     return c0, (0, n_heads * head_dim, head_dim, 1)
+
+
+def wide_counter(step, layer, n_layers, batch, n_heads, head_dim):
+    """(c0, strides) of a prefill-step tensor laid out [batch][T][head][d] (T < TMAX)."""
+    row = n_heads * head_dim
+    c0 = ((step * n_layers + layer) * batch) * TMAX * row
+    return c0, (TMAX * row, row, head_dim, 1)
+
+
+def prompt_counter(qid, layer, n_layers, n_kv_heads, head_dim):
+    """(c0, strides) of a query's prefilled K or V of one layer laid out [1][t][head][d]:
+    the prompt positions of a prefill step carry the values a separate prefill
+    of the same query would have produced."""
+    c0, (s0, s1, s2, _) = prefill_counter(qid, n_layers, n_kv_heads, head_dim, layer0=layer)
+    return c0, (0, s2, s1, 1)
 
 
 # ------------------------------------------------------------------- host --
@@ -133,6 +151,23 @@ def decode_host(seed, stream, step, layer, n_layers, batch, n_heads, head_dim, d
     """Decode-step tensor (q, k_new or v_new): bits [batch][head][d]."""
     c0, st = decode_counter(step, layer, n_layers, batch, n_heads, head_dim)
     return fill_host(seed, stream, dtype, (1, batch, n_heads, head_dim), c0, st)[0]
+
+
+def prefill_step_host(seed, which, step, layer, n_layers, batch, T, n_heads, head_dim, dtype,
+                      inserted=()):
+    """Inputs of a step that prefills queries inside the batch: which in 'q', 'k',
+    'v'; bits [batch][T][head][d].  inserted: (slot, qid, prompt length) of the
+    queries prefilled in it; their prompt positions' keys and values are their
+    prefilled ones."""
+    stream = {"q": S_QW, "k": S_KW, "v": S_VW}[which]
+    c0, st = wide_counter(step, layer, n_layers, batch, n_heads, head_dim)
+    out = fill_host(seed, stream, dtype, (batch, T, n_heads, head_dim), c0, st)
+    if which != "q":
+        ps = S_PREFILL_K if which == "k" else S_PREFILL_V
+        for slot, qid, n in inserted:
+            c0, st = prompt_counter(qid, layer, n_layers, n_heads, head_dim)
+            out[slot, T - n:] = fill_host(seed, ps, dtype, (1, n, n_heads, head_dim), c0, st)[0]
+    return out
 
 
 # ----------------------------------------------------------------- device --
