@@ -39,6 +39,9 @@ def parse():
     p.add_argument("--layers", type=int, default=None,
                    help="resident layers (config 4's 80-layer padded cache exceeds HBM; default 24 there)")
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
+    p.add_argument("--no-pd", action="store_true",
+                   help="prefill the new queries inside the batch (no prefill/decode separation) "
+                        "instead of embedding prefilled ones")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=20, help="layers of step 0 the oracle runs")
     p.add_argument("--copy-bytes", type=int, default=2 << 30,
@@ -72,6 +75,104 @@ def placeholder_bytes(w, lens_before, ev):
     new = dict(zip(ev.insert, ev.insert_lens))
     owed = sum(max(0, lens_before[s] - new.get(s, 0)) for s in ev.evict)
     return 2 * w.n_layers * w.n_kv_heads * owed * w.head_dim * w.elem_bytes
+
+
+def prefill_flops(w, insert_lens):
+    """Algorithmic flops of the causal prefill attention of new queries, one layer:
+    per query head, 2*D flops per (position, visible key) pair for QK^T and the
+    same for PV."""
+    return sum(4 * w.n_q_heads * w.head_dim * n * (n + 1) // 2 for n in insert_lens)
+
+
+def bench_no_pd(args, w):
+    """The schedule without prefill/decode separation: a step with new queries
+    prefills them inside the batch (their prompts as T = longest-prompt input
+    positions, the other rows padded), leaving holes in the other rows."""
+    import torch
+
+    from workload import driver
+
+    cache, inputs = driver.open_cache(w, split=args.split, no_pd=True)
+    total_steps = args.warmup + args.steps
+    for s in range(args.warmup):
+        driver.run_step_no_pd(cache, inputs, s, w.steps[s])
+    torch.cuda.synchronize()
+    pre = []
+    for s in range(args.warmup, total_steps):
+        ev = w.steps[s]
+        ins = list(zip(ev.insert, ev.insert_qids, ev.insert_lens))
+        T = max(ev.insert_lens, default=1)
+        dec = [inputs.prefill_step(s, layer, T, ins) if ins else inputs.decode(s, layer)
+               for layer in range(w.n_layers)]
+        outs = torch.empty_like(dec[0][0])
+        pre.append((ins, dec, outs))
+    mask_buf = torch.empty((w.batch, cache.capacity + 1), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    n_ev = 2 * args.steps * (2 + w.n_layers) + 2
+    pool = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+    for e in pool:
+        e.record()
+    torch.cuda.synchronize()
+    pool_it = iter(pool)
+    E = lambda: next(pool_it)
+    ev_pf, ev_dec = [], []
+    bytes_dec = flops_pf = 0
+    live_tokens = prompt_tokens = 0
+    gc.collect()
+    gc.disable()
+    t_start, t_end = E(), E()
+    t_start.record()
+    for i, s in enumerate(range(args.warmup, total_steps)):
+        ev = w.steps[s]
+        ins, dec, outs = pre[i]
+        cache.evict(ev.evict, release=True)
+        if ins:
+            cache.shape_insert(ev.insert, ev.insert_lens)
+        cache.build_mask(out=mask_buf)
+        _, _, lens = cache.query()
+        for layer in range(w.n_layers):
+            q, kn, vn = dec[layer]
+            a, b = E(), E()
+            a.record()
+            cache.decode_attn(layer, q, kn, vn, out=outs)
+            b.record()
+            (ev_pf if ins else ev_dec).append((a, b))
+        if ins:
+            flops_pf += w.n_layers * prefill_flops(w, ev.insert_lens)
+            prompt_tokens += sum(ev.insert_lens)
+        else:
+            bytes_dec += w.n_layers * attn_bytes(w, lens)
+        live_tokens += sum(1 for n in lens if n > 0) + len(ins)
+        cache.advance()
+    t_end.record()
+    torch.cuda.synchronize()
+    gc.enable()
+    total_ms = t_start.elapsed_time(t_end)
+    ms = lambda evs: sum(x.elapsed_time(y) for x, y in evs)
+    pf_ms, dec_ms = ms(ev_pf), ms(ev_dec)
+    L, _, _ = cache.query()
+    return {
+        "metric": "query-tokens/s without prefill/decode separation (new queries prefilled in the batch)",
+        "value": round(live_tokens / (total_ms * 1e-3), 1),
+        "unit": "query-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded counter-based generator, values ~N(0,1))",
+        "config": {"workload": f"{w.name} schedule, no P&D separation: {w.dtype}, {w.n_layers} layers x "
+                               f"{w.n_q_heads} q-heads / {w.n_kv_heads} kv-heads x head_dim {w.head_dim}, "
+                               f"batch {w.batch}, initial padded length {w.L0}, ring capacity {cache.capacity}",
+                   "global_batch": w.batch, "seq_len": w.L0, "parallelism": "none (1 GPU)"},
+        "ops": {
+            "prefill_steps": {"layer_calls": len(ev_pf), "ms_per_call": round(pf_ms / max(1, len(ev_pf)), 4),
+                              "prompt_tokens": prompt_tokens,
+                              "prefill_TFLOP/s (calls incl. decode rows)":
+                                  round(flops_pf / (pf_ms * 1e-3) / 1e12, 2) if pf_ms else None},
+            "decode_steps": {"layer_calls": len(ev_dec), "ms_per_call": round(dec_ms / max(1, len(ev_dec)), 4),
+                             "GB/s": round(bytes_dec / (dec_ms * 1e-3) / 1e9, 1) if dec_ms else None},
+            "final_padded_length": L,
+        },
+    }
 
 
 def cpu_baseline(w, n_layers):
@@ -167,7 +268,6 @@ def main():
     from workload import configs, driver
 
     torch.cuda.set_device(0)
-    copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
     total_steps = args.warmup + args.steps
     if args.config == "cfg4":
         w = configs.cfg4(total_steps, n_layers=args.layers or 24)
@@ -175,6 +275,10 @@ def main():
         w = configs.CONFIGS[args.config](total_steps)
         if args.layers:
             raise SystemExit("--layers applies to cfg4 only")
+    if args.no_pd:
+        print(json.dumps(bench_no_pd(args, w)), flush=True)
+        return
+    copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
     cache, inputs = driver.open_cache(w, split=args.split)
     cap = cache.capacity
 

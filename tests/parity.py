@@ -127,13 +127,17 @@ def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale
 
 # ------------------------------------------------------------ sampled mode --
 class History:
-    """Where each slot's query came from, to rebuild any row's history on the host."""
+    """Where each slot's query came from, to rebuild any row's history on the host.
 
-    def __init__(self, w):
+    wide_steps: steps that prefilled new queries inside the batch; a live row's
+    token of such a step is position 0 of that step's wide inputs."""
+
+    def __init__(self, w, wide_steps=()):
         self.w = w
         self.qid = list(range(w.batch))
         self.plen = list(w.init_lens)
         self.first_step = [0] * w.batch      # first decode step of the query
+        self.wide_steps = set(wide_steps)
 
     def insert(self, slot, qid, n, step):
         self.qid[slot], self.plen[slot], self.first_step[slot] = qid, n, step
@@ -146,23 +150,35 @@ class History:
         c0, st = gen.prefill_counter(self.qid[slot], w.n_layers, w.n_kv_heads, w.head_dim,
                                      layer0=layer, head0=head)
         pre = gen.fill_host(w.seed, sid, w.dtype, (1, 1, self.plen[slot], w.head_dim), c0, st)[0, 0]
-        dsid = gen.S_KNEW if which == "k" else gen.S_VNEW
         toks = []
         for s in range(self.first_step[slot], step + 1):
-            c0, st = gen.decode_counter(s, layer, w.n_layers, w.batch, w.n_kv_heads, w.head_dim)
-            c0 += (slot * w.n_kv_heads + head) * w.head_dim
+            if s in self.wide_steps:
+                dsid = gen.S_KW if which == "k" else gen.S_VW
+                c0, st = gen.wide_counter(s, layer, w.n_layers, w.batch, w.n_kv_heads, w.head_dim)
+                c0 += slot * st[0] + head * w.head_dim       # position 0 of the slot
+            else:
+                dsid = gen.S_KNEW if which == "k" else gen.S_VNEW
+                c0, st = gen.decode_counter(s, layer, w.n_layers, w.batch, w.n_kv_heads, w.head_dim)
+                c0 += (slot * w.n_kv_heads + head) * w.head_dim
             toks.append(gen.fill_host(w.seed, dsid, w.dtype, (1, 1, 1, w.head_dim), c0, st)[0, 0])
         return np.concatenate([pre] + toks) if toks else pre
 
 
-def check_placeholders_outside_live(cache, fill_bits):
-    """On the GPU: a ring position holds non-placeholder bits iff it is a live token."""
+def check_placeholders_outside_live(cache, fill_bits, mask=None):
+    """On the GPU: a ring position holds non-placeholder bits iff it is a live
+    token (per the contiguous lengths, or the given 0-1 mask [B][>= L] of the
+    cached columns when rows have holes)."""
     L, base, lens = cache.query()
     cap = cache.capacity
     col = torch.arange(cap, device=cache.k.device)
     logical = (col - base) % cap                                 # logical column of each physical one
-    lens_t = torch.tensor(lens, device=cache.k.device)[:, None]
-    live = (logical[None, :] < L) & (logical[None, :] >= L - lens_t) & (lens_t > 0)   # [B][cap]
+    if mask is None:
+        lens_t = torch.tensor(lens, device=cache.k.device)[:, None]
+        live = (logical[None, :] < L) & (logical[None, :] >= L - lens_t) & (lens_t > 0)   # [B][cap]
+    else:
+        m = torch.zeros((cache.batch, cap + 1), dtype=torch.bool, device=cache.k.device)
+        m[:, :L] = mask[:, :L].bool()
+        live = m[:, torch.where(logical < L, logical, cap)]
     if cache.k.dtype == torch.bfloat16:
         idt, fill = torch.int16, int(np.array(fill_bits, np.uint16).view(np.int16))
     else:
@@ -242,6 +258,89 @@ def run_sampled(w, sample_steps, sample_layers, n_slots=4, seed=0, split=None, c
         pb.advance()
     torch.cuda.synchronize()
     check_placeholders_outside_live(cache, cache.fill_bits)
+    cache.close()
+    return worst, checked
+
+
+def run_sampled_no_pd(w, sample_steps, sample_layers=(0,), n_slots=4, n_pos=6, heads=(0,), seed=0):
+    """The schedule without prefill/decode separation, whole on the GPU (the
+    bench's launch configuration); metadata and the mask's width at every step;
+    at the sampled steps the whole mask, and for sampled rows their K/V at the
+    mask's ones (bit for bit, holes skipped) and outputs: a live row's position
+    0 over its history, a new query's sampled positions causally over its prompt."""
+    rng = np.random.default_rng(seed)
+    wide = [s for s, ev in enumerate(w.steps) if ev.insert]
+    cache, dev = driver.open_cache(w, no_pd=True)
+    pb = O.PaddedBatch(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype,
+                       fill_bits=cache.fill_bits, materialize=False)
+    pb.embed(list(range(w.batch)), w.init_lens, [None] * w.batch, [None] * w.batch)
+    hist = History(w, wide)
+    g = w.n_q_heads // w.n_kv_heads
+    sc = 1.0 / math.sqrt(w.head_dim)
+    worst, checked = 0.0, 0
+    for s, ev in enumerate(w.steps):
+        cache.evict(ev.evict, release=True)
+        pb.evict(ev.evict, release=True)
+        ins = list(zip(ev.insert, ev.insert_qids, ev.insert_lens))
+        if ins:
+            cache.shape_insert(ev.insert, ev.insert_lens)
+            pb.shape_insert(ev.insert, ev.insert_lens)
+        T = pb.step_width()
+        L, base, lens = cache.query()
+        assert (L, lens) == (pb.L, pb.lens), f"step {s}: metadata"
+        m = cache.build_mask()
+        assert m.shape[1] == L + T
+        M = pb.mask()
+        if s in sample_steps:
+            assert np.array_equal(m.cpu().numpy(), M), f"step {s}: mask"
+        live = pb.live()
+        for layer in range(w.n_layers):
+            q, kn, vn = dev.prefill_step(s, layer, T, ins) if ins else dev.decode(s, layer)
+            out = cache.decode_attn(layer, q, kn, vn)
+            if s not in sample_steps or layer not in sample_layers:
+                continue
+            qh = host_bits(q) if ins else host_bits(q)[:, None]
+            oh = O.widen(host_bits(out), w.dtype) if ins else O.widen(host_bits(out), w.dtype)[:, None]
+            rows = sorted(set(rng.choice(live, min(n_slots, len(live)), replace=False).tolist()))
+            for b in rows:
+                keep = np.flatnonzero(M[b, :L])
+                cols = torch.as_tensor((keep + base) % cache.capacity, device=cache.k.device)
+                for h in heads:
+                    kh = hist.row(b, layer, h, s, "k")
+                    vh = hist.row(b, layer, h, s, "v")
+                    assert len(kh) == len(keep) + 1, (s, b, len(kh), len(keep))
+                    assert np.array_equal(host_bits(cache.k[layer, b, h, cols]), kh[:-1]) and \
+                        np.array_equal(host_bits(cache.v[layer, b, h, cols]), vh[:-1]), \
+                        f"step {s} layer {layer} slot {b} head {h}: cached tokens"
+                    K, V = O.widen(kh, w.dtype), O.widen(vh, w.dtype)
+                    for hq in range(h * g, h * g + g):
+                        want = O.attend(O.widen(qh[b, 0, hq], w.dtype), K, V, sc)
+                        err = float(np.max(np.abs(oh[b, 0, hq] - want)))
+                        worst, checked = max(worst, err), checked + 1
+                        assert err <= TOL[w.dtype], f"step {s} slot {b} q-head {hq}: {err}"
+            for b, qid, p in ins:
+                pos = sorted(set([0, p - 1] + rng.integers(0, p, size=n_pos).tolist()))
+                for h in heads:
+                    c0, st = gen.prompt_counter(qid, layer, w.n_layers, w.n_kv_heads, w.head_dim)
+                    Kp = gen.fill_host(w.seed, gen.S_PREFILL_K, w.dtype, (1, p, w.n_kv_heads, w.head_dim), c0, st)[0, :, h]
+                    Vp = gen.fill_host(w.seed, gen.S_PREFILL_V, w.dtype, (1, p, w.n_kv_heads, w.head_dim), c0, st)[0, :, h]
+                    K, V = O.widen(Kp, w.dtype), O.widen(Vp, w.dtype)
+                    for hq in range(h * g, h * g + g):
+                        for i in pos:
+                            t = T - p + i
+                            want = O.attend(O.widen(qh[b, t, hq], w.dtype), K[:i + 1], V[:i + 1], sc)
+                            err = float(np.max(np.abs(oh[b, t, hq] - want)))
+                            worst, checked = max(worst, err), checked + 1
+                            assert err <= TOL[w.dtype], f"step {s} new slot {b} pos {i} q-head {hq}: {err}"
+        cache.advance()
+        for layer in range(w.n_layers):
+            pb.decode_layer(layer, None, None, None)
+        pb.advance()
+        for b, qid, p in ins:
+            hist.insert(b, qid, p, s + 1)
+    torch.cuda.synchronize()
+    cache.flush()
+    check_placeholders_outside_live(cache, cache.fill_bits, mask=cache.build_mask())
     cache.close()
     return worst, checked
 

@@ -39,3 +39,13 @@ def test_cfg4_gqa_resident_layers():
     print(f"[configs] cfg4 24 layers sampled", flush=True)
     err, n = parity.run_sampled(w, {0, 5}, {0, 23}, n_slots=3)
     print(f"[configs] cfg4: {n} outputs checked, max abs error {err:.3g}", flush=True)
+
+
+def test_cfg2_no_pd_sampled():
+    """Config 2's schedule without prefill/decode separation, as bench.py --no-pd
+    runs it (2 + 16 steps, every step prefilling two queries inside the batch)."""
+    w = configs.cfg2(18)
+    print(f"[configs] cfg2 no-P&D sampled: capacity {w.capacity_no_pd()}", flush=True)
+    err, n = parity.run_sampled_no_pd(w, {0, 1, 9, 17}, heads=(0, 31))
+    print(f"[configs] cfg2 no-P&D: {n} outputs checked, max abs error {err:.3g}", flush=True)
+    assert n > 0

@@ -106,6 +106,13 @@ class Workload:
         cap = need + self.n_steps + extra_steps + 1
         return (cap + 63) // 64 * 64
 
+    def capacity_no_pd(self):
+        """Ring columns when the new queries are prefilled inside the batch: a step
+        with insertions appends as many columns as its longest prompt."""
+        need = max(self.L0, max(self.init_lens, default=0))
+        cap = need + sum(max(e.insert_lens, default=1) for e in self.steps) + 1
+        return (cap + 63) // 64 * 64
+
 
 def _pin_max(lens, L0):
     """Give the longest drawn row exactly L0 columns (the batch's padded length)."""

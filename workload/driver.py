@@ -71,10 +71,13 @@ def prefill_bytes(w, length):
     return 2 * w.n_layers * w.n_kv_heads * length * w.head_dim * w.elem_bytes
 
 
-def open_cache(w, capacity=None, device="cuda", fill_bits=None, split=None, init_budget=8 << 30):
+def open_cache(w, capacity=None, device="cuda", fill_bits=None, split=None, init_budget=8 << 30,
+               no_pd=False):
     """A BatonCache holding the workload's initial batch, built by embedding the
     B initial queries (query id = slot) into an empty batch, a group at a time."""
-    cap = w.capacity() if capacity is None else capacity
+    if capacity is None:
+        capacity = w.capacity_no_pd() if no_pd else w.capacity()
+    cap = capacity
     cache = BatonCache(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, cap,
                        dtype=w.dtype, fill_bits=fill_bits, device=device)
     if split is not None:
@@ -91,6 +94,24 @@ def open_cache(w, capacity=None, device="cuda", fill_bits=None, split=None, init
             del srcs
             group, used = [], 0
     return cache, inputs
+
+
+def run_step_no_pd(cache, inputs, s, ev, mask=True):
+    """Step s without prefill/decode separation: evict, register the new queries
+    for prefill inside the batch, mask, every layer (prefill-step inputs when
+    there are new queries), advance."""
+    w = inputs.w
+    cache.evict(ev.evict, release=True)
+    inserted = list(zip(ev.insert, ev.insert_qids, ev.insert_lens))
+    if inserted:
+        cache.shape_insert(ev.insert, ev.insert_lens)
+    T = cache.step_width
+    m = cache.build_mask() if mask else None
+    for layer in range(w.n_layers):
+        q, kn, vn = inputs.prefill_step(s, layer, T, inserted) if inserted else inputs.decode(s, layer)
+        cache.decode_attn(layer, q, kn, vn)
+    cache.advance()
+    return m
 
 
 def run_step(cache, inputs, s, ev, layers=None, outs=None, mask=True):
