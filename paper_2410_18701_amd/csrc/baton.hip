@@ -23,7 +23,11 @@
 #endif
 
 #ifndef BATON_PREFILL_MFMA
-#define BATON_PREFILL_MFMA 1   // bf16 prefill attention on the matrix cores
+#define BATON_PREFILL_MFMA 1   // bf16 prefill attention on the matrix cores (0: vector ALUs)
+#endif
+
+#ifndef BATON_PREFILL_SPLIT_LEN
+#define BATON_PREFILL_SPLIT_LEN 256   // longer prompts: two key streams per prefill workgroup
 #endif
 
 static_assert(BATON_MAX_BATCH == baton::kMetaThreads, "meta kernel covers every slot");
@@ -266,16 +270,25 @@ bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, hipStream_t s) 
 
 template <int D, int G>
 void launch_prefill_g(const baton_cache* c, baton::PrefillArgs& a, hipStream_t s) {
-  const bool mfma = BATON_PREFILL_MFMA && c->d.dtype == BATON_BF16;
-  const int32_t per_tile = mfma ? 16 : baton::kWave / (D * c->esz / 16);
+  const bool fa = BATON_PREFILL_MFMA && c->d.dtype == BATON_BF16;
+  const int32_t per_tile = fa ? 64 : baton::kWave / (D * c->esz / 16);
   int32_t tiles = 0;
   for (int32_t i = 0; i < a.n_ins; ++i) {
     tiles += (a.plen[i] + per_tile - 1) / per_tile;
     a.tile_end[i] = tiles;
   }
-  const dim3 grid((unsigned)tiles, (unsigned)(c->d.n_kv_heads * G));
-  if (mfma)
-    hipLaunchKernelGGL((baton::prefill_mfma_kernel<D, G>), grid, dim3(baton::kWave), 0, s, a);
+  const int32_t hq = c->d.n_kv_heads * G;
+  a.n_tiles = tiles;
+  // one XCD per kv-head's readers when the kv-heads (else the query heads) split evenly
+  a.unit_heads = c->d.n_kv_heads % 8 == 0 ? G : 1;
+  a.xcd_map = (hq / a.unit_heads) % 8 == 0 ? 1 : 0;
+  const dim3 grid((unsigned)((int64_t)tiles * hq));
+  int32_t longest = 0;
+  for (int32_t i = 0; i < a.n_ins; ++i) longest = std::max(longest, a.plen[i]);
+  if (fa && longest > BATON_PREFILL_SPLIT_LEN)
+    hipLaunchKernelGGL((baton::prefill_fa_kernel<D, G, 2>), grid, dim3(512), 0, s, a);
+  else if (fa)
+    hipLaunchKernelGGL((baton::prefill_fa_kernel<D, G, 1>), grid, dim3(256), 0, s, a);
   else if (c->d.dtype == BATON_BF16)
     hipLaunchKernelGGL((baton::prefill_valu_kernel<baton::BF16Tag, D, G>), grid, dim3(baton::kWave), 0, s, a);
   else
@@ -510,6 +523,8 @@ baton_status baton_shape_insert(baton_cache* c, const int32_t* slots, int32_t n,
   for (int32_t i = 0; i < n; ++i)
     if (c->lens[slots[i]] != 0) return BATON_ESLOT;
   if (c->L + T > c->d.capacity) return BATON_ECAPACITY;
+  // a prompt's keys of all kv-heads are addressed with 32-bit byte offsets
+  if ((int64_t)T * c->d.n_kv_heads * c->d.head_dim * c->esz >= (int64_t(1) << 31)) return BATON_EINVAL;
   bool others = false;
   for (int32_t b = 0; b < c->d.batch; ++b) others |= c->lens[b] > 0;
   if (T > 1 && others && (int32_t)c->holes.size() + 1 > BATON_MAX_HOLES) return BATON_ECAPACITY;

@@ -6,17 +6,18 @@
 // position's key and value is appended to the cache as column L + T - p + i.
 // The other rows of the step are decoded by the work-item kernels.
 //
-// Work: one wave per (tile of prompt positions, query head); the tiles of the
-// prefilled queries are numbered consecutively, a query's longest tiles (the
-// last positions, which see the most keys) first.  Keys and values come
-// straight from k_new / v_new (the whole prompt is read by every tile of a
+// Work: one workgroup per (tile of prompt positions, query head); the tiles
+// of the prefilled queries are numbered consecutively, a query's longest
+// tiles (the last positions, which see the most keys) first.  Keys and values
+// come straight from k_new / v_new (the prompt is read by every tile of a
 // head, through the caches).  The first query head of each kv-head appends
-// its tile's positions.
+// its tile's positions.  bf16 runs on the matrix cores (prefill_fa_kernel),
+// fp32 on the vector ALUs (prefill_valu_kernel).
 #pragma once
 
 #include "common.hpp"
 #include "decode_attn.hpp"
-#include "decode_attn_mfma.hpp"
+#include "decode_attn_mfma.hpp"   // bf16x8, f32x4, as_bf16x8
 
 namespace baton {
 
@@ -31,31 +32,54 @@ struct PrefillArgs {
   uint32_t* out;            // [batch][T][n_q_heads][D]
   int64_t cap, base, L;
   int32_t T, layer, batch, n_kv_heads, n_ins;
+  int32_t n_tiles;          // tiles over all prefilled queries (per query head)
+  int32_t unit_heads;       // query heads that read the same keys (G), or 1
+  int32_t xcd_map;          // 1: keep each unit's workgroups on one XCD (units % 8 == 0)
   float qscale;             // scale * log2(e)
   int32_t slot[kMaxPrefill];
   int32_t plen[kMaxPrefill];
   int32_t tile_end[kMaxPrefill];   // inclusive prefix of tiles over the prefilled queries
 };
 
-// The prefilled query and tile of block x; tiles are handed out last first.
-__device__ __forceinline__ void prefill_tile(const PrefillArgs& a, int32_t& i, int32_t& tile) {
-  const int32_t g = blockIdx.x;
-  i = 0;
-  while (i < a.n_ins - 1 && g >= a.tile_end[i]) ++i;
-  tile = a.tile_end[i] - 1 - g;   // the query's tiles, counted from its last one
+// The work of this workgroup: query head hq, prefilled query ins, tile.  The
+// grid is one-dimensional, n_tiles per query head.  Workgroups are dealt to
+// the XCDs round-robin by index, and each XCD has its own L2; with xcd_map the
+// index is decoded so that all workgroups reading one kv-head's keys (a unit:
+// its G query heads x all tiles) run on the same XCD.  Within a query head a
+// prefilled query's tiles are handed out last first (the last positions see
+// the most keys).
+__device__ __forceinline__ void prefill_work(const PrefillArgs& a, int& hq, int32_t& ins,
+                                             int32_t& tile) {
+  const int32_t L = blockIdx.x;
+  int32_t g;
+  if (a.xcd_map) {
+    const int32_t xcd = L % 8, k = L / 8;
+    const int32_t per_unit = a.n_tiles * a.unit_heads;
+    const int32_t u = xcd + 8 * (k / per_unit);
+    const int32_t r = k % per_unit;
+    hq = u * a.unit_heads + r / a.n_tiles;
+    g = r % a.n_tiles;
+  } else {
+    hq = L / a.n_tiles;
+    g = L % a.n_tiles;
+  }
+  ins = 0;
+  while (ins < a.n_ins - 1 && g >= a.tile_end[ins]) ++ins;
+  tile = a.tile_end[ins] - 1 - g;   // the query's tiles, counted from its last one
 }
 
-// Appends prompt positions [t0, t0 + n) of kv-head h (all lanes of the wave).
+// Appends prompt positions [t0, t0 + n) of kv-head h (threads tid of nthr).
 template <int VPT>
 __device__ __forceinline__ void prefill_append(const PrefillArgs& a, int b, int h, int32_t p,
-                                               int64_t row0, int32_t t0, int32_t n, int lane) {
+                                               int64_t row0, int32_t t0, int32_t n, int tid,
+                                               int nthr = kWave) {
   const int64_t ring_row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
   u32x4* rk = reinterpret_cast<u32x4*>(a.k) + ring_row * a.cap * VPT;
   u32x4* rv = reinterpret_cast<u32x4*>(a.v) + ring_row * a.cap * VPT;
   const u32x4* kin = reinterpret_cast<const u32x4*>(a.knew);
   const u32x4* vin = reinterpret_cast<const u32x4*>(a.vnew);
   const int64_t c0 = a.base + a.L + a.T - p;   // < 2 * cap: base < cap, L + T <= cap
-  for (int idx = lane; idx < n * VPT; idx += kWave) {
+  for (int idx = tid; idx < n * VPT; idx += nthr) {
     const int32_t t = t0 + idx / VPT;
     const int e = idx % VPT;
     int64_t col = c0 + t;
@@ -66,86 +90,18 @@ __device__ __forceinline__ void prefill_append(const PrefillArgs& a, int b, int 
   }
 }
 
-// bf16 on the matrix cores: 16 prompt positions per wave as the 16 columns of
-// mfma_block's query operand, 32 keys per iteration, a causal mask per lane
-// (lane l scores the keys of position l % 16).
-template <int D, int G>
-__global__ void __launch_bounds__(kWave) prefill_mfma_kernel(const PrefillArgs a) {
-  using Geo = MfmaGeo<D>;
-  constexpr int VPT = Geo::kVpt, KK = Geo::kKk, DT = Geo::kDt;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[32 * Geo::kLdsRow];
-  const int hq = blockIdx.y, h = hq / G, lane = threadIdx.x;
-  const int g4 = lane / 16, c16 = lane % 16;
-  int32_t ins, tile;
-  prefill_tile(a, ins, tile);
-  const int b = a.slot[ins];
-  const int32_t p = a.plen[ins];
-  const int32_t i0 = tile * 16;
-  const int64_t row0 = (int64_t)b * a.T + (a.T - p);   // input row of prompt position 0
-  const int nkv = a.n_kv_heads, nq = nkv * G;
-  const u32x4* qin = reinterpret_cast<const u32x4*>(a.q);
-  const u32x4* kin = reinterpret_cast<const u32x4*>(a.knew);
-  const u32x4* vin = reinterpret_cast<const u32x4*>(a.vnew);
-  const u32x4 zero = {0, 0, 0, 0};
-
-  const int32_t qi = i0 + c16;                          // this lane's query position
-  bf16x8 qb[KK];
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk)
-    qb[kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] : zero);
-
-  float m = -INFINITY, lsum = 0.f;
-  f32x4 o[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int32_t last = min(i0 + 15, p - 1);            // last position of the tile
-  const int tau = (c16 / 4) + 4 * (c16 % 4);          // token of this lane's key row in a tile
-  for (int32_t tt = 0; tt <= last; tt += 32) {
-    u32x4 kA[KK], kB[KK], vw[Geo::kVLoads];
-    const int32_t ta = tt + tau, tb = tt + 16 + tau;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kA[kk] = ta < p ? kin[((row0 + ta) * nkv + h) * VPT + kk * 4 + g4] : zero;
-      kB[kk] = tb < p ? kin[((row0 + tb) * nkv + h) * VPT + kk * 4 + g4] : zero;
-    }
-#pragma unroll
-    for (int u = 0; u < Geo::kVLoads; ++u) {
-      const int32_t t = tt + u * Geo::kTpiV + lane / VPT;
-      vw[u] = t < p ? vin[((row0 + t) * nkv + h) * VPT + lane % VPT] : zero;
-    }
-    const int32_t lim = qi < p ? qi - tt : -1;         // keys tt .. tt + lim are visible
-    const uint32_t mask = lim >= 31 ? 0xFFFFFFFFu : (lim < 0 ? 0u : ((2u << lim) - 1u));
-    mfma_block<D, G>(kA, kB, vw, qb, mask, a.qscale, lds, m, lsum, o, lane);
-  }
-
-  // Row sums over the four lane groups; lane l's output rows are positions i0 + 4*g4 + r.
-  lsum += __shfl_xor(lsum, 16, kWave);
-  lsum += __shfl_xor(lsum, 32, kWave);
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int qr = 4 * g4 + r;
-    const float lr = __shfl(lsum, qr, kWave);
-    if (i0 + qr < p) {
-      const float inv = 1.f / lr;
-      uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + i0 + qr) * nq + hq) * D;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o16[16 * dt + c16] = (uint16_t)f32_to_bf16_rne(o[dt][r] * inv);
-    }
-  }
-  if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, i0, min(16, p - i0), lane);
-}
-
 // Any element type on the vector ALUs: a prompt position per lane group (LPT
 // lanes, 16 bytes each), TPI positions per wave, the keys one at a time.
 template <typename T, int D, int G>
 __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a) {
   using Geo = Geometry<T, D>;
   constexpr int EPL = Geo::kEpl, LPT = Geo::kLpt, TPI = Geo::kTpi, VPT = Geo::kVpt;
-  const int hq = blockIdx.y, h = hq / G, lane = threadIdx.x;
+  const int lane = threadIdx.x;
   const int r = lane / LPT, cl = lane % LPT;
+  int hq;
   int32_t ins, tile;
-  prefill_tile(a, ins, tile);
+  prefill_work(a, hq, ins, tile);
+  const int h = hq / G;
   const int b = a.slot[ins];
   const int32_t p = a.plen[ins];
   const int32_t i0 = tile * TPI;
@@ -194,6 +150,230 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
     reinterpret_cast<u32x4*>(a.out)[((row0 + qi) * nq + hq) * VPT + cl] = Lane16<T>::narrow(o);
   }
   if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, i0, min(TPI, p - i0), lane);
+}
+
+// bf16 on the matrix cores, flash-attention style: a workgroup of 4*S waves
+// takes 64 prompt positions of one query head; four waves cover the positions
+// (16 each) and S such quartets split the keys, each walking every S-th tile
+// of KT keys (S tiles staged in LDS per iteration, K and V both as rows,
+// 16-byte stores), and the quartets' softmax states merge through LDS at the
+// end -- S shortens the longest causal tile's chain of iterations.
+//  * QK^T: A = 16 key rows (lane l: key l % 16 of the half tile), B = the
+//    wave's 16 positions; the score of key 4*(l/16) + r (first 16 keys) and
+//    16 + 4*(l/16) + r (next 16) for position l % 16 lands in lane l,
+//    register r.
+//  * PV: A = P with k = 8*(l/16) + e standing for key 4*(l/16) + e (e < 4)
+//    and 16 + 4*(l/16) + e - 4 (e >= 4); B = V rows in that order, read with
+//    the LDS transpose load (ds_read_b64_tr_b16): within a group of 16 lanes,
+//    lane i receives element i % 4 of the 8-byte block addressed by lane
+//    i / 4 + 4e, for e = 0..3; lane m of group g addresses key 4g + m / 4 at
+//    columns 16*dt + 4*(m % 4), so lane i gets V[4g + e][16*dt + i].
+// Rows are padded to 8 dwords past a multiple of 32, so that the 16 rows of a
+// transpose load spread over all banks.
+#ifndef BATON_PREFILL_KT
+#define BATON_PREFILL_KT 64
+#endif
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint8_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(__attribute__((address_space(3))) void*)(p));
+}
+
+template <int D, int G, int S>
+__global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a) {
+  constexpr int VPT = D / 8, KK = D / 32, DT = D / 16;
+  constexpr int KT = BATON_PREFILL_KT;       // keys per LDS tile and key stream
+  constexpr int ROW = D * 2 + 32;            // bytes per staged key / value row
+  constexpr int NT = 256 * S;                // threads
+  constexpr int NLD = KT * VPT / 256;        // 16-byte vectors per thread per stage, K and V each
+  constexpr int REC = DT * 4 + 2;            // floats per lane of a merged softmax state
+  static_assert((ROW / 4) % 32 == 8, "row padding");
+  static_assert(S == 1 || (S - 1) * 4 * kWave * REC * 4 <= S * KT * ROW, "merge area");
+  __shared__ __attribute__((aligned(16))) uint8_t ldsK[S * KT * ROW];
+  __shared__ __attribute__((aligned(16))) uint8_t ldsV[S * KT * ROW];
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = tid % kWave;
+  const int ks = wave / 4;                             // key stream of this wave
+  const int g4 = lane / 16, c16 = lane % 16;
+  int hq;
+  int32_t ins, tile;
+  prefill_work(a, hq, ins, tile);
+  const int h = hq / G;
+  const int b = a.slot[ins];
+  const int32_t p = a.plen[ins];
+  const int32_t wg0 = tile * 64;                       // first position of the workgroup
+  const int32_t i0 = wg0 + (wave % 4) * 16;            // first position of this wave
+  const int64_t row0 = (int64_t)b * a.T + (a.T - p);
+  const int nkv = a.n_kv_heads, nq = nkv * G;
+  const u32x4* qin = reinterpret_cast<const u32x4*>(a.q);
+  const u32x4* kin = reinterpret_cast<const u32x4*>(a.knew);
+  const u32x4* vin = reinterpret_cast<const u32x4*>(a.vnew);
+  const u32x4 zero = {0, 0, 0, 0};
+
+  const int32_t qi = i0 + c16;
+  bf16x8 qb[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk)
+    qb[kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] : zero);
+
+  float m = -INFINITY, lsum = 0.f;
+  f32x4 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int32_t wg_last = min(wg0 + 63, p - 1);
+  const int32_t w_last = min(i0 + 15, p - 1);
+  // This lane's transpose-load address within a value row block: key offset
+  // 4*g4 + c16/4, columns 4*(c16 % 4).
+  const int tr_off = (4 * g4 + c16 / 4) * ROW + (c16 % 4) * 8;
+  // The prompt's keys and values of head h as raw buffers: token t's row at
+  // byte t * nkv * D * 2; a token past the prompt gets an offset beyond the
+  // range, which loads zeros (no branch, no wait per load).
+  const uint32_t tok_bytes = (uint32_t)nkv * VPT * 16;
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<u32x4*>(kin + (row0 * nkv + h) * VPT), 0, (uint32_t)p * tok_bytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<u32x4*>(vin + (row0 * nkv + h) * VPT), 0, (uint32_t)p * tok_bytes, kBufferWord3);
+  u32x4 kr[NLD], vr[NLD];
+  auto fetch = [&](int32_t kt, u32x4 (&kr)[NLD], u32x4 (&vr)[NLD]) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int v = tid + NT * u;
+      const int32_t t = kt + v / VPT;
+      const uint32_t off = t < p ? (uint32_t)t * tok_bytes + (uint32_t)(v % VPT) * 16u : 0x80000000u;
+      kr[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off, 0, 0));
+      vr[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off, 0, 0));
+    }
+  };
+  auto compute = [&](int32_t k0) {
+#pragma unroll
+    for (int half = 0; half < KT / 32; ++half) {
+      const int kb = ks * KT + 32 * half;              // key row of the block in the stage
+      const int32_t tt = k0 + kb;
+      if (tt > w_last) break;                          // wave-uniform
+      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const u32x4 ka = *reinterpret_cast<const u32x4*>(ldsK + (kb + c16) * ROW + (kk * 4 + g4) * 16);
+        const u32x4 kc = *reinterpret_cast<const u32x4*>(ldsK + (kb + 16 + c16) * ROW + (kk * 4 + g4) * 16);
+        sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka), qb[kk], sa, 0, 0, 0);
+        sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc), qb[kk], sb, 0, 0, 0);
+      }
+      const int32_t lim = qi < p ? qi - tt : -1;       // keys tt .. tt + lim are visible
+      float s[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s[r] = 4 * g4 + r <= lim ? sa[r] * a.qscale : -INFINITY;
+        s[4 + r] = 16 + 4 * g4 + r <= lim ? sb[r] * a.qscale : -INFINITY;
+      }
+      float mx = s[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float mn = fmaxf(m, mx);
+      const float ref = mn == -INFINITY ? 0.f : mn;
+      // exponents are <= 0 here: the hardware exp2 (results below the
+      // smallest normal flush to 0, which a softmax weight may)
+      const float alpha = __builtin_amdgcn_exp2f(m - ref);
+      bf16x8 pa;
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const __bf16 pb = (__bf16)__builtin_amdgcn_exp2f(s[e] - ref);
+        pa[e] = pb;
+        psum += (float)pb;
+      }
+      lsum = lsum * alpha + psum;
+      m = mn;
+      // Rescale the accumulators only when some position's maximum moved
+      // (after the first keys it rarely does).
+      if (__ballot(alpha != 1.f)) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float ar = __shfl(alpha, 4 * g4 + r, kWave);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt][r] *= ar;
+        }
+      }
+      const uint8_t* vblk = ldsV + kb * ROW + tr_off;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const s16x4 lo = lds_read_tr16(vblk + dt * 32);
+        const s16x4 hi = lds_read_tr16(vblk + 16 * ROW + dt * 32);
+        const s16x4 w2[2] = {lo, hi};
+        const bf16x8 vb = __builtin_bit_cast(bf16x8, w2);
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
+      }
+    }
+  };
+  // The next stage's loads are in flight while the current one is computed.
+  fetch(0, kr, vr);
+  for (int32_t k0 = 0; k0 <= wg_last; k0 += S * KT) {   // bounds are workgroup-uniform
+    __syncthreads();                                   // the previous stage is consumed
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int v = tid + NT * u;
+      const int off = (v / VPT) * ROW + (v % VPT) * 16;
+      *reinterpret_cast<u32x4*>(ldsK + off) = kr[u];
+      *reinterpret_cast<u32x4*>(ldsV + off) = vr[u];
+    }
+    __syncthreads();
+    if (k0 + S * KT <= wg_last) fetch(k0 + S * KT, kr, vr);
+    compute(k0);
+  }
+
+  if constexpr (S > 1) {
+    // Key streams 1.. hand their states to stream 0 (same positions, same lane).
+    __syncthreads();                                   // the stage buffers are free
+    float* mrg = reinterpret_cast<float*>(ldsK) + ((ks - 1) * 4 + wave % 4) * kWave * REC + lane * REC;
+    if (ks > 0) {
+      mrg[0] = m;
+      mrg[1] = lsum;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mrg[2 + dt * 4 + r] = o[dt][r];
+    }
+    __syncthreads();
+    if (ks == 0) {
+#pragma unroll
+      for (int k = 1; k < S; ++k) {
+        const float* src = reinterpret_cast<const float*>(ldsK) + ((k - 1) * 4 + wave % 4) * kWave * REC + lane * REC;
+        const float m2 = src[0];
+        const float mm = fmaxf(m, m2);
+        const float fa = m == -INFINITY ? 0.f : exp2f(m - mm);
+        const float fb = m2 == -INFINITY ? 0.f : exp2f(m2 - mm);
+        lsum = lsum * fa + src[1] * fb;
+        m = mm;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float far = __shfl(fa, 4 * g4 + r, kWave);
+          const float fbr = __shfl(fb, 4 * g4 + r, kWave);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt][r] = o[dt][r] * far + src[2 + dt * 4 + r] * fbr;
+        }
+      }
+    }
+  }
+  if (ks == 0) {
+    lsum += __shfl_xor(lsum, 16, kWave);
+    lsum += __shfl_xor(lsum, 32, kWave);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qr = 4 * g4 + r;
+      const float lr = __shfl(lsum, qr, kWave);
+      if (i0 + qr < p) {
+        const float inv = 1.f / lr;
+        uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + i0 + qr) * nq + hq) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o16[16 * dt + c16] = (uint16_t)f32_to_bf16_rne(o[dt][r] * inv);
+      }
+    }
+  }
+  if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, wg0, min(64, p - wg0), tid, NT);
 }
 
 }  // namespace baton
