@@ -160,6 +160,11 @@ baton_status baton_kv_embed(baton_cache* cache, const int32_t* slots, int32_t n,
  * layout baton_kv_embed takes, so baton_kv_embed(slot', len, k_dst, v_dst)
  * re-inserts the query into any free slot with its tokens bit for bit.  The
  * batch is not changed; preempting a query is extract, then baton_kv_evict.
+ * The destinations (and baton_kv_embed's sources) may be device memory or
+ * pinned host memory mapped for the device (hipHostMalloc; pass its device
+ * address, hipHostGetDevicePointer): the kernel then moves the tokens over the
+ * host link directly, with no device staging -- queries parked in host memory
+ * to scale the batch.
  * Errors: EINVAL (n < 0, null arrays or pointers, misaligned pointer, slot out
  * of range, duplicate), ESLOT (a slot is free), ESTATE (inside a decode step),
  * EHIP.

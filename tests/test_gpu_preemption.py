@@ -66,3 +66,61 @@ def test_host_round_trip():
         B.baton_kv_extract(cache.handle, [1, 1], [dk, dk], [dv, dv])
     assert e.value.status == B.BATON_EINVAL
     cache.close()
+
+
+def _device_pointer(host_ptr):
+    """The device address of pinned host memory (HIP's own answer), or None."""
+    import ctypes
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+    except OSError:
+        return None
+    out = ctypes.c_void_p()
+    rc = hip.hipHostGetDevicePointer(ctypes.byref(out), ctypes.c_void_p(host_ptr), ctypes.c_uint(0))
+    return out.value if rc == 0 else None
+
+
+def test_direct_host_offload():
+    """Batch-size scaling with the keys and values held in host memory: extract
+    writes straight into pinned host buffers over PCIe, and embed reads them back
+    from there, with no device staging -- the same bits as through device memory."""
+    import time
+    from workload import driver
+    from workload.configs import Workload
+    w = Workload("h", "bf16", 2, 4, 8, 2, 128, 1, 0, seed=5)
+    dev = driver.DeviceInputs(w)
+    lens = [40, 300, 17]
+    caches = []
+    for _ in range(2):
+        c = BatonCache(2, 4, 8, 2, 128, capacity=512, dtype="bf16")
+        srcs = [dev.prefill(q, n) for q, n in zip([0, 1, 2], lens)]
+        c.embed([0, 1, 2], lens, [s[0] for s in srcs], [s[1] for s in srcs])
+        caches.append(c)
+    torch.cuda.synchronize()
+    direct, staged = caches
+    n = direct.tokens()[1]
+    hk = torch.empty((2, 2, n, 128), dtype=torch.bfloat16, pin_memory=True)
+    hv = torch.empty_like(hk, pin_memory=True)
+    dk, dv = _device_pointer(hk.data_ptr()), _device_pointer(hv.data_ptr())
+    if dk is None or dv is None:
+        pytest.skip("pinned host memory is not mapped for the device")
+    t0 = time.perf_counter()
+    B.baton_kv_extract(direct.handle, [1], [dk], [dv], torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    print(f"[offload] {2 * hk.numel() * 2 / 1e6:.1f} MB extracted to host in {dt * 1e3:.2f} ms", flush=True)
+    ks, vs = staged.extract([1])
+    assert np.array_equal(parity.host_bits(ks[0]), hk.view(torch.int16).numpy().view(np.uint16))
+    assert np.array_equal(parity.host_bits(vs[0]), hv.view(torch.int16).numpy().view(np.uint16))
+    for c in caches:
+        c.evict([1], release=True)
+    B.baton_kv_embed(direct.handle, [3], [n], [dk], [dv], torch.cuda.current_stream())
+    staged.embed([3], [n], ks, vs)
+    for c in caches:
+        c.flush()
+    torch.cuda.synchronize()
+    assert direct.query() == staged.query()
+    assert np.array_equal(parity.host_bits(direct.k), parity.host_bits(staged.k))
+    assert np.array_equal(parity.host_bits(direct.v), parity.host_bits(staged.v))
+    for c in caches:
+        c.close()
