@@ -294,6 +294,64 @@ baton_status baton_cache_tokens(const baton_cache* cache, int32_t* tokens);
  */
 baton_status baton_set_split_tokens(baton_cache* cache, int32_t tokens);
 
+/*
+ * ---- A whole decode layer around the attention --------------------------
+ * The paper serves llama2-7b (sec. 5; its layers as sec. 2.1 describes them:
+ * W^Q, W^K, W^V projections, attention, feed-forward networks between).
+ * These calls are the rest of such a layer, so that a decode step runs end to
+ * end: RMS normalisation, the projections (hipBLASLt GEMMs), rotary position
+ * embedding at each query's own position, the gated feed-forward.  bf16 only;
+ * every output is rounded to nearest even.
+ */
+typedef struct baton_gemm baton_gemm; /* opaque: a hipBLASLt handle and its cached algorithm choices */
+
+/* Create / free a GEMM handle (hipBLASLt keeps internal resources of its own).
+   Errors: EINVAL (null out), EHIP. */
+baton_status baton_gemm_create(baton_gemm** out);
+baton_status baton_gemm_destroy(baton_gemm* gemm);
+
+/*
+ * y[r] (+)= x[r] . W^T for r < rows: x device [rows][in_dim], W device
+ * [out_dim][in_dim] (a linear layer's stored weight), y device [rows][out_dim];
+ * accumulate = 1 adds to y (the residual stream), 0 overwrites it.  fp32
+ * accumulation.  ws: device workspace the GEMM may use (ws_bytes, may be 0).
+ * Errors: EINVAL (null or misaligned pointer, sizes < 1 or not multiples of 8,
+ * accumulate not 0/1), EDTYPE (dtype not bf16), EHIP (no algorithm fits).
+ */
+baton_status baton_linear(baton_gemm* gemm, int32_t dtype, const void* x, const void* w, void* y,
+                          int32_t rows, int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws,
+                          size_t ws_bytes, hipStream_t stream);
+
+/*
+ * y[r] = x[r] / sqrt(mean_j x[r][j]^2 + eps) * gain: x, y device [rows][dim],
+ * gain device [dim]; dim a multiple of 8.  y may alias x.
+ * Errors: EINVAL (null or misaligned pointer, bad sizes, eps < 0), EDTYPE.
+ */
+baton_status baton_rmsnorm(int32_t dtype, const void* x, const void* gain, void* y, int32_t rows,
+                           int32_t dim, float eps, hipStream_t stream);
+
+/*
+ * Split a fused projection qkv device [batch][(n_q_heads + 2 n_kv_heads)
+ * head_dim] (query heads, then key heads, then value heads) into q
+ * [batch][n_q_heads][head_dim], k_new and v_new [batch][n_kv_heads][head_dim],
+ * rotating q and k: pair (i, i + head_dim/2) of a head by angle
+ * pos_b * theta^(-2i/head_dim), pos_b = slot b's token count
+ * (baton_cache_tokens), the position of the token being decoded.  The angles
+ * are taken in double precision.  Decode steps only.
+ * Errors: EINVAL (null pointer, theta <= 1), EDTYPE (cache not bf16), ESTATE
+ * (a prefill is registered), EHIP.
+ */
+baton_status baton_rope_qkv(const baton_cache* cache, const void* qkv, void* q, void* k_new, void* v_new,
+                            float theta, hipStream_t stream);
+
+/*
+ * out[r][j] = silu(gate_up[r][j]) * gate_up[r][dim + j], silu(z) = z / (1 + e^-z):
+ * gate_up device [rows][2 dim] (gate, then up), out device [rows][dim].
+ * Errors: EINVAL (null or misaligned pointer, dim not a multiple of 8), EDTYPE.
+ */
+baton_status baton_silu_mul(int32_t dtype, const void* gate_up, void* out, int32_t rows, int32_t dim,
+                            hipStream_t stream);
+
 /* Static English text of a status. */
 const char* baton_status_string(baton_status status);
 

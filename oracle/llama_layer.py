@@ -81,7 +81,7 @@ def to_bits(x, dtype):
     return ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
 
 
-def decode_layer(pb, layer, x, w, positions, theta, eps, scale=None):
+def decode_layer(pb, layer, x, w, positions, theta, eps, scale=None, stored=None):
     """One decode layer of the batch in float64.
 
     pb: the baton_oracle.PaddedBatch (its decode_layer appends this layer's
@@ -90,15 +90,20 @@ def decode_layer(pb, layer, x, w, positions, theta, eps, scale=None):
     norm2 [hidden], gate_up [2 F][hidden] (gate rows first), down [hidden][F];
     positions [B]: each slot's token count.  Keys and values enter the cache
     rounded to the cache's element type, as the GPU stores them.  Returns the
-    new residual stream [B][hidden] (free rows unchanged)."""
+    new residual stream [B][hidden] (free rows unchanged).
+
+    stored: None, or an element type in which every intermediate is stored
+    between operations (the GPU's bf16 activations); the rounding then happens
+    where the GPU rounds, and only the order of accumulation differs."""
     Hq, Hkv, D = pb.Hq, pb.Hkv, pb.D
-    h = rmsnorm(x, w["norm1"], eps)
-    q, k, v = split_qkv(linear(h, w["qkv"]), Hq, Hkv, D)
+    r = (lambda v: v) if stored is None else (lambda v: widen(to_bits(v, stored), stored))
+    h = r(rmsnorm(x, w["norm1"], eps))
+    q, k, v = split_qkv(r(linear(h, w["qkv"])), Hq, Hkv, D)
     pos = np.asarray(positions, np.float64)[:, None]
     q, k = rope(q, pos, theta), rope(k, pos, theta)
-    att = pb.decode_layer(layer, to_bits(q, pb.dtype), to_bits(k, pb.dtype), to_bits(v, pb.dtype), scale)
-    x = x + linear(att.reshape(att.shape[0], Hq * D), w["o"])
-    h2 = rmsnorm(x, w["norm2"], eps)
-    gu = linear(h2, w["gate_up"])
+    att = r(pb.decode_layer(layer, to_bits(q, pb.dtype), to_bits(k, pb.dtype), to_bits(v, pb.dtype), scale))
+    x = r(x + linear(att.reshape(att.shape[0], Hq * D), w["o"]))
+    h2 = r(rmsnorm(x, w["norm2"], eps))
+    gu = r(linear(h2, w["gate_up"]))
     F = gu.shape[-1] // 2
-    return x + linear(silu(gu[:, :F]) * gu[:, F:], w["down"])
+    return r(x + linear(r(silu(gu[:, :F]) * gu[:, F:]), w["down"]))

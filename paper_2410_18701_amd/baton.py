@@ -67,13 +67,21 @@ def lib():
         L.baton_cache_flush.argtypes = [vp, vp]
         L.baton_cache_query.argtypes = [vp, P(i64), P(i64), P(i32)]
         L.baton_set_split_tokens.argtypes = [vp, i32]
+        L.baton_gemm_create.argtypes = [P(vp)]
+        L.baton_gemm_destroy.argtypes = [vp]
+        L.baton_linear.argtypes = [vp, i32, vp, vp, vp, i32, i32, i32, i32, vp, ctypes.c_size_t, vp]
+        L.baton_rmsnorm.argtypes = [i32, vp, vp, vp, i32, i32, ctypes.c_float, vp]
+        L.baton_rope_qkv.argtypes = [vp, vp, vp, vp, vp, ctypes.c_float, vp]
+        L.baton_silu_mul.argtypes = [i32, vp, vp, i32, i32, vp]
         L.baton_status_string.argtypes = [st]
         L.baton_status_string.restype = ctypes.c_char_p
         for name in ("baton_cache_create", "baton_cache_destroy", "baton_kv_evict", "baton_kv_embed",
                      "baton_kv_extract",
                      "baton_build_mask", "baton_decode_attn", "baton_step_advance",
                      "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
-                     "baton_shape_insert", "baton_cache_tokens"):
+                     "baton_shape_insert", "baton_cache_tokens", "baton_gemm_create",
+                     "baton_gemm_destroy", "baton_linear", "baton_rmsnorm", "baton_rope_qkv",
+                     "baton_silu_mul"):
             getattr(L, name).restype = st
         _lib = L
     return _lib
@@ -194,3 +202,33 @@ def baton_cache_query(cache, batch):
 
 def baton_set_split_tokens(cache, tokens):
     _check(lib().baton_set_split_tokens(cache, tokens), "baton_set_split_tokens")
+
+
+# ---- decode layer around the attention ----
+def baton_gemm_create():
+    out = ctypes.c_void_p()
+    _check(lib().baton_gemm_create(ctypes.byref(out)), "baton_gemm_create")
+    return out.value
+
+
+def baton_gemm_destroy(gemm):
+    _check(lib().baton_gemm_destroy(gemm), "baton_gemm_destroy")
+
+
+def baton_linear(gemm, dtype, x, w, y, rows, out_dim, in_dim, accumulate, ws, ws_bytes, stream=None):
+    _check(lib().baton_linear(gemm, dtype, _ptr(x), _ptr(w), _ptr(y), rows, out_dim, in_dim,
+                              int(accumulate), _ptr(ws), ws_bytes, _stream(stream)), "baton_linear")
+
+
+def baton_rmsnorm(dtype, x, gain, y, rows, dim, eps, stream=None):
+    _check(lib().baton_rmsnorm(dtype, _ptr(x), _ptr(gain), _ptr(y), rows, dim, float(eps), _stream(stream)),
+           "baton_rmsnorm")
+
+
+def baton_rope_qkv(cache, qkv, q, k_new, v_new, theta, stream=None):
+    _check(lib().baton_rope_qkv(cache, _ptr(qkv), _ptr(q), _ptr(k_new), _ptr(v_new), float(theta),
+                                _stream(stream)), "baton_rope_qkv")
+
+
+def baton_silu_mul(dtype, gate_up, out, rows, dim, stream=None):
+    _check(lib().baton_silu_mul(dtype, _ptr(gate_up), _ptr(out), rows, dim, _stream(stream)), "baton_silu_mul")

@@ -5,7 +5,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libbaton.so")
-SOURCES = [os.path.join(HERE, "csrc", "baton.hip")]
+SOURCES = [os.path.join(HERE, "csrc", "baton.hip"), os.path.join(HERE, "csrc", "layer.hip")]
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=gfx950",
@@ -17,7 +17,7 @@ FLAGS = [
 
 
 def build(verbose=False, extra=()):
-    cmd = ["hipcc", *FLAGS, *extra, *SOURCES, "-o", LIB + ".tmp"]
+    cmd = ["hipcc", *FLAGS, *extra, *SOURCES, "-lhipblaslt", "-o", LIB + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True, cwd=HERE)

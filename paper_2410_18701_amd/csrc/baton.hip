@@ -13,6 +13,7 @@
 #include "decode_attn.hpp"
 #include "decode_attn_mfma.hpp"
 #include "kv_ops.hpp"
+#include "layer_ops.hpp"
 #include "prefill_attn.hpp"
 
 #ifndef BATON_GQA_MFMA
@@ -713,6 +714,27 @@ baton_status baton_cache_tokens(const baton_cache* c, int32_t* tokens) {
   const baton::HoleList hl = hole_list(c);
   for (int32_t b = 0; b < c->d.batch; ++b) tokens[b] = row_tokens(c, b, hl);
   return BATON_OK;
+}
+
+baton_status baton_rope_qkv(const baton_cache* c, const void* qkv, void* q, void* k_new, void* v_new,
+                            float theta, hipStream_t stream) {
+  if (!c || !qkv || !q || !k_new || !v_new || !(theta > 1.f) || !std::isfinite(theta)) return BATON_EINVAL;
+  if (c->d.dtype != BATON_BF16) return BATON_EDTYPE;
+  if (c->n_prefill) return BATON_ESTATE;   // decode steps only
+  baton::RopeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.qkv = static_cast<const uint16_t*>(qkv);
+  a.q = static_cast<uint16_t*>(q);
+  a.k = static_cast<uint16_t*>(k_new);
+  a.v = static_cast<uint16_t*>(v_new);
+  a.n_q_heads = c->d.n_q_heads;
+  a.n_kv_heads = c->d.n_kv_heads;
+  a.head_dim = c->d.head_dim;
+  a.log2_theta = std::log2((double)theta);
+  const baton::HoleList hl = hole_list(c);
+  for (int32_t b = 0; b < c->d.batch; ++b) a.pos[b] = row_tokens(c, b, hl);
+  hipLaunchKernelGGL(baton::rope_qkv_kernel, dim3(c->d.batch), dim3(baton::kRowThreads), 0, stream, a);
+  return hip_status(hipGetLastError());
 }
 
 baton_status baton_set_split_tokens(baton_cache* c, int32_t tokens) {

@@ -1,0 +1,125 @@
+// Host side of the decode-layer operations around the attention: hipBLASLt
+// GEMMs for the projections, launches of the row and elementwise kernels.
+// The C ABI is documented in include/baton.h.
+#include <hip/hip_runtime.h>
+#include <hipblaslt/hipblaslt.h>
+
+#include <cmath>
+#include <map>
+#include <new>
+#include <tuple>
+
+#include "baton.h"
+#include "layer_ops.hpp"
+
+struct baton_gemm {
+  hipblasLtHandle_t lt = nullptr;
+  // Heuristic choice per (rows, out_dim, in_dim, accumulate, workspace bytes).
+  std::map<std::tuple<int32_t, int32_t, int32_t, int32_t, size_t>, hipblasLtMatmulAlgo_t> algos;
+};
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct LtDescs {
+  hipblasLtMatmulDesc_t op = nullptr;
+  hipblasLtMatrixLayout_t a = nullptr, b = nullptr, c = nullptr;
+  ~LtDescs() {
+    if (a) hipblasLtMatrixLayoutDestroy(a);
+    if (b) hipblasLtMatrixLayoutDestroy(b);
+    if (c) hipblasLtMatrixLayoutDestroy(c);
+    if (op) hipblasLtMatmulDescDestroy(op);
+  }
+};
+
+// y [rows][out] = x [rows][in] . w [out][in]^T in column-major terms:
+// y^T (out x rows) = op(A) . op(B) with A = w viewed as in x out (transposed)
+// and B = x viewed as in x rows.
+bool make_descs(LtDescs& d, int32_t rows, int32_t out, int32_t in) {
+  const hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
+  if (hipblasLtMatmulDescCreate(&d.op, HIPBLAS_COMPUTE_32F, HIP_R_32F) != HIPBLAS_STATUS_SUCCESS) return false;
+  if (hipblasLtMatmulDescSetAttribute(d.op, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof(ta)) != HIPBLAS_STATUS_SUCCESS ||
+      hipblasLtMatmulDescSetAttribute(d.op, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof(tb)) != HIPBLAS_STATUS_SUCCESS)
+    return false;
+  return hipblasLtMatrixLayoutCreate(&d.a, HIP_R_16BF, in, out, in) == HIPBLAS_STATUS_SUCCESS &&
+         hipblasLtMatrixLayoutCreate(&d.b, HIP_R_16BF, in, rows, in) == HIPBLAS_STATUS_SUCCESS &&
+         hipblasLtMatrixLayoutCreate(&d.c, HIP_R_16BF, out, rows, out) == HIPBLAS_STATUS_SUCCESS;
+}
+
+}  // namespace
+
+extern "C" {
+
+baton_status baton_gemm_create(baton_gemm** out) {
+  if (!out) return BATON_EINVAL;
+  baton_gemm* g = new (std::nothrow) baton_gemm();
+  if (!g) return BATON_EINVAL;
+  if (hipblasLtCreate(&g->lt) != HIPBLAS_STATUS_SUCCESS) {
+    delete g;
+    return BATON_EHIP;
+  }
+  *out = g;
+  return BATON_OK;
+}
+
+baton_status baton_gemm_destroy(baton_gemm* g) {
+  if (g) {
+    if (g->lt) hipblasLtDestroy(g->lt);
+    delete g;
+  }
+  return BATON_OK;
+}
+
+baton_status baton_linear(baton_gemm* g, int32_t dtype, const void* x, const void* w, void* y,
+                          int32_t rows, int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  if (!g || !x || !w || !y || rows < 1 || out_dim < 1 || in_dim < 1 || (ws_bytes && !ws)) return BATON_EINVAL;
+  if (accumulate != 0 && accumulate != 1) return BATON_EINVAL;
+  if (dtype != BATON_BF16) return BATON_EDTYPE;
+  if (!aligned16(x) || !aligned16(w) || !aligned16(y) || in_dim % 8 || out_dim % 8) return BATON_EINVAL;
+  LtDescs d;
+  if (!make_descs(d, rows, out_dim, in_dim)) return BATON_EHIP;
+  const auto key = std::make_tuple(rows, out_dim, in_dim, accumulate, ws_bytes);
+  auto it = g->algos.find(key);
+  if (it == g->algos.end()) {
+    hipblasLtMatmulPreference_t pref;
+    if (hipblasLtMatmulPreferenceCreate(&pref) != HIPBLAS_STATUS_SUCCESS) return BATON_EHIP;
+    const uint64_t max_ws = ws_bytes;
+    hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &max_ws, sizeof(max_ws));
+    hipblasLtMatmulHeuristicResult_t res[1];
+    int n = 0;
+    const hipblasStatus_t st = hipblasLtMatmulAlgoGetHeuristic(g->lt, d.op, d.a, d.b, d.c, d.c, pref, 1, res, &n);
+    hipblasLtMatmulPreferenceDestroy(pref);
+    if (st != HIPBLAS_STATUS_SUCCESS || n < 1 || res[0].workspaceSize > ws_bytes) return BATON_EHIP;
+    it = g->algos.emplace(key, res[0].algo).first;
+  }
+  const float alpha = 1.f, beta = accumulate ? 1.f : 0.f;
+  const hipblasStatus_t st = hipblasLtMatmul(g->lt, d.op, &alpha, w, d.a, x, d.b, &beta, y, d.c, y, d.c,
+                                             &it->second, ws, ws_bytes, stream);
+  return st == HIPBLAS_STATUS_SUCCESS ? BATON_OK : BATON_EHIP;
+}
+
+baton_status baton_rmsnorm(int32_t dtype, const void* x, const void* gain, void* y, int32_t rows, int32_t dim,
+                           float eps, hipStream_t stream) {
+  if (!x || !gain || !y || rows < 1 || dim < 8 || dim % 8 || !(eps >= 0.f) || !std::isfinite(eps)) return BATON_EINVAL;
+  if (dtype != BATON_BF16) return BATON_EDTYPE;
+  if (!aligned16(x) || !aligned16(gain) || !aligned16(y)) return BATON_EINVAL;
+  hipLaunchKernelGGL(baton::rmsnorm_kernel, dim3(rows), dim3(baton::kRowThreads), 0, stream,
+                     static_cast<const baton::u32x4*>(x), static_cast<const baton::u32x4*>(gain),
+                     static_cast<baton::u32x4*>(y), dim / 8, 1.0f / dim, eps);
+  return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
+}
+
+baton_status baton_silu_mul(int32_t dtype, const void* gate_up, void* out, int32_t rows, int32_t dim,
+                            hipStream_t stream) {
+  if (!gate_up || !out || rows < 1 || dim < 8 || dim % 8) return BATON_EINVAL;
+  if (dtype != BATON_BF16) return BATON_EDTYPE;
+  if (!aligned16(gate_up) || !aligned16(out)) return BATON_EINVAL;
+  const int64_t n_vec = (int64_t)rows * (dim / 8);
+  hipLaunchKernelGGL(baton::silu_mul_kernel, dim3((unsigned)((n_vec + 255) / 256)), dim3(256), 0, stream,
+                     static_cast<const baton::u32x4*>(gate_up), static_cast<baton::u32x4*>(out), dim / 8, n_vec);
+  return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
+}
+
+}  // extern "C"

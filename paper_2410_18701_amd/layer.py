@@ -1,0 +1,100 @@
+"""A whole decode layer around the re-batched attention, as C-ABI calls.
+
+Each method is argument marshalling for one libbaton call (paper_2410_18701_amd/
+baton.py); PyTorch provides the buffers.  The layer is the paper's model's
+(llama2-7b, sec. 5): RMS norm -> fused QKV projection -> rotary embedding at
+each query's token count -> re-batched attention (BatonCache.decode_attn) ->
+output projection added to the residual stream -> RMS norm -> gate/up
+projection -> silu(gate) * up -> down projection added to the residual stream.
+"""
+from . import baton as B
+
+
+def _stream():
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+class Gemm:
+    """A hipBLASLt handle for baton_linear, with a device workspace."""
+
+    def __init__(self, ws_bytes=32 << 20):
+        import torch
+        self.handle = B.baton_gemm_create()
+        self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+
+    def linear(self, x, w, y, accumulate=False):
+        """y (+)= x . w^T; x [rows][in], w [out][in], y [rows][out] (bf16, contiguous)."""
+        rows, in_dim = x.shape
+        out_dim = w.shape[0]
+        if w.shape[1] != in_dim or tuple(y.shape) != (rows, out_dim):
+            raise ValueError("linear: shapes do not match")
+        for t in (x, w, y):
+            if not t.is_contiguous():
+                raise ValueError("linear: contiguous tensors only")
+        B.baton_linear(self.handle, B.BATON_BF16, x, w, y, rows, out_dim, in_dim, accumulate, self.ws,
+                       self.ws.numel(), _stream())
+        return y
+
+    def close(self):
+        if self.handle:
+            B.baton_gemm_destroy(self.handle)
+            self.handle = None
+
+
+def rmsnorm(x, gain, y, eps):
+    rows, dim = x.shape
+    if tuple(y.shape) != (rows, dim) or gain.numel() != dim:
+        raise ValueError("rmsnorm: shapes do not match")
+    B.baton_rmsnorm(B.BATON_BF16, x, gain, y, rows, dim, eps, _stream())
+    return y
+
+
+def silu_mul(gate_up, out):
+    rows, two_f = gate_up.shape
+    if tuple(out.shape) != (rows, two_f // 2):
+        raise ValueError("silu_mul: shapes do not match")
+    B.baton_silu_mul(B.BATON_BF16, gate_up, out, rows, two_f // 2, _stream())
+    return out
+
+
+def rope_qkv(cache, qkv, q, k_new, v_new, theta):
+    width = (cache.n_q_heads + 2 * cache.n_kv_heads) * cache.head_dim
+    if tuple(qkv.shape) != (cache.batch, width):
+        raise ValueError("rope_qkv: qkv must be [batch][(Hq + 2 Hkv) * head_dim]")
+    if q.numel() != cache.batch * cache.n_q_heads * cache.head_dim or \
+            k_new.numel() != cache.batch * cache.n_kv_heads * cache.head_dim or v_new.numel() != k_new.numel():
+        raise ValueError("rope_qkv: output sizes do not match the cache")
+    B.baton_rope_qkv(cache.handle, qkv, q, k_new, v_new, theta, _stream())
+
+
+class DecodeLayers:
+    """The layers of one model over one BatonCache, with preallocated activations.
+
+    weights[layer]: dict of bf16 device tensors norm1 [hid], qkv [(Hq + 2 Hkv) D][hid],
+    o [hid][Hq D], norm2 [hid], gate_up [2 F][hid], down [hid][F]."""
+
+    def __init__(self, cache, weights, gemm, theta=10000.0, eps=1e-5):
+        import torch
+        self.cache, self.w, self.gemm, self.theta, self.eps = cache, weights, gemm, theta, eps
+        Bt, Hq, Hkv, D = cache.batch, cache.n_q_heads, cache.n_kv_heads, cache.head_dim
+        hid = weights[0]["norm1"].numel()
+        F = weights[0]["down"].shape[1]
+        e = lambda *s: torch.empty(s, dtype=torch.bfloat16, device="cuda")
+        self.h, self.qkv = e(Bt, hid), e(Bt, (Hq + 2 * Hkv) * D)
+        self.q, self.k, self.v, self.att = e(Bt, Hq, D), e(Bt, Hkv, D), e(Bt, Hkv, D), e(Bt, Hq, D)
+        self.gu, self.act = e(Bt, 2 * F), e(Bt, F)
+
+    def layer(self, layer, x):
+        """One layer of the decode step on the residual stream x [batch][hid] (in place)."""
+        w = self.w[layer]
+        rmsnorm(x, w["norm1"], self.h, self.eps)
+        self.gemm.linear(self.h, w["qkv"], self.qkv)
+        rope_qkv(self.cache, self.qkv, self.q, self.k, self.v, self.theta)
+        self.cache.decode_attn(layer, self.q, self.k, self.v, out=self.att)
+        self.gemm.linear(self.att.view(self.att.shape[0], -1), w["o"], x, accumulate=True)
+        rmsnorm(x, w["norm2"], self.h, self.eps)
+        self.gemm.linear(self.h, w["gate_up"], self.gu)
+        silu_mul(self.gu, self.act)
+        self.gemm.linear(self.act, w["down"], x, accumulate=True)
+        return x

@@ -1,0 +1,160 @@
+"""The decode layer around the attention on the GPU (through the C ABI) against
+the layer oracle: each operation on the GPU's own inputs, then whole layers
+over several decode steps with evictions and insertions, on a small model and
+on llama2-7b's shapes.
+
+Tolerances: an operation's output is stored in bf16 (8 significant bits), so
+one operation may differ from the float64 definition by half a unit in the
+last place, 2^-9 relative, plus the fp32 accumulation of a GEMM; bound used:
+2^-7 |ref| + 1e-3.  Whole layers are compared with the oracle storing every
+intermediate in bf16 where the GPU does; a bf16 tie that the two round apart
+propagates, so the bound there is 2^-5 |ref| + 2e-2, checked at the end of
+every layer."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.baton_oracle as O
+import oracle.llama_layer as LL
+from paper_2410_18701_amd import layer as PL
+from paper_2410_18701_amd.cache import BatonCache
+from tests import parity
+from workload import driver, gen
+from workload import model as M
+from workload.configs import Workload
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits(rng, shape, scale_exp=0):
+    x = rng.standard_normal(shape).astype(np.float32) * np.float32(2.0 ** -scale_exp)
+    return LL.to_bits(x.astype(np.float64), O.BF16)
+
+
+def _dev(bits):
+    return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _val(t):
+    return O.widen(parity.host_bits(t), O.BF16)
+
+
+def _close(got, want, rel=2.0 ** -7, atol=1e-3, what=""):
+    err = np.abs(got - want) - (rel * np.abs(want) + atol)
+    assert np.all(err <= 0), f"{what}: worst excess {err.max():.3g} at {np.unravel_index(err.argmax(), err.shape)}"
+
+
+@pytest.mark.parametrize("rows,out_dim,in_dim", [(1, 64, 64), (5, 520, 136), (64, 4096, 4096), (8, 4096, 11008)])
+def test_linear(rows, out_dim, in_dim):
+    rng = np.random.default_rng(rows + out_dim)
+    k = round(np.log2(in_dim) / 2)
+    xb, wb, yb = _bits(rng, (rows, in_dim)), _bits(rng, (out_dim, in_dim), k), _bits(rng, (rows, out_dim))
+    g = PL.Gemm()
+    y = torch.empty((rows, out_dim), dtype=torch.bfloat16, device="cuda")
+    g.linear(_dev(xb), _dev(wb), y)
+    want = LL.linear(O.widen(xb, O.BF16), O.widen(wb, O.BF16))
+    _close(_val(y), want, what="linear")
+    y2 = _dev(yb)
+    g.linear(_dev(xb), _dev(wb), y2, accumulate=True)
+    _close(_val(y2), O.widen(yb, O.BF16) + want, what="linear accumulate")
+    g.close()
+
+
+def test_rmsnorm_and_silu_mul():
+    rng = np.random.default_rng(11)
+    xb, gb = _bits(rng, (7, 4096)), _bits(rng, (4096,))
+    y = torch.empty((7, 4096), dtype=torch.bfloat16, device="cuda")
+    PL.rmsnorm(_dev(xb), _dev(gb), y, 1e-5)
+    _close(_val(y), LL.rmsnorm(O.widen(xb, O.BF16), O.widen(gb, O.BF16), 1e-5), atol=1e-6, what="rmsnorm")
+    gub = _bits(rng, (7, 2 * 11008))
+    out = torch.empty((7, 11008), dtype=torch.bfloat16, device="cuda")
+    PL.silu_mul(_dev(gub), out)
+    gu = O.widen(gub, O.BF16)
+    _close(_val(out), LL.silu(gu[:, :11008]) * gu[:, 11008:], atol=1e-6, what="silu_mul")
+
+
+def test_rope_at_token_counts():
+    """Positions are the slots' token counts: holes from an in-batch prefill
+    do not count, free slots are rotated at 0."""
+    B, Hq, Hkv, D = 4, 8, 2, 128
+    cache = BatonCache(1, B, Hq, Hkv, D, capacity=256, dtype="bf16")
+    w = Workload("r", "bf16", 1, B, Hq, Hkv, D, 1, 0, seed=9)
+    dev = driver.DeviceInputs(w)
+    srcs = [dev.prefill(q, n) for q, n in zip([0, 1], [30, 5])]
+    cache.embed([0, 1], [30, 5], [s[0] for s in srcs], [s[1] for s in srcs])
+    cache.shape_insert([2], [12])
+    q, kn, vn = dev.prefill_step(0, 0, 12, [(2, 2, 12)])
+    cache.decode_attn(0, q, kn, vn)
+    cache.advance()
+    toks = cache.tokens()
+    assert toks == [31, 6, 12, 0]
+    rng = np.random.default_rng(12)
+    qkvb = _bits(rng, (B, (Hq + 2 * Hkv) * D))
+    qo = torch.empty((B, Hq, D), dtype=torch.bfloat16, device="cuda")
+    ko = torch.empty((B, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    vo = torch.empty((B, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    PL.rope_qkv(cache, _dev(qkvb), qo, ko, vo, 10000.0)
+    qr, kr, vr = LL.split_qkv(O.widen(qkvb, O.BF16), Hq, Hkv, D)
+    pos = np.array(toks, np.float64)[:, None]
+    _close(_val(qo), LL.rope(qr, pos, 1e4), atol=2e-3, what="rope q")
+    _close(_val(ko), LL.rope(kr, pos, 1e4), atol=2e-3, what="rope k")
+    assert np.array_equal(parity.host_bits(vo), LL.split_qkv(qkvb, Hq, Hkv, D)[2])
+    cache.close()
+
+
+def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128):
+    """GPU layers and the oracle in lockstep; returns the worst relative excess."""
+    w = Workload("layer", "bf16", NL, B, m.n_q_heads, m.n_kv_heads, m.head_dim, 1, 0, seed=seed)
+    dev = driver.DeviceInputs(w)
+    cache = BatonCache(NL, B, m.n_q_heads, m.n_kv_heads, m.head_dim, capacity=capacity, dtype="bf16")
+    pb = O.PaddedBatch(NL, B, m.n_q_heads, m.n_kv_heads, m.head_dim, O.BF16, fill_bits=cache.fill_bits)
+    wd = [M.weights_device(seed, m, l) for l in range(NL)]
+    wh = [M.weights_host(seed, m, l) for l in range(NL)]
+    gemm = PL.Gemm()
+    layers = PL.DecodeLayers(cache, wd, gemm, m.theta, m.eps)
+    step = 0
+    for op in steps_ops:
+        if op[0] == "embed":
+            _, slots, lens, qids = op
+            srcs = [dev.prefill(q, n) for q, n in zip(qids, lens)]
+            cache.embed(slots, lens, [s[0] for s in srcs], [s[1] for s in srcs])
+            pb.embed(slots, lens, [gen.prefill_host(seed, "k", q, NL, m.n_kv_heads, n, m.head_dim, "bf16")
+                                   for q, n in zip(qids, lens)],
+                     [gen.prefill_host(seed, "v", q, NL, m.n_kv_heads, n, m.head_dim, "bf16")
+                      for q, n in zip(qids, lens)])
+        elif op[0] == "evict":
+            cache.evict(op[1], release=True)
+            pb.evict(op[1], release=True)
+        else:
+            x = M.x_device(seed, step, B, m.hidden)
+            xh = M.bf16_value(M.x_host(seed, step, B, m.hidden))
+            assert np.array_equal(_val(x), xh)
+            pos = cache.tokens()
+            live = [b for b in range(B) if pb.lens[b] > 0]
+            for layer in range(NL):
+                layers.layer(layer, x)
+                xh = LL.decode_layer(pb, layer, xh, wh[layer], pos, m.theta, m.eps, stored=O.BF16)
+                got = _val(x)
+                _close(got[live], xh[live], rel=2.0 ** -5, atol=2e-2, what=f"step {step} layer {layer}")
+                xh = got   # both sides go on from the GPU's stream
+            cache.advance()
+            pb.advance()
+            step += 1
+    torch.cuda.synchronize()
+    L, _, lens = cache.query()
+    assert (L, lens) == (pb.L, pb.lens)
+    gemm.close()
+    cache.close()
+
+
+def test_layers_small_model():
+    m = M.ModelShape(256, 4, 2, 64, 512)
+    ops = [("embed", [0, 1, 2], [9, 30, 4], [0, 1, 2]), ("step",), ("step",),
+           ("evict", [1]), ("embed", [3, 1], [12, 40], [3, 4]), ("step",), ("evict", [0]), ("step",)]
+    _run_layers(m, 2, 4, ops)
+
+
+def test_layers_llama2_7b_shape():
+    ops = [("embed", [0, 1, 2, 3], [100, 7, 33, 64], [0, 1, 2, 3]), ("step",),
+           ("evict", [2]), ("embed", [2], [20], [4]), ("step",)]
+    _run_layers(M.LLAMA2_7B, 2, 4, ops, capacity=192)
