@@ -42,6 +42,8 @@ def parse():
     p.add_argument("--no-pd", action="store_true",
                    help="prefill the new queries inside the batch (no prefill/decode separation) "
                         "instead of embedding prefilled ones")
+    p.add_argument("--model", default=None, choices=["llama2-7b"],
+                   help="run whole decode layers of this model (synthetic weights) around the attention")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=20, help="layers of step 0 the oracle runs")
     p.add_argument("--copy-bytes", type=int, default=2 << 30,
@@ -175,6 +177,90 @@ def bench_no_pd(args, w):
     }
 
 
+def bench_model(args, w):
+    """Whole decode steps of a llama2-7b-shaped model on the workload's schedule:
+    evict, embed, mask, then per layer RMS norm, QKV projection, rotary
+    embedding, the re-batched attention, output projection, RMS norm, gated
+    feed-forward; synthetic weights resident in HBM."""
+    import torch
+
+    from paper_2410_18701_amd import layer as PL
+    from workload import driver
+    from workload import model as M
+
+    m = M.LLAMA2_7B
+    if (w.n_q_heads, w.n_kv_heads, w.head_dim) != (m.n_q_heads, m.n_kv_heads, m.head_dim):
+        raise SystemExit("--model llama2-7b needs a workload with 32 heads of 128 (cfg2, cfg3, cfg5)")
+    cache, inputs = driver.open_cache(w, split=args.split)
+    weights = [M.weights_device(w.seed, m, l) for l in range(w.n_layers)]
+    wbytes = sum(t.numel() * 2 for lw in weights for t in lw.values())
+    gemm = PL.Gemm()
+    layers = PL.DecodeLayers(cache, weights, gemm, m.theta, m.eps)
+    total_steps = args.warmup + args.steps
+    xs = [M.x_device(w.seed, s, w.batch, m.hidden) for s in range(total_steps)]
+
+    def step(s, pre=None, ev_attn=None, ev_layer=None, E=None):
+        ev = w.steps[s]
+        cache.evict(ev.evict, release=True)
+        if ev.insert:
+            srcs = pre if pre is not None else [inputs.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+            cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+        cache.build_mask(out=mask_buf)
+        n_live = sum(1 for n in cache.query()[2] if n > 0)
+        x = xs[s]
+        for layer in range(w.n_layers):
+            if E is not None:
+                a = E()
+                a.record()
+            layers.layer(layer, x)
+            if E is not None:
+                b = E()
+                b.record()
+                ev_layer.append((a, b))
+        cache.advance()
+        return n_live
+
+    mask_buf = torch.empty((w.batch, cache.capacity + 1), dtype=torch.uint8, device="cuda")
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    pre = [[inputs.prefill(q, n) for q, n in zip(w.steps[s].insert_qids, w.steps[s].insert_lens)]
+           for s in range(args.warmup, total_steps)]
+    pool = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps * w.n_layers + 2)]
+    for e in pool:
+        e.record()
+    torch.cuda.synchronize()
+    it = iter(pool)
+    E = lambda: next(it)
+    ev_layer, live_tokens = [], 0
+    gc.collect()
+    gc.disable()
+    t0, t1 = E(), E()
+    t0.record()
+    for i, s in enumerate(range(args.warmup, total_steps)):
+        live_tokens += step(s, pre[i], None, ev_layer, E)
+    t1.record()
+    torch.cuda.synchronize()
+    gc.enable()
+    total_ms = t0.elapsed_time(t1)
+    layer_ms = sum(a.elapsed_time(b) for a, b in ev_layer)
+    per_layer_w = wbytes / w.n_layers
+    gemm.close()
+    return {
+        "metric": "decode tokens/s of whole llama2-7b-shaped decode steps (synthetic weights)",
+        "value": round(live_tokens / (total_ms * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded generator weights and activations)",
+        "config": {"workload": f"{w.name} schedule with llama2-7b layers: {w.n_layers} layers, hidden "
+                               f"{m.hidden}, ffn {m.ffn}, batch {w.batch}, initial padded length {w.L0}",
+                   "global_batch": w.batch, "seq_len": w.L0, "parallelism": "none (1 GPU)"},
+        "ops": {"layer": {"ms_per_call": round(layer_ms / len(ev_layer), 4),
+                          "weight_bytes_per_layer": int(per_layer_w)},
+                "weights_GB": round(wbytes / 1e9, 2)},
+    }
+
+
 def cpu_baseline(w, n_layers):
     """The oracle, timed on this host over step 0 of the workload for n_layers
     layers (one layer of the batch at a time), scaled to query-tokens/s of the
@@ -277,6 +363,9 @@ def main():
             raise SystemExit("--layers applies to cfg4 only")
     if args.no_pd:
         print(json.dumps(bench_no_pd(args, w)), flush=True)
+        return
+    if args.model:
+        print(json.dumps(bench_model(args, w)), flush=True)
         return
     copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
     cache, inputs = driver.open_cache(w, split=args.split)

@@ -315,6 +315,7 @@ baton_status baton_gemm_destroy(baton_gemm* gemm);
  * [out_dim][in_dim] (a linear layer's stored weight), y device [rows][out_dim];
  * accumulate = 1 adds to y (the residual stream), 0 overwrites it.  fp32
  * accumulation.  ws: device workspace the GEMM may use (ws_bytes, may be 0).
+ * The algorithm is hipBLASLt's first choice for the shape, kept per handle.
  * Errors: EINVAL (null or misaligned pointer, sizes < 1 or not multiples of 8,
  * accumulate not 0/1), EDTYPE (dtype not bf16), EHIP (no algorithm fits).
  */
@@ -337,7 +338,7 @@ baton_status baton_rmsnorm(int32_t dtype, const void* x, const void* gain, void*
  * rotating q and k: pair (i, i + head_dim/2) of a head by angle
  * pos_b * theta^(-2i/head_dim), pos_b = slot b's token count
  * (baton_cache_tokens), the position of the token being decoded.  The angles
- * are taken in double precision.  Decode steps only.
+ * are formed and reduced modulo 2 pi in double precision.  Decode steps only.
  * Errors: EINVAL (null pointer, theta <= 1), EDTYPE (cache not bf16), ESTATE
  * (a prefill is registered), EHIP.
  */

@@ -733,7 +733,8 @@ baton_status baton_rope_qkv(const baton_cache* c, const void* qkv, void* q, void
   a.log2_theta = std::log2((double)theta);
   const baton::HoleList hl = hole_list(c);
   for (int32_t b = 0; b < c->d.batch; ++b) a.pos[b] = row_tokens(c, b, hl);
-  hipLaunchKernelGGL(baton::rope_qkv_kernel, dim3(c->d.batch), dim3(baton::kRowThreads), 0, stream, a);
+  const int heads = c->d.n_q_heads + 2 * c->d.n_kv_heads;
+  hipLaunchKernelGGL(baton::rope_qkv_kernel, dim3(c->d.batch * heads), dim3(baton::kWave), 0, stream, a);
   return hip_status(hipGetLastError());
 }
 

@@ -14,7 +14,7 @@
 
 struct baton_gemm {
   hipblasLtHandle_t lt = nullptr;
-  // Heuristic choice per (rows, out_dim, in_dim, accumulate, workspace bytes).
+  // Algorithm choice per (rows, out_dim, in_dim, 0, workspace bytes).
   std::map<std::tuple<int32_t, int32_t, int32_t, int32_t, size_t>, hipblasLtMatmulAlgo_t> algos;
 };
 
@@ -80,9 +80,12 @@ baton_status baton_linear(baton_gemm* g, int32_t dtype, const void* x, const voi
   if (!aligned16(x) || !aligned16(w) || !aligned16(y) || in_dim % 8 || out_dim % 8) return BATON_EINVAL;
   LtDescs d;
   if (!make_descs(d, rows, out_dim, in_dim)) return BATON_EHIP;
-  const auto key = std::make_tuple(rows, out_dim, in_dim, accumulate, ws_bytes);
+  const auto key = std::make_tuple(rows, out_dim, in_dim, 0, ws_bytes);
   auto it = g->algos.find(key);
   if (it == g->algos.end()) {
+    // hipBLASLt's first choice.  (Timing its candidates back to back was
+    // measured and misleads: the repeated weight matrix stays in the caches,
+    // while a decode step reads each weight once from HBM.)
     hipblasLtMatmulPreference_t pref;
     if (hipblasLtMatmulPreferenceCreate(&pref) != HIPBLAS_STATUS_SUCCESS) return BATON_EHIP;
     const uint64_t max_ws = ws_bytes;

@@ -52,9 +52,10 @@ __global__ void __launch_bounds__(kRowThreads) rmsnorm_kernel(const u32x4* __res
 }
 
 // Split of the fused projection qkv [B][(Hq + 2 Hkv) D] into q [B][Hq][D],
-// k [B][Hkv][D] (both rotated) and v [B][Hkv][D].  Rotation of pair
-// (i, i + D/2) by pos_b * theta^(-2i/D); the angles and their sines and
-// cosines are taken in double precision, once per row, in LDS.
+// k [B][Hkv][D] (both rotated) and v [B][Hkv][D].  One wave per (row, head):
+// lane i < D/2 rotates pair (i, i + D/2) by pos_b * theta^(-2i/D).  The angle
+// is formed and reduced modulo 2 pi in double precision, its sine and cosine
+// then taken in single precision on [-pi, pi].
 struct RopeArgs {
   const uint16_t* qkv;
   uint16_t* q;
@@ -65,37 +66,29 @@ struct RopeArgs {
   int32_t pos[512];
 };
 
-__global__ void __launch_bounds__(kRowThreads) rope_qkv_kernel(const RopeArgs a) {
-  __shared__ float cs[2][128];   // cos, sin of the row's D/2 <= 128 pairs
-  const int b = blockIdx.x;
-  const int D = a.head_dim, half = D / 2;
-  if (threadIdx.x < half) {
-    const double inv = exp2(-(double)(2 * threadIdx.x) / D * a.log2_theta);
-    double s, c;
-    sincos((double)a.pos[b] * inv, &s, &c);
-    cs[0][threadIdx.x] = (float)c;
-    cs[1][threadIdx.x] = (float)s;
+__global__ void __launch_bounds__(kWave) rope_qkv_kernel(const RopeArgs a) {
+  const int hq = a.n_q_heads, hkv = a.n_kv_heads, D = a.head_dim, half = D / 2;
+  const int heads = hq + 2 * hkv;
+  const int b = blockIdx.x / heads, head = blockIdx.x - b * heads;
+  const uint16_t* src = a.qkv + ((int64_t)b * heads + head) * D;
+  const int i = threadIdx.x;
+  if (head >= hq + hkv) {                      // a value head: copied
+    uint16_t* dst = a.v + ((int64_t)b * hkv + (head - hq - hkv)) * D;
+    for (int e = i; e < D; e += kWave) dst[e] = src[e];
+    return;
   }
-  __syncthreads();
-  const int hq = a.n_q_heads, hkv = a.n_kv_heads;
-  const int64_t width = (int64_t)(hq + 2 * hkv) * D;
-  const uint16_t* src = a.qkv + b * width;
-  // rotated heads: q then k, pairs (i, i + half)
-  const int rot = (hq + hkv) * half;
-  for (int e = threadIdx.x; e < rot; e += kRowThreads) {
-    const int head = e / half, i = e - head * half;
-    const float x0 = __uint_as_float((uint32_t)src[head * D + i] << 16);
-    const float x1 = __uint_as_float((uint32_t)src[head * D + i + half] << 16);
-    const float c = cs[0][i], s = cs[1][i];
-    const float y0 = x0 * c - x1 * s, y1 = x0 * s + x1 * c;
-    uint16_t* dst = head < hq ? a.q + ((int64_t)b * hq + head) * D
-                              : a.k + ((int64_t)b * hkv + (head - hq)) * D;
-    dst[i] = (uint16_t)f32_to_bf16_rne(y0);
-    dst[i + half] = (uint16_t)f32_to_bf16_rne(y1);
-  }
-  // values copied
-  for (int e = threadIdx.x; e < hkv * D; e += kRowThreads)
-    a.v[(int64_t)b * hkv * D + e] = src[(hq + hkv) * D + e];
+  if (i >= half) return;
+  const double inv = exp2(-(double)(2 * i) / D * a.log2_theta);
+  const double two_pi = 6.283185307179586;
+  double ang = (double)a.pos[b] * inv;
+  ang -= two_pi * rint(ang / two_pi);
+  float s, c;
+  sincosf((float)ang, &s, &c);
+  const float x0 = __uint_as_float((uint32_t)src[i] << 16);
+  const float x1 = __uint_as_float((uint32_t)src[i + half] << 16);
+  uint16_t* dst = head < hq ? a.q + ((int64_t)b * hq + head) * D : a.k + ((int64_t)b * hkv + (head - hq)) * D;
+  dst[i] = (uint16_t)f32_to_bf16_rne(x0 * c - x1 * s);
+  dst[i + half] = (uint16_t)f32_to_bf16_rne(x0 * s + x1 * c);
 }
 
 // out[r][j] = silu(gate_up[r][j]) * gate_up[r][F + j], 8 elements per thread.
