@@ -254,6 +254,29 @@ class PaddedBatch:
             out.append((self.K[:, s][:, :, keep].copy(), self.V[:, s][:, :, keep].copy()))
         return out
 
+    def move(self, src, dst):
+        """Live queries change slots: query src[i] moves, cache and mask row bit
+        for bit, into the free slot dst[i], which leaves src[i] free -- moving
+        queries within the batch (sec. 4.3), e.g. to gather the live rows at
+        the front of the batch dimension.  L does not change."""
+        self._check_between_steps()
+        if len(src) != len(dst) or len(set(src) | set(dst)) != 2 * len(src) or \
+                any(not 0 <= s < self.B for s in list(src) + list(dst)):
+            raise ValueError("bad slot lists")
+        if any(self.lens[s] == 0 for s in src) or any(self.lens[d] != 0 for d in dst):
+            raise LookupError("moving a free slot or into a live one")
+        for s, d in zip(src, dst):
+            if self.materialize:
+                self.K[:, d] = self.K[:, s]
+                self.V[:, d] = self.V[:, s]
+                self.K[:, s] = self.fill
+                self.V[:, s] = self.fill
+            self.M[d] = self.M[s]
+            self.M[s] = 0
+            self.lens[d], self.lens[s] = self.lens[s], 0
+            self.hist_k[d], self.hist_v[d] = self.hist_k[s], self.hist_v[s]
+            self.hist_k[s] = self.hist_v[s] = None
+
     def shape_insert(self, slots, lens):
         """Register new queries to be prefilled inside the batch in the next step
         (no prefill/decode separation, sec. 4.1): slots must be free, lens are

@@ -605,3 +605,40 @@ def pin_inbatch_prefill_isolation(O):
 
 
 ALL_PINS += [pin_inbatch_prefill_replay, pin_inbatch_prefill_sdpa, pin_inbatch_prefill_isolation]
+
+
+def pin_move_is_a_permutation(O):
+    """Moving queries between slots (sec. 4.3) permutes the batch and nothing
+    else: after a move the batch equals the batch that had the queries in the
+    new slots from the start -- rows, mask, lengths, and every later output."""
+    rng = np.random.default_rng(51)
+    NL, B, Hq, Hkv, D = 2, 5, 4, 2, 8
+
+    def bits(shape):
+        return rng.standard_normal(shape).astype(np.float32).view(np.uint32)
+
+    lens = [6, 3, 9]
+    ks = [bits((NL, Hkv, n, D)) for n in lens]
+    vs = [bits((NL, Hkv, n, D)) for n in lens]
+    a = O.PaddedBatch(NL, B, Hq, Hkv, D, O.F32)
+    a.embed([1, 3, 4], lens, ks, vs)
+    a.move([3, 4], [0, 2])                       # compact: live rows 0, 1, 2
+    b = O.PaddedBatch(NL, B, Hq, Hkv, D, O.F32)
+    b.embed([1, 0, 2], lens, ks, vs)
+    assert a.L == b.L and a.lens == b.lens
+    assert np.array_equal(a.K, b.K) and np.array_equal(a.V, b.V) and np.array_equal(a.mask(), b.mask())
+    for _ in range(2):
+        for layer in range(NL):
+            q, kn, vn = bits((B, Hq, D)), bits((B, Hkv, D)), bits((B, Hkv, D))
+            assert np.array_equal(a.decode_layer(layer, q, kn, vn), b.decode_layer(layer, q, kn, vn))
+        a.advance()
+        b.advance()
+    try:
+        a.move([0], [1])
+    except LookupError:
+        pass
+    else:
+        raise AssertionError("moved into a live slot")
+
+
+ALL_PINS.append(pin_move_is_a_permutation)
