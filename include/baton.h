@@ -173,6 +173,21 @@ baton_status baton_kv_extract(const baton_cache* cache, const int32_t* slots, in
                               void* const* k_dst, void* const* v_dst, hipStream_t stream);
 
 /*
+ * Live queries change slots (sec. 4.3 moves queries within and out of the
+ * batch; moving the live ones to the front compacts the batch dimension):
+ * src, dst host arrays of n pairs, src[i] live, dst[i] free, no slot listed
+ * twice.  Query src[i]'s row -- its tokens, holes and mask -- moves bit for bit
+ * into slot dst[i] (same columns), and src[i] becomes free, its tokens owed
+ * placeholders as after an eviction.  L and base do not change.  One launch
+ * (plus one for placeholders the targets still owed).
+ * Errors: EINVAL (n < 0, null arrays, slot out of range or listed twice),
+ * ESLOT (a source free or a target live), ESTATE (inside a decode step, or a
+ * prefill registered), EHIP.
+ */
+baton_status baton_kv_move(baton_cache* cache, const int32_t* src, const int32_t* dst, int32_t n,
+                           hipStream_t stream);
+
+/*
  * Prefill new queries inside the batch in the next step (sec. 4.1, without
  * prefill/decode separation).  slots, lens: host arrays of n >= 1 entries:
  * distinct free slots and their prompt lengths.  The next step's input has

@@ -58,6 +58,7 @@ def lib():
         L.baton_kv_embed.argtypes = [vp, P(i32), i32, P(i32), P(vp), P(vp), vp]
         L.baton_kv_extract.argtypes = [vp, P(i32), i32, P(vp), P(vp), vp]
         L.baton_shape_insert.argtypes = [vp, P(i32), i32, P(i32)]
+        L.baton_kv_move.argtypes = [vp, P(i32), P(i32), i32, vp]
         L.baton_cache_tokens.argtypes = [vp, P(i32)]
         L.baton_build_mask.argtypes = [vp, vp, i64, vp]
         L.baton_decode_attn_workspace_bytes.argtypes = [vp]
@@ -79,7 +80,7 @@ def lib():
                      "baton_kv_extract",
                      "baton_build_mask", "baton_decode_attn", "baton_step_advance",
                      "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
-                     "baton_shape_insert", "baton_cache_tokens", "baton_gemm_create",
+                     "baton_shape_insert", "baton_cache_tokens", "baton_kv_move", "baton_gemm_create",
                      "baton_gemm_destroy", "baton_linear", "baton_rmsnorm", "baton_rope_qkv",
                      "baton_silu_mul"):
             getattr(L, name).restype = st
@@ -151,6 +152,14 @@ def baton_kv_extract(cache, slots, k_dst, v_dst, stream=None):
     ks = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in k_dst])
     vs = (ctypes.c_void_p * max(1, n))(*[_ptr(x) for x in v_dst])
     _check(lib().baton_kv_extract(cache, s_arr, n, ks, vs, _stream(stream)), "baton_kv_extract")
+
+
+def baton_kv_move(cache, src, dst, stream=None):
+    s_arr, n = _i32s(src)
+    d_arr, nd = _i32s(dst)
+    if nd != n:
+        raise ValueError("src and dst must have the same length")
+    _check(lib().baton_kv_move(cache, s_arr, d_arr, n, _stream(stream)), "baton_kv_move")
 
 
 def baton_shape_insert(cache, slots, lens):

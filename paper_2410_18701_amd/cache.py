@@ -65,6 +65,10 @@ class BatonCache:
         B.baton_kv_embed(self.handle, slots, lens, k_src, v_src,
                          stream if stream is not None else _cur_stream())
 
+    def move(self, src, dst, stream=None):
+        """Live queries src[i] move to free slots dst[i] (cache and mask rows)."""
+        B.baton_kv_move(self.handle, src, dst, stream if stream is not None else _cur_stream())
+
     def shape_insert(self, slots, lens):
         """Prefill these queries inside the batch in the next step (no prefill/decode
         separation); that step's inputs and outputs have a position axis of

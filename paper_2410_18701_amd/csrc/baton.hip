@@ -168,10 +168,11 @@ struct Seg {
   const void* vs;
   int32_t ext_len = 0;   // tokens per (layer, head) of the contiguous side; 0: len
   int32_t ext_t0 = 0;    // the segment's first token there
+  int32_t dst_slot = -1; // a move: the slot receiving the columns
 };
 
 template <int VPT>
-baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs, bool extract,
+baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs, int mode,
                              hipStream_t s) {
   constexpr int TT = baton::kCopyThreads * baton::kCopyVecs / VPT;
   for (size_t off = 0; off < segs.size(); off += baton::kMaxSegs) {
@@ -184,7 +185,7 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
     a.batch = c->d.batch;
     a.n_kv_heads = c->d.n_kv_heads;
     a.fill_word = fill_word(c);
-    a.extract = extract ? 1 : 0;
+    a.extract = mode;
     const size_t n = std::min<size_t>(baton::kMaxSegs, segs.size() - off);
     int64_t tiles = 0;
     int32_t used = 0;
@@ -196,6 +197,7 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
       a.len[used] = g.len;
       a.col0[used] = g.col0;
       a.tiles_per_row[used] = tpr;
+      a.dst_slot[used] = g.dst_slot;
       a.ext_len[used] = g.ext_len > 0 ? g.ext_len : g.len;
       a.ext_t0[used] = g.ext_t0;
       a.kext[used] = static_cast<uint32_t*>(const_cast<void*>(g.ks));
@@ -215,12 +217,13 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
   return BATON_OK;
 }
 
+// mode: 0 copy into the ring (or placeholders), 1 copy out of it, 2 row to row.
 baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hipStream_t s,
-                         bool extract = false) {
+                         int mode = 0) {
   switch (c->vpt) {
-    case 8: return launch_segs_vpt<8>(c, segs, extract, s);
-    case 16: return launch_segs_vpt<16>(c, segs, extract, s);
-    case 32: return launch_segs_vpt<32>(c, segs, extract, s);
+    case 8: return launch_segs_vpt<8>(c, segs, mode, s);
+    case 16: return launch_segs_vpt<16>(c, segs, mode, s);
+    case 32: return launch_segs_vpt<32>(c, segs, mode, s);
     default: return BATON_EDTYPE;
   }
 }
@@ -507,7 +510,48 @@ baton_status baton_kv_extract(const baton_cache* c, const int32_t* slots, int32_
       done += t1 - t0;
     });
   }
-  return launch_segs(c, segs, stream, /*extract=*/true);
+  return launch_segs(c, segs, stream, /*mode=*/1);
+}
+
+baton_status baton_kv_move(baton_cache* c, const int32_t* src, const int32_t* dst, int32_t n,
+                           hipStream_t stream) {
+  if (!c || n < 0 || (n > 0 && (!src || !dst))) return BATON_EINVAL;
+  if (c->n_done || c->n_prefill) return BATON_ESTATE;
+  std::vector<uint8_t> seen(c->d.batch, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    for (const int32_t s : {src[i], dst[i]}) {
+      if (s < 0 || s >= c->d.batch || seen[s]) return BATON_EINVAL;
+      seen[s] = 1;
+    }
+  }
+  for (int32_t i = 0; i < n; ++i)
+    if (c->lens[src[i]] == 0 || c->lens[dst[i]] != 0) return BATON_ESLOT;
+  // The moved span ends at base + L in both rows; the columns of the target's
+  // earlier query in front of it, still owed placeholders, are written in the
+  // same launch.
+  const int64_t end = ring(c->base + c->L, c->d.capacity);
+  std::vector<Seg> copies, fills;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t len = c->lens[src[i]];
+    Seg g{src[i], len, ring(end - len, c->d.capacity), nullptr, nullptr};
+    g.dst_slot = dst[i];
+    copies.push_back(g);
+    const int32_t owed = c->pending[dst[i]];
+    if (owed > len) fills.push_back({dst[i], owed - len, ring(end - owed, c->d.capacity), nullptr, nullptr});
+  }
+  baton_status st = launch_segs(c, copies, stream, /*mode=*/2);
+  if (st == BATON_OK && !fills.empty()) st = launch_segs(c, fills, stream);
+  if (st != BATON_OK) return st;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t s = src[i], d = dst[i];
+    c->lens[d] = c->lens[s];
+    c->epoch[d] = c->epoch[s];
+    c->pending[d] = 0;
+    c->pending[s] = c->lens[s];   // the source's tokens are owed placeholders now
+    c->lens[s] = 0;
+  }
+  c->meta_valid = false;
+  return BATON_OK;
 }
 
 baton_status baton_shape_insert(baton_cache* c, const int32_t* slots, int32_t n, const int32_t* lens) {

@@ -25,13 +25,14 @@ struct SegArgs {
   int64_t cap;              // ring columns
   int32_t n_layers, batch, n_kv_heads;
   int32_t n_segs;
-  int32_t extract;          // 1: ring -> ext, 0: ext (or placeholder) -> ring
+  int32_t extract;          // 1: ring -> ext, 0: ext (or placeholder) -> ring, 2: ring row -> ring row
   uint32_t fill_word;       // placeholder bits replicated to a 32-bit word
   int32_t slot[kMaxSegs];
   int32_t len[kMaxSegs];
   int32_t tiles_per_row[kMaxSegs];
   int64_t col0[kMaxSegs];
   int64_t tile_end[kMaxSegs];           // inclusive prefix of tiles over segments
+  int32_t dst_slot[kMaxSegs];           // mode 2: the slot whose row receives the columns
   int32_t ext_len[kMaxSegs];            // tokens per (layer, head) of the contiguous side
   int32_t ext_t0[kMaxSegs];             // its first token of this segment
   uint32_t* kext[kMaxSegs];             // contiguous side; null: placeholders
@@ -66,6 +67,27 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
 
   u32x4 val[kCopyVecs];
   const u32x4 fill = {a.fill_word, a.fill_word, a.fill_word, a.fill_word};
+  if (a.extract == 2) {     // the same ring columns of another slot's row
+    u32x4* dst = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
+                 (((int64_t)layer * a.batch + a.dst_slot[i]) * a.n_kv_heads + h) * a.cap * VPT;
+#pragma unroll
+    for (int r = 0; r < kCopyVecs; ++r) {
+      const int idx = threadIdx.x + r * kCopyThreads;
+      if (idx < nt * VPT) {
+        const int t = idx / VPT, e = idx - (idx / VPT) * VPT;
+        val[r] = __builtin_nontemporal_load(ring + ring_add(c0, t, a.cap) * VPT + e);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kCopyVecs; ++r) {
+      const int idx = threadIdx.x + r * kCopyThreads;
+      if (idx < nt * VPT) {
+        const int t = idx / VPT, e = idx - (idx / VPT) * VPT;
+        __builtin_nontemporal_store(val[r], dst + ring_add(c0, t, a.cap) * VPT + e);
+      }
+    }
+    return;
+  }
   if (a.extract) {
 #pragma unroll
     for (int r = 0; r < kCopyVecs; ++r) {

@@ -356,6 +356,7 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
       ("extract", slots, tag)        store the slots' K/V aside (GPU and oracle)
       ("embed_saved", slots, tag)    re-insert stored queries into these slots
       ("shape", slots, lens, qids)   prefill new queries inside the batch in the next step
+      ("move", src, dst)             live queries change slots
       ("step", s)                    mask, every layer with step-s inputs, advance
       ("flush",)                     the placeholder writes evictions still owe
     After a step or a flush the whole ring is compared; after the other
@@ -398,6 +399,9 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
             cache.embed(slots, [k.shape[2] for k in ks], ks, vs)
             pb.embed(slots, [k.shape[2] for k, _ in saved_cpu[tag]], [k for k, _ in saved_cpu[tag]],
                      [v for _, v in saved_cpu[tag]])
+        elif kind == "move":
+            cache.move(op[1], op[2])
+            pb.move(op[1], op[2])
         elif kind == "shape":
             _, slots, lens, qids = op
             cache.shape_insert(slots, lens)
@@ -438,7 +442,7 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
         else:
             raise ValueError(kind)
         torch.cuda.synchronize()
-        check_ring(cache, pb, str(op), live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape"))
+        check_ring(cache, pb, str(op), live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape", "move"))
         want_tok = [pb.hist_k[b].shape[2] if pb.lens[b] > 0 else 0 for b in range(B)]
         assert cache.tokens() == want_tok, (op, cache.tokens(), want_tok)
     cache.close()

@@ -90,6 +90,10 @@ def test_host_checks_leave_state_unchanged():
         assert status(B.baton_build_mask, h, FAKE_K, 0) == B.BATON_EINVAL   # ld < L + 1
         assert status(B.baton_set_split_tokens, h, 100) == B.BATON_EINVAL
         assert B.baton_cache_query(h, 4) == (0, 0, [0, 0, 0, 0])
+        assert status(B.baton_kv_move, h, [1], [2]) == B.BATON_ESLOT              # source free
+        assert status(B.baton_kv_move, h, [1], [1]) == B.BATON_EINVAL             # listed twice
+        assert status(B.baton_kv_move, h, [0], [7]) == B.BATON_EINVAL             # out of range
+        B.baton_kv_move(h, [], [])                                                 # nothing to do
         # in-batch prefill registration (host metadata only)
         assert status(B.baton_shape_insert, h, [], []) == B.BATON_EINVAL          # nothing to insert
         assert status(B.baton_shape_insert, h, [1, 1], [3, 3]) == B.BATON_EINVAL  # duplicate

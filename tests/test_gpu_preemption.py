@@ -124,3 +124,23 @@ def test_direct_host_offload():
     assert np.array_equal(parity.host_bits(direct.v), parity.host_bits(staged.v))
     for c in caches:
         c.close()
+
+
+@pytest.mark.parametrize("shape", [("bf16", 2, 6, 8, 2, 128), ("f32", 1, 6, 4, 4, 64)],
+                         ids=lambda s: f"{s[0]}-{s[1]}x{s[2]}-{s[3]}/{s[4]}x{s[5]}")
+def test_move_and_compact(shape):
+    """Queries moved between slots -- compaction of the live rows to the front,
+    a move into a slot that still owes placeholders, a row with holes -- in
+    lockstep with the oracle; later outputs as if they had always been there."""
+    ops = [
+        ("embed", [1, 3, 5], [30, 70, 12], [0, 1, 2]), ("step", 0),
+        ("move", [3, 5], [0, 2]),                 # compact: live rows 0, 1, 2
+        ("step", 1),
+        ("evict", [1]), ("move", [2], [1]),       # the target owes the evicted query's tokens
+        ("step", 2),
+        ("shape", [2], [9], [3]), ("step", 3),    # a prefill step leaves holes in rows 0 and 1
+        ("move", [0, 1], [4, 5]),                 # holey rows move
+        ("step", 4), ("flush",), ("step", 5),
+    ]
+    err = parity.run_script(shape, ops, capacity=256, split=64)
+    print(f"[move] {shape}: max abs error {err:.3g}", flush=True)
