@@ -301,9 +301,10 @@ baton_status baton_cache_query(const baton_cache* cache, int64_t* L, int64_t* ba
 baton_status baton_cache_tokens(const baton_cache* cache, int32_t* tokens);
 
 /*
- * Tuning: tokens per split of a row in baton_decode_attn (a multiple of 64,
- * 64 .. 4096), or 0 (the default) to let each step choose from its total
- * number of cached tokens (256 .. 1024).  Changes
+ * Tuning: tokens per split of a row in baton_decode_attn, i.e. per work item
+ * (one workgroup; a multiple of 64, 64 .. 4096), or 0 (the default) to let
+ * each step choose from its total number of cached tokens (256 .. 4096, about
+ * 4096 items per layer).  Changes
  * baton_decode_attn_workspace_bytes; only between steps.
  * Errors: EINVAL (out of range), ESTATE (inside a decode step).
  */

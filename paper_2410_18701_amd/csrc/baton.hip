@@ -133,15 +133,23 @@ void drop_holes(baton_cache* c) {
   c->holes.erase(c->holes.begin(), c->holes.begin() + k);
 }
 
-// Automatic split: enough items to fill the GPU about twice over at the
-// occupancy of these kernels, never smaller than 256 tokens (per-item set-up
-// and partial records) nor larger than 1024 (the merge and the tail).
-constexpr int64_t kAutoSplitMin = 256, kAutoSplitMax = 1024, kAutoItems = 8192;
+// Automatic split: about kAutoItems work items (workgroups of
+// BATON_ATTN_WAVES waves) over the step's live tokens, which fills the GPU
+// several times over at the occupancy of these kernels, never fewer than 256
+// tokens per item (per-item set-up) nor more than 4096 (the tail).
+#ifndef BATON_AUTO_ITEMS
+#define BATON_AUTO_ITEMS 4096
+#endif
+#ifndef BATON_AUTO_SPLIT_MIN
+#define BATON_AUTO_SPLIT_MIN 256
+#endif
+constexpr int64_t kAutoSplitMin = BATON_AUTO_SPLIT_MIN, kAutoSplitMax = 4096, kAutoItems = BATON_AUTO_ITEMS;
 
 // Workspace layout: [items: max_items] [rows with several items: batch]
+// [dispatch order: max_items int32]
 // [partials: n_kv_heads][max_items][group][head_dim + 4] fp32.
 struct WsLayout {
-  size_t items_off, multi_off, partial_off, total;
+  size_t items_off, multi_off, order_off, partial_off, total;
   int64_t max_items;
 };
 
@@ -154,7 +162,8 @@ WsLayout ws_layout(const baton_cache* c) {
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   w.items_off = 0;
   w.multi_off = up(w.items_off + sizeof(baton::Item) * w.max_items);
-  w.partial_off = up(w.multi_off + sizeof(int4) * B);
+  w.order_off = up(w.multi_off + sizeof(int4) * B);
+  w.partial_off = up(w.order_off + sizeof(int32_t) * w.max_items);
   w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * w.max_items * c->group *
                                    (c->d.head_dim + 4));
   return w;
@@ -236,15 +245,19 @@ baton_status launch_segs(const baton_cache* c, const std::vector<Seg>& segs, hip
 #define BATON_ATTN_U_LARGE_G 4   // G = 4, 8
 #endif
 
+#ifndef BATON_ATTN_WAVES
+#define BATON_ATTN_WAVES 2       // waves per attention workgroup (one work item)
+#endif
+
 template <typename T, int D, int G>
 void launch_attn_t(const baton::AttnArgs& a, int n_items, int n_multi, int hkv, hipStream_t s) {
   constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
+  constexpr int NW = BATON_ATTN_WAVES;
+  const dim3 grid(n_items * hkv);
   if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= BATON_MFMA_MIN_GROUP)
-    hipLaunchKernelGGL((baton::attn_mfma_kernel<D, G>), dim3(n_items, hkv), dim3(baton::kWave), 0,
-                       s, a);
+    hipLaunchKernelGGL((baton::attn_mfma_kernel<D, G, NW>), grid, dim3(baton::kWave * NW), 0, s, a);
   else
-    hipLaunchKernelGGL((baton::attn_kernel<T, D, G, U>), dim3(n_items, hkv), dim3(baton::kWave), 0,
-                       s, a);
+    hipLaunchKernelGGL((baton::attn_kernel<T, D, G, U, NW>), grid, dim3(baton::kWave * NW), 0, s, a);
   if (n_multi > 0)
     hipLaunchKernelGGL((baton::combine_kernel<T, D, G>), dim3(n_multi, hkv * G), dim3(baton::kWave),
                        0, s, a);
@@ -641,7 +654,8 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     if (items > w.max_items) return BATON_EINVAL;   // cannot happen: the layout bounds every row
     hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, m,
                        reinterpret_cast<baton::Item*>(wsb + w.items_off),
-                       reinterpret_cast<int4*>(wsb + w.multi_off));
+                       reinterpret_cast<int4*>(wsb + w.multi_off),
+                       reinterpret_cast<int32_t*>(wsb + w.order_off));
     const baton_status st = hip_status(hipGetLastError());
     if (st != BATON_OK) return st;
     c->n_items = (int32_t)items;
@@ -660,6 +674,7 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.out = static_cast<uint32_t*>(out);
   a.items = reinterpret_cast<const baton::Item*>(wsb + w.items_off);
   a.multi = reinterpret_cast<const int4*>(wsb + w.multi_off);
+  a.order = reinterpret_cast<const int32_t*>(wsb + w.order_off);
   a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
   a.cap = c->d.capacity;
   a.base = c->base;

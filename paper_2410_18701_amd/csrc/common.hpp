@@ -78,6 +78,11 @@ struct Lane16<BF16Tag> {
   }
 };
 
+// Base-2 exponential by the hardware instruction alone (no range fix-up):
+// results below 2^-126 flush to zero, which leaves a softmax sum -- whose
+// largest term is 1 -- unchanged in fp32; exp2(-inf) = 0.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // Cross-lane moves inside a row of 16 lanes (DPP), for reductions over the
 // lanes that share one token row.
 template <int CTRL>

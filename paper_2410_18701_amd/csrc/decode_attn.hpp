@@ -4,19 +4,22 @@
 // Work item = (slot b, split c) x kv-head h: a range of at most S tokens t of
 // row (layer, b, h) inside one run of consecutive tokens, where token t <
 // len_b is cache column L - len_b + t and token len_b is the current token
-// (k_new/v_new, appended to the cache by the item that holds it).  Placeholder
-// columns, holes included, are never addressed.  One wave per item: a token row of D elements is spread
-// over LPT = D*elem/16 lanes (16 bytes each), so one wave instruction reads
-// TPI = 64/LPT whole token rows; each of those TPI lane groups keeps its own
-// online-softmax state (max m, sum l, weighted values acc) over the tokens it
-// reads, and the groups merge once at the end of the item.  An item that is
-// its row's only one writes the output; otherwise it writes an (m, l, acc)
-// partial and combine_kernel merges the row's partials with the log-sum-exp
-// rescale.  (Merging in the attention kernel by the last item to arrive would
-// need an agent-scope release per item, which on gfx950 writes back the L2;
-// measured, that costs far more than the second launch.)  A free slot gets one
-// item that writes zeros.  Exponentials are base 2 with scale*log2(e) folded
-// into q.
+// (k_new/v_new, appended to the cache by the wave that holds it).  Placeholder
+// columns, holes included, are never addressed.  One workgroup of NW waves per
+// item; wave w streams the w-th of NW equal contiguous shares of the item's
+// tokens.  In a wave a token row of D elements is spread over LPT =
+// D*elem/16 lanes (16 bytes each), so one wave instruction reads TPI = 64/LPT
+// whole token rows; each of those TPI lane groups keeps its own online-softmax
+// state (max m, sum l, weighted values acc) over the tokens it reads.  The
+// lane groups merge by cross-lane moves, the waves through LDS.  An item that
+// is its row's only one writes the output; otherwise it writes one (m, l, acc)
+// partial record and combine_kernel merges the row's partials with the
+// log-sum-exp rescale.  Rows up to S tokens (most rows at the usual S of a
+// thousand tokens and more) thus need no partial record at all.  (Merging in
+// the attention kernel by the last item to arrive would need an agent-scope
+// release per item, which on gfx950 writes back the L2; measured, that costs
+// far more than the second launch.)  A free slot gets one item that writes
+// zeros.  Exponentials are base 2 with scale*log2(e) folded into q.
 #pragma once
 
 #include "common.hpp"
@@ -57,16 +60,30 @@ __host__ __device__ __forceinline__ int32_t row_items(const MetaArgs& a, int b) 
   return cnt;
 }
 
+// Size classes of the dispatch order: an item of t tokens (split S) is in
+// class t * kSizeClasses / (S + 1); the order runs from the largest class down.
+constexpr int kSizeClasses = 64;
+
+__device__ __forceinline__ int32_t size_class(int32_t t, int32_t split) {
+  return (int32_t)((int64_t)t * kSizeClasses / (split + 1));
+}
+
 // Builds the per-step work list in the workspace: one descriptor per item, so
-// that an item needs a single load to start, and the list of rows with
-// several items (first item, item count, slot) for combine_kernel.
+// that an item needs a single load to start; the list of rows with several
+// items (first item, item count, slot) for combine_kernel; and the dispatch
+// order, the items from the most tokens to the fewest (a counting sort over
+// size classes; the order within a class is arbitrary and affects no result).
+// The attention workgroups are then dealt largest first, so that the ones that
+// start last are short and the launch ends with little of the GPU idle.
 __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, Item* ws_items,
-                                                            int4* ws_multi) {
+                                                            int4* ws_multi, int32_t* ws_order) {
   __shared__ int32_t scan[kMetaThreads];
   __shared__ int32_t scan_multi[kMetaThreads];
+  __shared__ int32_t cursor[kSizeClasses];
   const int b = threadIdx.x;
   const int32_t n = b < a.batch ? a.lens[b] : 0;
   const int32_t cnt = b < a.batch ? row_items(a, b) : 0;
+  if (b < kSizeClasses) cursor[b] = 0;
   scan[b] = cnt;
   scan_multi[b] = cnt > 1 ? 1 : 0;
   __syncthreads();
@@ -83,14 +100,39 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
     const int4 row = make_int4(first, cnt, 0, 0);
     if (n == 0) {
       ws_items[first] = Item{make_int4(b, 0, 0, -1), row};
+      atomicAdd(&cursor[0], 1);
     } else {
       int32_t c = first;
       row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
-        for (int32_t t = t0; t < t1; t += a.split)
-          ws_items[c++] = Item{make_int4(b, t, min(t + a.split, t1), n), row};
+        for (int32_t t = t0; t < t1; t += a.split) {
+          const int32_t te = min(t + a.split, t1);
+          ws_items[c++] = Item{make_int4(b, t, te, n), row};
+          atomicAdd(&cursor[size_class(te - t, a.split)], 1);
+        }
       });
     }
     if (cnt > 1) ws_multi[scan_multi[b] - 1] = make_int4(first, cnt, b, 0);
+  }
+  __syncthreads();
+  if (b == 0) {   // start of each class in the order, largest class first
+    int32_t pos = 0;
+    for (int k = kSizeClasses - 1; k >= 0; --k) {
+      const int32_t c = cursor[k];
+      cursor[k] = pos;
+      pos += c;
+    }
+  }
+  __syncthreads();
+  if (b < a.batch && cnt > 0) {
+    if (n == 0) {
+      ws_order[atomicAdd(&cursor[0], 1)] = first;
+    } else {
+      int32_t c = first;
+      row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
+        for (int32_t t = t0; t < t1; t += a.split, ++c)
+          ws_order[atomicAdd(&cursor[size_class(min(t + a.split, t1) - t, a.split)], 1)] = c;
+      });
+    }
   }
 }
 
@@ -104,6 +146,7 @@ struct AttnArgs {
   uint32_t* out;             // [batch][tw][n_q_heads][D]
   const Item* items;         // workspace
   const int4* multi;         // rows with several items: (first item, count, slot)
+  const int32_t* order;      // dispatch order of the items
   float* partial;            // [n_kv_heads][n_items][G][D + 4]
   int64_t cap, base, L;
   int32_t layer, batch, n_kv_heads, split, n_items;
@@ -155,13 +198,13 @@ __device__ __forceinline__ void online_update(const u32x4 (&kw)[U], const u32x4 
 #pragma unroll
     for (int u = 0; u < U; ++u) mt = fmaxf(mt, s[u][gi]);
     const float ref = mt == -INFINITY ? 0.f : mt;
-    const float alpha = exp2f(m[gi] - ref);
+    const float alpha = fast_exp2(m[gi] - ref);
     l[gi] *= alpha;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[gi][e] *= alpha;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float p = exp2f(s[u][gi] - ref);
+      const float p = fast_exp2(s[u][gi] - ref);
       l[gi] += p;
       float vf[EPL];
       Lane16<T>::widen(vw[u], vf);
@@ -232,11 +275,76 @@ __device__ __forceinline__ void merge_row(const float* base, int32_t count, uint
 }
 
 #ifndef BATON_ATTN_WAVES_PER_EU
-#define BATON_ATTN_WAVES_PER_EU 0   // 0: compiler's choice
+#define BATON_ATTN_WAVES_PER_EU 2   // keeps the register budget at two waves per SIMD (0: compiler's choice)
 #endif
 
-template <typename T, int D, int G, int U>
-__global__ void __launch_bounds__(kWave)
+// The work unit (item, kv-head) of this workgroup: workgroups are dealt in
+// the order of the work list's dispatch order (largest items first), all
+// kv-heads of an item next to each other.
+__device__ __forceinline__ void work_unit(const AttnArgs& a, int32_t& item, int32_t& h) {
+  const int32_t k = blockIdx.x;
+  item = a.order[k / a.n_kv_heads];
+  h = k % a.n_kv_heads;
+}
+
+// Merge of the NW waves of a workgroup, each holding the online-softmax state
+// of its share of the item's tokens for the G query heads: wave w has put its
+// max, sum and accumulator into sm_m[w][gi], sm_l[w][gi], sm_acc[w][gi][D]
+// (a wave with no tokens: max -inf, sum 0).  Every thread of the workgroup
+// then merges pairs of output elements with the log-sum-exp rescale and writes
+// the item's output (the item is its row's only one) or its partial record.
+template <typename T, int D, int G, int NW>
+__device__ __forceinline__ void wg_merge_write(const float (&sm_m)[NW][G], const float (&sm_l)[NW][G],
+                                               const float (&sm_acc)[NW][G][D], bool whole_row,
+                                               uint32_t* outw, float* rec0, int tid) {
+  constexpr int REC = D + 4;
+  for (int p = tid; p < G * D / 2; p += NW * kWave) {
+    const int gi = p / (D / 2), e = 2 * (p % (D / 2));
+    float mm = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) mm = fmaxf(mm, sm_m[w][gi]);
+    float l = 0.f, o0 = 0.f, o1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = sm_m[w][gi];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - mm);
+      l = fmaf(f, sm_l[w][gi], l);
+      o0 = fmaf(f, sm_acc[w][gi][e], o0);
+      o1 = fmaf(f, sm_acc[w][gi][e + 1], o1);
+    }
+    if (whole_row) {
+      const float inv = 1.f / l;
+      if constexpr (T::kBytes == 4) {
+        outw[gi * D + e] = __float_as_uint(o0 * inv);
+        outw[gi * D + e + 1] = __float_as_uint(o1 * inv);
+      } else {
+        outw[(gi * D + e) / 2] = f32_to_bf16_rne(o0 * inv) | (f32_to_bf16_rne(o1 * inv) << 16);
+      }
+    } else {
+      float* rec = rec0 + gi * REC;
+      rec[e] = o0;
+      rec[e + 1] = o1;
+      if (e == 0) {
+        rec[D] = mm;
+        rec[D + 1] = l;
+      }
+    }
+  }
+}
+
+// Tokens [wb, we) of an item [t_begin, t_end) that wave w of NW streams: equal
+// contiguous shares, whole loop steps of STEP tokens except at the end.
+template <int NW, int STEP>
+__device__ __forceinline__ void wave_share(int32_t t_begin, int32_t t_end, int w, int32_t& wb,
+                                           int32_t& we) {
+  const int32_t per = (t_end - t_begin + NW - 1) / NW;
+  const int32_t part = (per + STEP - 1) / STEP * STEP;
+  wb = min(t_begin + w * part, t_end);
+  we = min(wb + part, t_end);
+}
+
+template <typename T, int D, int G, int U, int NW>
+__global__ void __launch_bounds__(kWave * NW)
 #if BATON_ATTN_WAVES_PER_EU > 0
 __attribute__((amdgpu_waves_per_eu(BATON_ATTN_WAVES_PER_EU)))
 #endif
@@ -244,28 +352,31 @@ attn_kernel(const AttnArgs a) {
   using Geo = Geometry<T, D>;
   constexpr int EPL = Geo::kEpl, LPT = Geo::kLpt, TPI = Geo::kTpi, VPT = Geo::kVpt;
   constexpr int REC = D + 4;   // floats per partial record
-  const int item = blockIdx.x;
-  const int h = blockIdx.y;
-  const int lane = threadIdx.x;
+  __shared__ float sm_m[NW][G], sm_l[NW][G];
+  __shared__ float sm_acc[NW][G][D];
+  int32_t item, h;
+  work_unit(a, item, h);
+  const int tid = threadIdx.x;
+  // wave of the workgroup, as a scalar: the loop bounds derived from it are uniform
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int lane = tid % kWave;
   const int r = lane / LPT;        // token row within an instruction
   const int cl = lane % LPT;       // 16-byte slice of the row
 
   const int4 it = a.items[item].span;
   const int4 rw = a.items[item].row;
   const int b = it.x;
-  const int32_t t_begin = it.y, t_end = it.z;
   const int32_t n = it.w;          // cached tokens; token n is the current one
   const int64_t bt = (int64_t)b * a.tw;   // input row of the slot's position 0
   uint32_t* outw = a.out + ((bt * a.n_kv_heads + h) * G) * (D * T::kBytes / 4);
   if (n < 0) {                     // free slot: the output rows are zero
-    if (r == 0) {
-#pragma unroll
-      for (int gi = 0; gi < G; ++gi)
-        reinterpret_cast<u32x4*>(outw)[gi * VPT + cl] = u32x4{0, 0, 0, 0};
-    }
+    for (int v = tid; v < G * VPT; v += NW * kWave) reinterpret_cast<u32x4*>(outw)[v] = u32x4{0, 0, 0, 0};
     return;
   }
   const bool whole_row = rw.y == 1;
+  constexpr int32_t STEP = TPI * U;
+  int32_t t_begin, t_end;          // this wave's share of the item's tokens
+  wave_share<NW, STEP>(it.y, it.z, w, t_begin, t_end);
 
   const int64_t row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
   constexpr uint32_t ROWB = VPT * 16;                     // bytes per token row
@@ -284,8 +395,8 @@ attn_kernel(const AttnArgs a) {
   float qf[G][EPL];
 #pragma unroll
   for (int gi = 0; gi < G; ++gi) {
-    const u32x4 w = reinterpret_cast<const u32x4*>(a.q)[((bt * a.n_kv_heads + h) * G + gi) * VPT + cl];
-    Lane16<T>::widen(w, qf[gi]);
+    const u32x4 qw = reinterpret_cast<const u32x4*>(a.q)[((bt * a.n_kv_heads + h) * G + gi) * VPT + cl];
+    Lane16<T>::widen(qw, qf[gi]);
 #pragma unroll
     for (int e = 0; e < EPL; ++e) qf[gi][e] *= a.qscale;
   }
@@ -299,12 +410,13 @@ attn_kernel(const AttnArgs a) {
     for (int e = 0; e < EPL; ++e) acc[gi][e] = 0.f;
   }
 
-  // Cached tokens of the item, software-pipelined: the 2U loads of the next
+  // Cached tokens of the share, software-pipelined: the 2U loads of the next
   // iteration are in flight while the current one is computed.  A token past
   // the end gets an offset beyond the buffer's range, which the hardware
-  // answers with zeros (its score is then set to -inf).
+  // answers with zeros and no memory access (its score is then set to -inf).
+  // The loads are issued unconditionally, also past the end: a load under a
+  // branch would make the wait before the computation wait for it too.
   const int32_t c_end = min(t_end, n);
-  constexpr int32_t STEP = TPI * U;
   auto issue = [&](int32_t tt, u32x4 (&kw)[U], u32x4 (&vw)[U], bool (&valid)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -320,21 +432,23 @@ attn_kernel(const AttnArgs a) {
   if (t_begin < c_end) {
     u32x4 ka[U], va[U], kb[U], vb[U];
     bool la[U], lb[U];
+    const int32_t n_iter = (c_end - t_begin + STEP - 1) / STEP;
     issue(t_begin, ka, va, la);
-    for (int32_t tt = t_begin;;) {
-      if (tt + STEP < c_end) issue(tt + STEP, kb, vb, lb);
+    int32_t tt = t_begin;
+    for (int32_t i = 0; i + 2 <= n_iter; i += 2) {
+      issue(tt + STEP, kb, vb, lb);
+      __builtin_amdgcn_sched_barrier(0);   // keep the loads ahead of the computation
       online_update<T, G, U, EPL, LPT>(ka, va, la, qf, m, l, acc);
-      tt += STEP;
-      if (tt >= c_end) break;
-      if (tt + STEP < c_end) issue(tt + STEP, ka, va, la);
+      issue(tt + 2 * STEP, ka, va, la);
+      __builtin_amdgcn_sched_barrier(0);
       online_update<T, G, U, EPL, LPT>(kb, vb, lb, qf, m, l, acc);
-      tt += STEP;
-      if (tt >= c_end) break;
+      tt += 2 * STEP;
     }
+    if (n_iter & 1) online_update<T, G, U, EPL, LPT>(ka, va, la, qf, m, l, acc);
   }
 
   // The current token: read from k_new / v_new by lane group 0, appended to
-  // the cache as column L by the item that holds it (once per row).
+  // the cache as column L by the wave that holds it (once per row).
   if (n >= t_begin && n < t_end) {
     u32x4 kw[1] = {knew[cl]}, vw[1] = {vnew[cl]};
     bool valid[1] = {r == 0};
@@ -346,7 +460,7 @@ attn_kernel(const AttnArgs a) {
     }
   }
 
-  // Merge the TPI lane groups.
+  // Merge the TPI lane groups of the wave.
 #pragma unroll
   for (int off = LPT; off < kWave; off <<= 1) {
 #pragma unroll
@@ -366,32 +480,21 @@ attn_kernel(const AttnArgs a) {
     }
   }
 
-  if (whole_row) {
-    if (r == 0) {
-#pragma unroll
-      for (int gi = 0; gi < G; ++gi) {
-        const float inv = 1.f / l[gi];
-        float o[EPL];
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) o[e] = acc[gi][e] * inv;
-        reinterpret_cast<u32x4*>(outw)[gi * VPT + cl] = Lane16<T>::narrow(o);
-      }
-    }
-    return;
-  }
-  float* part = a.partial + ((int64_t)h * a.n_items) * G * REC;
+  // Merge the waves through LDS and write the output or the partial record.
   if (r == 0) {
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
-      float* rec = part + ((int64_t)item * G + gi) * REC;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) rec[cl * EPL + e] = acc[gi][e];
+      for (int e = 0; e < EPL; ++e) sm_acc[w][gi][cl * EPL + e] = acc[gi][e];
       if (cl == 0) {
-        rec[D] = m[gi];
-        rec[D + 1] = l[gi];
+        sm_m[w][gi] = m[gi];
+        sm_l[w][gi] = l[gi];
       }
     }
   }
+  __syncthreads();
+  float* rec0 = a.partial + (((int64_t)h * a.n_items + item) * G) * REC;
+  wg_merge_write<T, D, G, NW>(sm_m, sm_l, sm_acc, whole_row, outw, rec0, tid);
 }
 
 // One wave per (row with several items, query head): the log-sum-exp merge

@@ -16,7 +16,9 @@
 //    head_dim.  V is staged in LDS row by row (coalesced global loads) and read
 //    back transposed, 2 bytes per lane; the token order above makes the four
 //    lane groups of one read hit consecutive rows, i.e. disjoint banks.
-// The current token (k_new, v_new) is a one-token tile of its own.  Partial
+// The current token (k_new, v_new) is a one-token tile of its own.  As in the
+// VALU kernel, a workgroup of NW waves takes one work item, each wave an equal
+// contiguous share of its tokens, and the waves merge through LDS; partial
 // records and outputs have the layout of the VALU kernel, so combine_kernel
 // merges both.
 #pragma once
@@ -113,30 +115,37 @@ __device__ __forceinline__ void mfma_block(const u32x4 (&kA)[D / 32], const u32x
 #define BATON_MFMA_WAVES_PER_EU 0   // 0: compiler's choice
 #endif
 
-template <int D, int G>
-__global__ void __launch_bounds__(kWave)
+template <int D, int G, int NW>
+__global__ void __launch_bounds__(kWave * NW)
 #if BATON_MFMA_WAVES_PER_EU > 0
 __attribute__((amdgpu_waves_per_eu(BATON_MFMA_WAVES_PER_EU)))
 #endif
 attn_mfma_kernel(const AttnArgs a) {
   using Geo = MfmaGeo<D>;
   constexpr int VPT = Geo::kVpt, KK = Geo::kKk, DT = Geo::kDt, REC = D + 4;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[32 * Geo::kLdsRow];
-  const int item = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  __shared__ __attribute__((aligned(16))) uint8_t lds_v[NW][32 * Geo::kLdsRow];
+  __shared__ float sm_m[NW][G], sm_l[NW][G];
+  __shared__ float sm_acc[NW][G][D];
+  int32_t item, h;
+  work_unit(a, item, h);
+  const int tid = threadIdx.x;
+  // wave of the workgroup, as a scalar: the loop bounds derived from it are uniform
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
   const int g4 = lane / 16, c16 = lane % 16;
+  uint8_t* lds = lds_v[w];
 
   const int4 it = a.items[item].span;
   const int4 rw = a.items[item].row;
   const int b = it.x;
-  const int32_t t_begin = it.y, t_end = it.z, n = it.w;
+  const int32_t n = it.w;
   const int64_t bt = (int64_t)b * a.tw;   // input row of the slot's position 0
   uint32_t* outw = a.out + ((bt * a.n_kv_heads + h) * G) * (D / 2);
   if (n < 0) {                       // free slot: zero output rows
-#pragma unroll
-    for (int gi = 0; gi < G; ++gi)
-      if (lane < VPT) reinterpret_cast<u32x4*>(outw)[gi * VPT + lane] = u32x4{0, 0, 0, 0};
+    for (int v = tid; v < G * VPT; v += NW * kWave) reinterpret_cast<u32x4*>(outw)[v] = u32x4{0, 0, 0, 0};
     return;
   }
+  int32_t t_begin, t_end;            // this wave's share of the item's tokens
+  wave_share<NW, 32>(it.y, it.z, w, t_begin, t_end);
   const int64_t row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
   constexpr uint32_t ROWB = VPT * 16;
   const uint32_t ring_bytes = (uint32_t)a.cap * ROWB;
@@ -153,8 +162,8 @@ attn_mfma_kernel(const AttnArgs a) {
   const u32x4* qrow = reinterpret_cast<const u32x4*>(a.q) + ((bt * a.n_kv_heads + h) * G) * VPT;
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
-    const u32x4 w = c16 < G ? qrow[c16 * VPT + kk * 4 + g4] : u32x4{0, 0, 0, 0};
-    qb[kk] = as_bf16x8(w);
+    const u32x4 qw = c16 < G ? qrow[c16 * VPT + kk * 4 + g4] : u32x4{0, 0, 0, 0};
+    qb[kk] = as_bf16x8(qw);
   }
 
   float m = -INFINITY, lsum = 0.f;
@@ -210,32 +219,26 @@ attn_mfma_kernel(const AttnArgs a) {
     }
   }
 
-  // Row sums over the four lane groups; lane l's output rows are heads 4*g4 + r.
+  // Row sums over the four lane groups; lane l's output rows are heads
+  // 4*g4 + r.  The wave's state goes to LDS for the workgroup's merge.
   lsum += __shfl_xor(lsum, 16, kWave);
   lsum += __shfl_xor(lsum, 32, kWave);
-  const bool whole_row = rw.y == 1;
-  float* part = a.partial + ((int64_t)h * a.n_items) * G * REC;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int head = 4 * g4 + r;
     const float lr = __shfl(lsum, head, kWave);
     const float mr = __shfl(m, head, kWave);
     if (head >= G) continue;
-    if (whole_row) {
-      const float inv = 1.f / lr;
-      uint16_t* out16 = reinterpret_cast<uint16_t*>(outw) + head * D;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) out16[16 * dt + c16] = (uint16_t)f32_to_bf16_rne(o[dt][r] * inv);
-    } else {
-      float* rec = part + ((int64_t)item * G + head) * REC;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) rec[16 * dt + c16] = o[dt][r];
-      if (c16 == 0) {
-        rec[D] = mr;
-        rec[D + 1] = lr;
-      }
+    for (int dt = 0; dt < DT; ++dt) sm_acc[w][head][16 * dt + c16] = o[dt][r];
+    if (c16 == 0) {
+      sm_m[w][head] = mr;
+      sm_l[w][head] = lr;
     }
   }
+  __syncthreads();
+  float* rec0 = a.partial + (((int64_t)h * a.n_items + item) * G) * REC;
+  wg_merge_write<BF16Tag, D, G, NW>(sm_m, sm_l, sm_acc, rw.y == 1, outw, rec0, tid);
 }
 
 }  // namespace baton
