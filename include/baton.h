@@ -340,6 +340,40 @@ baton_status baton_linear(baton_gemm* gemm, int32_t dtype, const void* x, const 
                           size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The same product at a decode step's batch (rows <= 64) on the library's
+ * weight-streaming kernel, which reads the weight in a packed form made once
+ * per weight by baton_linear_pack.  The weight dominates the traffic of such
+ * a product and is read exactly once; the packed form lets each wave stream it
+ * in contiguous 1 KB blocks.
+ *
+ * baton_linear_packed_bytes: bytes of the packed form of an [out_dim][in_dim]
+ * weight: 2 * ceil(out_dim / 16) * 16 * ceil(in_dim / 32) * 32 (0 for sizes < 1).
+ *
+ * baton_linear_pack: writes the packed form of w (device [out_dim][in_dim],
+ * bf16) into wp (device, caller-owned, baton_linear_packed_bytes, 16-byte
+ * aligned): 16-row slices of w, each a run of 1 KB blocks, one per 32 columns,
+ * block (s, t) holding at byte 16 l the eight elements
+ * w[16 s + l % 16][32 t + 8 (l / 16) ...] (zeros past out_dim or in_dim).
+ * Errors: EINVAL (null or misaligned pointer, sizes < 1 or not multiples of
+ * 8), EDTYPE (not bf16), EHIP.
+ *
+ * baton_linear_packed: y[r] (+)= x[r] . W^T for r < rows <= 64, W given by its
+ * packed form wp; x, y, accumulate as in baton_linear.  fp32 accumulation;
+ * when the output has few 16-row slices the sum is split along in_dim and the
+ * fp32 partial sums, kept in ws (device, caller-owned; as many splits as
+ * ws_bytes holds rows * out_dim floats for, none with ws_bytes = 0), are added
+ * in a second launch in a fixed order.  Errors: EINVAL (null or misaligned
+ * pointer, rows outside 1..64, sizes < 1 or not multiples of 8, accumulate not
+ * 0/1), EDTYPE, EHIP.
+ */
+size_t baton_linear_packed_bytes(int32_t out_dim, int32_t in_dim);
+baton_status baton_linear_pack(int32_t dtype, const void* w, void* wp, int32_t out_dim, int32_t in_dim,
+                               hipStream_t stream);
+baton_status baton_linear_packed(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                 int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/*
  * y[r] = x[r] / sqrt(mean_j x[r][j]^2 + eps) * gain: x, y device [rows][dim],
  * gain device [dim]; dim a multiple of 8.  y may alias x.
  * Errors: EINVAL (null or misaligned pointer, bad sizes, eps < 0), EDTYPE.

@@ -71,6 +71,10 @@ def lib():
         L.baton_gemm_create.argtypes = [P(vp)]
         L.baton_gemm_destroy.argtypes = [vp]
         L.baton_linear.argtypes = [vp, i32, vp, vp, vp, i32, i32, i32, i32, vp, ctypes.c_size_t, vp]
+        L.baton_linear_packed_bytes.argtypes = [i32, i32]
+        L.baton_linear_packed_bytes.restype = ctypes.c_size_t
+        L.baton_linear_pack.argtypes = [i32, vp, vp, i32, i32, vp]
+        L.baton_linear_packed.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, vp, ctypes.c_size_t, vp]
         L.baton_rmsnorm.argtypes = [i32, vp, vp, vp, i32, i32, ctypes.c_float, vp]
         L.baton_rope_qkv.argtypes = [vp, vp, vp, vp, vp, ctypes.c_float, vp]
         L.baton_silu_mul.argtypes = [i32, vp, vp, i32, i32, vp]
@@ -81,8 +85,8 @@ def lib():
                      "baton_build_mask", "baton_decode_attn", "baton_step_advance",
                      "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
                      "baton_shape_insert", "baton_cache_tokens", "baton_kv_move", "baton_gemm_create",
-                     "baton_gemm_destroy", "baton_linear", "baton_rmsnorm", "baton_rope_qkv",
-                     "baton_silu_mul"):
+                     "baton_gemm_destroy", "baton_linear", "baton_linear_pack", "baton_linear_packed",
+                     "baton_rmsnorm", "baton_rope_qkv", "baton_silu_mul"):
             getattr(L, name).restype = st
         _lib = L
     return _lib
@@ -227,6 +231,19 @@ def baton_gemm_destroy(gemm):
 def baton_linear(gemm, dtype, x, w, y, rows, out_dim, in_dim, accumulate, ws, ws_bytes, stream=None):
     _check(lib().baton_linear(gemm, dtype, _ptr(x), _ptr(w), _ptr(y), rows, out_dim, in_dim,
                               int(accumulate), _ptr(ws), ws_bytes, _stream(stream)), "baton_linear")
+
+
+def baton_linear_packed_bytes(out_dim, in_dim):
+    return lib().baton_linear_packed_bytes(out_dim, in_dim)
+
+
+def baton_linear_pack(dtype, w, wp, out_dim, in_dim, stream=None):
+    _check(lib().baton_linear_pack(dtype, _ptr(w), _ptr(wp), out_dim, in_dim, _stream(stream)), "baton_linear_pack")
+
+
+def baton_linear_packed(dtype, x, wp, y, rows, out_dim, in_dim, accumulate, ws, ws_bytes, stream=None):
+    _check(lib().baton_linear_packed(dtype, _ptr(x), _ptr(wp), _ptr(y), rows, out_dim, in_dim, int(accumulate),
+                                     _ptr(ws), ws_bytes, _stream(stream)), "baton_linear_packed")
 
 
 def baton_rmsnorm(dtype, x, gain, y, rows, dim, eps, stream=None):

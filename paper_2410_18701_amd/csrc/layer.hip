@@ -1,9 +1,11 @@
-// Host side of the decode-layer operations around the attention: hipBLASLt
-// GEMMs for the projections, launches of the row and elementwise kernels.
+// Host side of the decode-layer operations around the attention: the
+// projections (hipBLASLt on stored weights; the weight-streaming GEMM on
+// packed weights up to 64 rows), launches of the row and elementwise kernels.
 // The C ABI is documented in include/baton.h.
 #include <hip/hip_runtime.h>
 #include <hipblaslt/hipblaslt.h>
 
+#include <algorithm>
 #include <cmath>
 #include <map>
 #include <new>
@@ -45,6 +47,22 @@ bool make_descs(LtDescs& d, int32_t rows, int32_t out, int32_t in) {
   return hipblasLtMatrixLayoutCreate(&d.a, HIP_R_16BF, in, out, in) == HIPBLAS_STATUS_SUCCESS &&
          hipblasLtMatrixLayoutCreate(&d.b, HIP_R_16BF, in, rows, in) == HIPBLAS_STATUS_SUCCESS &&
          hipblasLtMatrixLayoutCreate(&d.c, HIP_R_16BF, out, rows, out) == HIPBLAS_STATUS_SUCCESS;
+}
+
+#ifndef BATON_GEMM_TARGET_WAVES
+#define BATON_GEMM_TARGET_WAVES 1024   // weight slices x splits when the slices alone are too few
+#endif
+#ifndef BATON_GEMM_MIN_SLICES
+#define BATON_GEMM_MIN_SLICES 512      // from this many slices on, no split along k
+#endif
+#ifndef BATON_GEMM_KU
+#define BATON_GEMM_KU 4                // 1 KB weight blocks per load batch of a wave
+#endif
+
+template <int MG>
+void launch_skinny_mg(const baton::SkinnyArgs& a, dim3 grid, hipStream_t s) {
+  hipLaunchKernelGGL((baton::skinny_gemm_kernel<MG, BATON_GEMM_KU>), grid, dim3(baton::kWave * baton::kGemmWaves), 0,
+                     s, a);
 }
 
 }  // namespace
@@ -101,6 +119,73 @@ baton_status baton_linear(baton_gemm* g, int32_t dtype, const void* x, const voi
   const hipblasStatus_t st = hipblasLtMatmul(g->lt, d.op, &alpha, w, d.a, x, d.b, &beta, y, d.c, y, d.c,
                                              &it->second, ws, ws_bytes, stream);
   return st == HIPBLAS_STATUS_SUCCESS ? BATON_OK : BATON_EHIP;
+}
+
+size_t baton_linear_packed_bytes(int32_t out_dim, int32_t in_dim) {
+  if (out_dim < 1 || in_dim < 1) return 0;
+  return (size_t)((out_dim + 15) / 16) * 16 * (size_t)((in_dim + 31) / 32) * 32 * 2;
+}
+
+baton_status baton_linear_pack(int32_t dtype, const void* w, void* wp, int32_t out_dim, int32_t in_dim,
+                               hipStream_t stream) {
+  if (!w || !wp || out_dim < 1 || in_dim < 1 || in_dim % 8 || out_dim % 8) return BATON_EINVAL;
+  if (dtype != BATON_BF16) return BATON_EDTYPE;
+  if (!aligned16(w) || !aligned16(wp) || in_dim > (1 << 24)) return BATON_EINVAL;
+  const int32_t kt = (in_dim + 31) / 32;
+  const int64_t n_pieces = (int64_t)((out_dim + 15) / 16) * kt * baton::kWave;
+  hipLaunchKernelGGL(baton::pack_weight_kernel, dim3((unsigned)((n_pieces + 255) / 256)), dim3(256), 0, stream,
+                     static_cast<const baton::u32x4*>(w), static_cast<baton::u32x4*>(wp), out_dim, in_dim, kt,
+                     n_pieces);
+  return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
+}
+
+baton_status baton_linear_packed(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                 int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  if (!x || !wp || !y || rows < 1 || rows > 64 || out_dim < 1 || in_dim < 1 || (ws_bytes && !ws))
+    return BATON_EINVAL;
+  if (accumulate != 0 && accumulate != 1) return BATON_EINVAL;
+  if (dtype != BATON_BF16) return BATON_EDTYPE;
+  if (!aligned16(x) || !aligned16(wp) || !aligned16(y) || in_dim % 8 || out_dim % 8 || in_dim > (1 << 24))
+    return BATON_EINVAL;
+  // 16-row weight slices; with fewer than BATON_GEMM_MIN_SLICES of them,
+  // split along k into about BATON_GEMM_TARGET_WAVES / slices ranges (at least
+  // 8 blocks of 32 each, and only as many as the workspace holds partial sums
+  // for).  Measured on the llama2-7b shapes at 64 rows: the split's partial
+  // sums and second launch cost more than they gain once the slices alone
+  // give two waves per SIMD.
+  const int32_t slices = (out_dim + 15) / 16, kt = (in_dim + 31) / 32;
+  int32_t S = 1;
+  if (slices < BATON_GEMM_MIN_SLICES)
+    S = std::max(1, std::min((BATON_GEMM_TARGET_WAVES + slices - 1) / slices, kt / 8));
+  if (!ws || !aligned16(ws)) S = 1;
+  while (S > 1 && (size_t)S * rows * out_dim * sizeof(float) > ws_bytes) --S;
+  const int32_t tc = (kt + S - 1) / S;
+  S = (kt + tc - 1) / tc;
+  baton::SkinnyArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.wp = static_cast<const uint16_t*>(wp);
+  a.y = static_cast<uint16_t*>(y);
+  a.part = static_cast<float*>(ws);
+  a.rows = rows;
+  a.N = out_dim;
+  a.K = in_dim;
+  a.kt = kt;
+  a.tc = tc;
+  a.accumulate = accumulate;
+  const dim3 grid((unsigned)((slices + baton::kGemmWaves - 1) / baton::kGemmWaves), (unsigned)S);
+  switch ((rows + 15) / 16) {
+    case 1: launch_skinny_mg<1>(a, grid, stream); break;
+    case 2: launch_skinny_mg<2>(a, grid, stream); break;
+    case 3: launch_skinny_mg<3>(a, grid, stream); break;
+    default: launch_skinny_mg<4>(a, grid, stream); break;
+  }
+  if (S > 1) {
+    const int64_t n_out = (int64_t)rows * out_dim;
+    hipLaunchKernelGGL(baton::gemm_reduce_kernel, dim3((unsigned)((n_out / 4 + 255) / 256)), dim3(256), 0, stream,
+                       a.part, a.y, S, n_out, accumulate);
+  }
+  return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
 }
 
 baton_status baton_rmsnorm(int32_t dtype, const void* x, const void* gain, void* y, int32_t rows, int32_t dim,

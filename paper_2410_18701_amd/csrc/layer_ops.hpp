@@ -1,7 +1,8 @@
-// Elementwise and row kernels of a decode layer around the attention (the
-// GEMMs are hipBLASLt's): RMS normalisation, the fused projection's split with
-// rotary embedding of queries and keys, and the gated activation.  bf16
-// storage, fp32 arithmetic, outputs rounded to nearest even.
+// Kernels of a decode layer around the attention: the weight-streaming GEMM
+// of the projections at decode batch sizes (larger batches use hipBLASLt), RMS
+// normalisation, the fused projection's split with rotary embedding of
+// queries and keys, and the gated activation.  bf16 storage, fp32
+// arithmetic, outputs rounded to nearest even.
 #pragma once
 
 #include "common.hpp"
@@ -106,6 +107,216 @@ __global__ void __launch_bounds__(256) silu_mul_kernel(const u32x4* __restrict__
     o[j] = pack_bf16(s0 * bf16_lo(u[j]), s1 * bf16_hi(u[j]));
   }
   out[i] = o;
+}
+
+// ------------------------------------------------------------ skinny GEMM --
+// y[m][n] (+)= sum_k x[m][k] w[n][k] for m < rows <= 64: a linear layer at a
+// decode step's batch.  The weight matrix (megabytes) is read exactly once and
+// dominates the traffic; x (rows x K) is small and stays in the caches.
+//
+// The weight is used in a packed form, made once per weight by
+// pack_weight_kernel: 16-row slices of w, each a run of 1 KB blocks, one per
+// step of 32 along k, block (s, t) holding at byte 16 l the eight elements
+// w[16 s + l % 16][32 t + 8 (l / 16) ..] (zeros past N or K) -- exactly the A
+// operand of v_mfma_f32_16x16x32_bf16 for lane l.  A wave owns one slice (four
+// per workgroup) and streams its blocks with one contiguous 1 KB load per
+// step, so every weight row is read in long bursts (in the stored row-major
+// layout a wave would touch 16 rows 64 bytes at a time, which the DRAM serves
+// at a fraction of its bandwidth).  When there are too few slices to occupy
+// the GPU the steps are also split into S ranges whose fp32 partial sums
+// gemm_reduce_kernel adds up.  x's rows are the B operand, 16 at a time (lane
+// l: row 16 j + l % 16, the same k group); lane l then holds outputs
+// (n0 + 4 (l / 16) + r, 16 j + l % 16), r < 4.  Loads are raw buffer loads
+// whose out-of-range offsets return zeros: x rows past `rows` and k past K
+// need no branch.
+typedef __bf16 gemm_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float gemm_f32x4 __attribute__((ext_vector_type(4)));
+
+struct SkinnyArgs {
+  const uint16_t* x;     // [rows][K]
+  const uint16_t* wp;    // packed weight: [ceil(N / 16)][ceil(K / 32)] blocks of 512 elements
+  uint16_t* y;           // [rows][N]
+  float* part;           // [S][rows][N] fp32, when S > 1
+  int32_t rows, N, K;
+  int32_t kt;            // blocks per slice, ceil(K / 32)
+  int32_t tc;            // blocks per split
+  int32_t accumulate;    // 1: y += x . w^T
+};
+
+#ifndef BATON_GEMM_WAVES
+#define BATON_GEMM_WAVES 4
+#endif
+constexpr int32_t kGemmWaves = BATON_GEMM_WAVES;   // weight slices per workgroup
+constexpr uint32_t kGemmOob = 0x80000000u;   // an offset past every buffer's range
+constexpr int32_t kGemmBufWord3 = 0x00020000;
+
+template <int AUX>   // 2: non-temporal
+__device__ __forceinline__ u32x4 gemm_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
+}
+
+// One thread per 16-byte piece of the packed weight.
+__global__ void __launch_bounds__(256) pack_weight_kernel(const u32x4* __restrict__ w, u32x4* __restrict__ wp,
+                                                          int32_t N, int32_t K, int32_t kt, int64_t n_pieces) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_pieces) return;
+  const int32_t l = (int32_t)(i % kWave);
+  const int64_t blk = i / kWave;
+  const int32_t t = (int32_t)(blk % kt);
+  const int32_t n = (int32_t)(blk / kt) * 16 + l % 16, k = 32 * t + 8 * (l / 16);
+  wp[i] = (n < N && k < K) ? w[((int64_t)n * K + k) / 8] : u32x4{0, 0, 0, 0};
+}
+
+// Activation rows staged in LDS per batch of KU blocks: 64 rows of 64 KU
+// bytes, each padded by 16 bytes so that the 16 rows one B-operand read spans
+// fall in different banks.
+template <int KU>
+struct GemmLds {
+  static constexpr int kRow = 64 * KU + 16;   // bytes per staged row
+  static constexpr int kBuf = 64 * kRow;      // one batch of 64 rows
+  static constexpr int kPieces = 4 * KU;      // 16-byte pieces per row and batch
+};
+
+template <int MG, int KU>
+__global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const SkinnyArgs a) {
+  using Lds = GemmLds<KU>;
+  constexpr int kXPer = 64 * Lds::kPieces / (kWave * kGemmWaves);   // activation pieces per thread and batch
+  __shared__ __attribute__((aligned(16))) uint8_t xs[2][Lds::kBuf];
+  const int tid = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int lane = tid % kWave, c16 = lane % 16, g4 = lane / 16;
+  const int32_t slice = blockIdx.x * kGemmWaves + w;
+  const int32_t n0 = slice * 16;
+  const int32_t n_rows = max(0, min(16, a.N - n0));   // 0: a wave past N (loads nothing, writes nothing)
+  const int32_t t_begin = blockIdx.y * a.tc, t_end = min(a.kt, t_begin + a.tc);
+  const uint32_t row_bytes = (uint32_t)a.K * 2u;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.wp) + ((int64_t)min(slice, (a.N + 15) / 16) * a.kt + t_begin) * 512, 0,
+      n_rows > 0 ? (t_end - t_begin) * 1024 : 0, kGemmBufWord3);
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.x), 0, (int32_t)(a.rows * row_bytes), kGemmBufWord3);
+
+  gemm_f32x4 acc[MG];
+#pragma unroll
+  for (int j = 0; j < MG; ++j) acc[j] = gemm_f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Loads of batch b (blocks t_begin + KU b ...): the workgroup's activation
+  // pieces (thread tid: pieces tid + 64 kGemmWaves i -- row p / (4 KU), 16 bytes at
+  // 16 (p % (4 KU)) of the batch) and this wave's weight blocks, both issued
+  // unconditionally (past the end they return zeros).
+  auto issue = [&](int32_t b, u32x4 (&xr)[kXPer], u32x4 (&wr)[KU]) {
+    const int32_t tb = t_begin + KU * b;
+#pragma unroll
+    for (int i = 0; i < kXPer; ++i) {
+      const int32_t p = tid + kWave * kGemmWaves * i;
+      const int32_t m = p / Lds::kPieces, c = p % Lds::kPieces;
+      const int32_t k = 32 * tb + 8 * c;
+      xr[i] = gemm_load<0>(rx, (m < a.rows && k < a.K && tb + c / 4 < t_end)
+                                   ? (uint32_t)m * row_bytes + (uint32_t)k * 2u : kGemmOob);
+    }
+#pragma unroll
+    for (int u = 0; u < KU; ++u)
+      wr[u] = gemm_load<2>(rw, tb + u < t_end ? (uint32_t)(tb + u - t_begin) * 1024u + (uint32_t)lane * 16u
+                                              : kGemmOob);   // streamed once
+  };
+  auto stage = [&](int buf, const u32x4 (&xr)[kXPer]) {
+#pragma unroll
+    for (int i = 0; i < kXPer; ++i) {
+      const int32_t p = tid + kWave * kGemmWaves * i;
+      *reinterpret_cast<u32x4*>(&xs[buf][(p / Lds::kPieces) * Lds::kRow + (p % Lds::kPieces) * 16]) = xr[i];
+    }
+  };
+  auto mult = [&](int buf, const u32x4 (&wr)[KU]) {
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      u32x4 xb[MG];
+#pragma unroll
+      for (int j = 0; j < MG; ++j)
+        xb[j] = *reinterpret_cast<const u32x4*>(&xs[buf][(16 * j + c16) * Lds::kRow + (32 * u + 8 * g4) * 2]);
+#pragma unroll
+      for (int j = 0; j < MG; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(gemm_bf16x8, wr[u]),
+                                                         __builtin_bit_cast(gemm_bf16x8, xb[j]), acc[j], 0, 0, 0);
+    }
+  };
+  // Four register sets: while batch b is multiplied, batches b + 1 .. b + 3
+  // are in flight (every batch's activation loads are issued ahead of its
+  // weight loads, so waiting for activations never waits for weights), and
+  // batch b + 1's activations, issued two batches earlier, go to LDS at the
+  // end of the step.  Batch b's activations are in LDS buffer b & 1.
+  const int32_t n_batch = (t_end - t_begin + KU - 1) / KU;   // the same for the whole workgroup
+  if (n_batch > 0) {
+    u32x4 x0[kXPer], x1[kXPer], x2[kXPer], x3[kXPer], w0[KU], w1[KU], w2[KU], w3[KU];
+    issue(0, x0, w0);
+    issue(1, x1, w1);
+    issue(2, x2, w2);
+    stage(0, x0);
+    __syncthreads();
+#define BATON_GEMM_STEP(S, XN, WN, WC, XS) \
+  issue(b + S + 3, XN, WN);                \
+  __builtin_amdgcn_sched_barrier(0);       \
+  mult((b + S) & 1, WC);                   \
+  stage((b + S + 1) & 1, XS);              \
+  __syncthreads();
+    // A counted loop with no exit inside its body (an exit between the steps
+    // makes the compiler drain every load in flight at the loop head), then
+    // the last n_batch % 4 steps.
+    int32_t b = 0;
+    for (; b + 4 <= n_batch; b += 4) {
+      BATON_GEMM_STEP(0, x3, w3, w0, x1)
+      BATON_GEMM_STEP(1, x0, w0, w1, x2)
+      BATON_GEMM_STEP(2, x1, w1, w2, x3)
+      BATON_GEMM_STEP(3, x2, w2, w3, x0)
+    }
+    if (b < n_batch) {
+      BATON_GEMM_STEP(0, x3, w3, w0, x1)
+      if (b + 1 < n_batch) {
+        BATON_GEMM_STEP(1, x0, w0, w1, x2)
+        if (b + 2 < n_batch) {
+          BATON_GEMM_STEP(2, x1, w1, w2, x3)
+        }
+      }
+    }
+#undef BATON_GEMM_STEP
+  }
+  const int32_t n = n0 + 4 * g4;
+  if (n >= a.N) return;
+#pragma unroll
+  for (int j = 0; j < MG; ++j) {
+    const int32_t m = 16 * j + c16;
+    if (m >= a.rows) continue;
+    if (gridDim.y > 1) {
+      *reinterpret_cast<float4*>(a.part + ((int64_t)blockIdx.y * a.rows + m) * a.N + n) =
+          make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+    } else {
+      uint2* yp = reinterpret_cast<uint2*>(a.y + (int64_t)m * a.N + n);
+      float v0 = acc[j][0], v1 = acc[j][1], v2 = acc[j][2], v3 = acc[j][3];
+      if (a.accumulate) {
+        const uint2 old = *yp;
+        v0 += bf16_lo(old.x); v1 += bf16_hi(old.x); v2 += bf16_lo(old.y); v3 += bf16_hi(old.y);
+      }
+      *yp = make_uint2(pack_bf16(v0, v1), pack_bf16(v2, v3));
+    }
+  }
+}
+
+// y[m][n] (+)= sum over the S splits of part[s][m][n], 4 outputs per thread,
+// the splits added in order.
+__global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* __restrict__ part, uint16_t* __restrict__ y,
+                                                          int32_t S, int64_t n_out, int32_t accumulate) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= n_out) return;
+  float4 v = *reinterpret_cast<const float4*>(part + i);
+  for (int32_t s = 1; s < S; ++s) {
+    const float4 p = *reinterpret_cast<const float4*>(part + s * n_out + i);
+    v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+  }
+  uint2* yp = reinterpret_cast<uint2*>(y + i);
+  if (accumulate) {
+    const uint2 old = *yp;
+    v.x += bf16_lo(old.x); v.y += bf16_hi(old.x); v.z += bf16_lo(old.y); v.w += bf16_hi(old.y);
+  }
+  *yp = make_uint2(pack_bf16(v.x, v.y), pack_bf16(v.z, v.w));
 }
 
 }  // namespace

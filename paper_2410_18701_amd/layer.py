@@ -15,8 +15,16 @@ def _stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+class PackedWeight:
+    """A weight in the packed form baton_linear_packed reads."""
+
+    def __init__(self, data, out_dim, in_dim):
+        self.data, self.out_dim, self.in_dim = data, out_dim, in_dim
+
+
 class Gemm:
-    """A hipBLASLt handle for baton_linear, with a device workspace."""
+    """A hipBLASLt handle for baton_linear, with a device workspace (also the
+    partial sums of baton_linear_packed)."""
 
     def __init__(self, ws_bytes=32 << 20):
         import torch
@@ -34,6 +42,28 @@ class Gemm:
                 raise ValueError("linear: contiguous tensors only")
         B.baton_linear(self.handle, B.BATON_BF16, x, w, y, rows, out_dim, in_dim, accumulate, self.ws,
                        self.ws.numel(), _stream())
+        return y
+
+    def pack(self, w):
+        """The packed form of a weight w [out][in] for linear_packed (made once per weight)."""
+        import torch
+        out_dim, in_dim = w.shape
+        if not w.is_contiguous():
+            raise ValueError("pack: contiguous tensors only")
+        wp = torch.empty(B.baton_linear_packed_bytes(out_dim, in_dim) // 2, dtype=w.dtype, device=w.device)
+        B.baton_linear_pack(B.BATON_BF16, w, wp, out_dim, in_dim, _stream())
+        return PackedWeight(wp, out_dim, in_dim)
+
+    def linear_packed(self, x, wp, y, accumulate=False):
+        """y (+)= x . w^T with w packed by pack(); x [rows <= 64][in], y [rows][out]."""
+        rows, in_dim = x.shape
+        if in_dim != wp.in_dim or tuple(y.shape) != (rows, wp.out_dim):
+            raise ValueError("linear_packed: shapes do not match")
+        for t in (x, y):
+            if not t.is_contiguous():
+                raise ValueError("linear_packed: contiguous tensors only")
+        B.baton_linear_packed(B.BATON_BF16, x, wp.data, y, rows, wp.out_dim, in_dim, accumulate, self.ws,
+                              self.ws.numel(), _stream())
         return y
 
     def close(self):
@@ -72,12 +102,18 @@ class DecodeLayers:
     """The layers of one model over one BatonCache, with preallocated activations.
 
     weights[layer]: dict of bf16 device tensors norm1 [hid], qkv [(Hq + 2 Hkv) D][hid],
-    o [hid][Hq D], norm2 [hid], gate_up [2 F][hid], down [hid][F]."""
+    o [hid][Hq D], norm2 [hid], gate_up [2 F][hid], down [hid][F].  Up to 64 slots
+    the projections run on the weight-streaming GEMM over packed copies of the
+    weights, made here once (packed=False keeps hipBLASLt on the stored weights)."""
 
-    def __init__(self, cache, weights, gemm, theta=10000.0, eps=1e-5):
+    PROJ = ("qkv", "o", "gate_up", "down")
+
+    def __init__(self, cache, weights, gemm, theta=10000.0, eps=1e-5, packed=None):
         import torch
         self.cache, self.w, self.gemm, self.theta, self.eps = cache, weights, gemm, theta, eps
         Bt, Hq, Hkv, D = cache.batch, cache.n_q_heads, cache.n_kv_heads, cache.head_dim
+        self.packed = (Bt <= 64) if packed is None else packed
+        self.wp = [{k: gemm.pack(w[k]) for k in self.PROJ} for w in weights] if self.packed else None
         hid = weights[0]["norm1"].numel()
         F = weights[0]["down"].shape[1]
         e = lambda *s: torch.empty(s, dtype=torch.bfloat16, device="cuda")
@@ -88,13 +124,17 @@ class DecodeLayers:
     def layer(self, layer, x):
         """One layer of the decode step on the residual stream x [batch][hid] (in place)."""
         w = self.w[layer]
+        if self.packed:
+            wp, lin = self.wp[layer], self.gemm.linear_packed
+        else:
+            wp, lin = w, self.gemm.linear
         rmsnorm(x, w["norm1"], self.h, self.eps)
-        self.gemm.linear(self.h, w["qkv"], self.qkv)
+        lin(self.h, wp["qkv"], self.qkv)
         rope_qkv(self.cache, self.qkv, self.q, self.k, self.v, self.theta)
         self.cache.decode_attn(layer, self.q, self.k, self.v, out=self.att)
-        self.gemm.linear(self.att.view(self.att.shape[0], -1), w["o"], x, accumulate=True)
+        lin(self.att.view(self.att.shape[0], -1), wp["o"], x, accumulate=True)
         rmsnorm(x, w["norm2"], self.h, self.eps)
-        self.gemm.linear(self.h, w["gate_up"], self.gu)
+        lin(self.h, wp["gate_up"], self.gu)
         silu_mul(self.gu, self.act)
-        self.gemm.linear(self.act, w["down"], x, accumulate=True)
+        lin(self.act, wp["down"], x, accumulate=True)
         return x

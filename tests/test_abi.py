@@ -112,3 +112,34 @@ def test_host_checks_leave_state_unchanged():
         assert B.baton_decode_attn_workspace_bytes(h) > ws                # more, smaller splits
     finally:
         B.baton_cache_destroy(h)
+
+
+def test_packed_linear_host_checks():
+    """Sizes of the packed weight, and the checks of baton_linear_pack /
+    baton_linear_packed (fake aligned addresses: every call fails before any
+    device work)."""
+    assert B.baton_linear_packed_bytes(4096, 4096) == 4096 * 4096 * 2
+    assert B.baton_linear_packed_bytes(1000, 1000) == 1008 * 1024 * 2   # 16-row slices, 32-column blocks
+    assert B.baton_linear_packed_bytes(0, 64) == 0
+    X, W, Y = 0x10000, 0x20000, 0x30000
+
+    def status(f, *a):
+        try:
+            f(*a)
+        except B.BatonError as e:
+            return e.status
+        return B.BATON_OK
+
+    assert status(B.baton_linear_pack, B.BATON_BF16, 0, W, 64, 64) == B.BATON_EINVAL            # null
+    assert status(B.baton_linear_pack, B.BATON_BF16, X + 8, W, 64, 64) == B.BATON_EINVAL        # misaligned
+    assert status(B.baton_linear_pack, B.BATON_BF16, X, W, 64, 60) == B.BATON_EINVAL            # in % 8
+    assert status(B.baton_linear_pack, B.BATON_F32, X, W, 64, 64) == B.BATON_EDTYPE
+    lp = B.baton_linear_packed
+    assert status(lp, B.BATON_BF16, X, W, Y, 65, 64, 64, 0, 0, 0) == B.BATON_EINVAL           # rows > 64
+    assert status(lp, B.BATON_BF16, X, W, Y, 0, 64, 64, 0, 0, 0) == B.BATON_EINVAL            # rows < 1
+    assert status(lp, B.BATON_BF16, X, W, 0, 8, 64, 64, 0, 0, 0) == B.BATON_EINVAL            # null y
+    assert status(lp, B.BATON_BF16, X, W + 4, Y, 8, 64, 64, 0, 0, 0) == B.BATON_EINVAL        # misaligned
+    assert status(lp, B.BATON_BF16, X, W, Y, 8, 68, 64, 0, 0, 0) == B.BATON_EINVAL            # out % 8
+    assert status(lp, B.BATON_BF16, X, W, Y, 8, 64, 64, 2, 0, 0) == B.BATON_EINVAL            # accumulate
+    assert status(lp, B.BATON_BF16, X, W, Y, 8, 64, 64, 0, 0, 1024) == B.BATON_EINVAL         # ws_bytes, no ws
+    assert status(lp, B.BATON_F32, X, W, Y, 8, 64, 64, 0, 0, 0) == B.BATON_EDTYPE

@@ -44,12 +44,14 @@ def _close(got, want, rel=2.0 ** -7, atol=1e-3, what=""):
     assert np.all(err <= 0), f"{what}: worst excess {err.max():.3g} at {np.unravel_index(err.argmax(), err.shape)}"
 
 
-@pytest.mark.parametrize("rows,out_dim,in_dim", [(1, 64, 64), (5, 520, 136), (64, 4096, 4096), (8, 4096, 11008)])
-def test_linear(rows, out_dim, in_dim):
+@pytest.mark.parametrize("rows,out_dim,in_dim,ws", [(1, 64, 64, 32 << 20), (5, 520, 136, 32 << 20),
+                                                    (64, 4096, 4096, 32 << 20), (8, 4096, 11008, 32 << 20),
+                                                    (100, 256, 512, 32 << 20)])
+def test_linear(rows, out_dim, in_dim, ws):
     rng = np.random.default_rng(rows + out_dim)
     k = round(np.log2(in_dim) / 2)
     xb, wb, yb = _bits(rng, (rows, in_dim)), _bits(rng, (out_dim, in_dim), k), _bits(rng, (rows, out_dim))
-    g = PL.Gemm()
+    g = PL.Gemm(ws_bytes=ws)
     y = torch.empty((rows, out_dim), dtype=torch.bfloat16, device="cuda")
     g.linear(_dev(xb), _dev(wb), y)
     want = LL.linear(O.widen(xb, O.BF16), O.widen(wb, O.BF16))
@@ -57,6 +59,45 @@ def test_linear(rows, out_dim, in_dim):
     y2 = _dev(yb)
     g.linear(_dev(xb), _dev(wb), y2, accumulate=True)
     _close(_val(y2), O.widen(yb, O.BF16) + want, what="linear accumulate")
+    g.close()
+
+
+def _pack_reference(wb):
+    """The packed weight layout written out from its definition (include/baton.h):
+    16-row slices, 1 KB blocks per 32 columns, lane l's 8 elements at 16 l."""
+    N, K = wb.shape
+    S, T = -(-N // 16), -(-K // 32)
+    pad = np.zeros((S * 16, T * 32), wb.dtype)
+    pad[:N, :K] = wb
+    out = np.zeros((S, T, 64, 8), wb.dtype)
+    for lane in range(64):
+        g, r = lane // 16, lane % 16
+        for t in range(T):
+            out[:, t, lane, :] = pad[r::16, 32 * t + 8 * g:32 * t + 8 * g + 8]
+    return out.reshape(-1)
+
+
+# (rows, out_dim, in_dim, workspace bytes): one split along in_dim (many
+# outputs, or no workspace), several splits and their reduction (64 x 4096 x
+# 4096, 8 x 4096 x 11008), a partial 16-row slice and a column tail shorter
+# than 32 (17 x 1000 x 1000), every group of 16 rows.
+@pytest.mark.parametrize("rows,out_dim,in_dim,ws", [
+    (1, 64, 64, 32 << 20), (5, 520, 136, 32 << 20), (64, 4096, 4096, 32 << 20), (8, 4096, 11008, 32 << 20),
+    (17, 1000, 1000, 32 << 20), (33, 12288, 4096, 32 << 20), (64, 4096, 4096, 0), (48, 22016, 4096, 32 << 20)])
+def test_linear_packed(rows, out_dim, in_dim, ws):
+    rng = np.random.default_rng(rows + out_dim + 7)
+    k = round(np.log2(in_dim) / 2)
+    xb, wb, yb = _bits(rng, (rows, in_dim)), _bits(rng, (out_dim, in_dim), k), _bits(rng, (rows, out_dim))
+    g = PL.Gemm(ws_bytes=ws)
+    wp = g.pack(_dev(wb))
+    assert np.array_equal(parity.host_bits(wp.data), _pack_reference(wb)), "packed layout"
+    y = torch.empty((rows, out_dim), dtype=torch.bfloat16, device="cuda")
+    g.linear_packed(_dev(xb), wp, y)
+    want = LL.linear(O.widen(xb, O.BF16), O.widen(wb, O.BF16))
+    _close(_val(y), want, what="linear_packed")
+    y2 = _dev(yb)
+    g.linear_packed(_dev(xb), wp, y2, accumulate=True)
+    _close(_val(y2), O.widen(yb, O.BF16) + want, what="linear_packed accumulate")
     g.close()
 
 
@@ -102,7 +143,7 @@ def test_rope_at_token_counts():
     cache.close()
 
 
-def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128):
+def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128, packed=None):
     """GPU layers and the oracle in lockstep; returns the worst relative excess."""
     w = Workload("layer", "bf16", NL, B, m.n_q_heads, m.n_kv_heads, m.head_dim, 1, 0, seed=seed)
     dev = driver.DeviceInputs(w)
@@ -111,7 +152,7 @@ def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128):
     wd = [M.weights_device(seed, m, l) for l in range(NL)]
     wh = [M.weights_host(seed, m, l) for l in range(NL)]
     gemm = PL.Gemm()
-    layers = PL.DecodeLayers(cache, wd, gemm, m.theta, m.eps)
+    layers = PL.DecodeLayers(cache, wd, gemm, m.theta, m.eps, packed=packed)
     step = 0
     for op in steps_ops:
         if op[0] == "embed":
@@ -147,11 +188,12 @@ def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128):
     cache.close()
 
 
-def test_layers_small_model():
+@pytest.mark.parametrize("packed", [True, False], ids=["packed", "hipblaslt"])
+def test_layers_small_model(packed):
     m = M.ModelShape(256, 4, 2, 64, 512)
     ops = [("embed", [0, 1, 2], [9, 30, 4], [0, 1, 2]), ("step",), ("step",),
            ("evict", [1]), ("embed", [3, 1], [12, 40], [3, 4]), ("step",), ("evict", [0]), ("step",)]
-    _run_layers(m, 2, 4, ops)
+    _run_layers(m, 2, 4, ops, packed=packed)
 
 
 def test_layers_llama2_7b_shape():
