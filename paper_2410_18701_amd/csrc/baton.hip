@@ -707,11 +707,16 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     p.batch = c->d.batch;
     p.n_kv_heads = c->d.n_kv_heads;
     p.qscale = a.qscale;
+    // the prefilled queries, longest prompt first (their longest tiles are dealt first)
     for (int32_t b = 0; b < c->d.batch; ++b)
       if (c->plen[b] > 0) {
-        p.slot[p.n_ins] = b;
-        p.plen[p.n_ins] = c->plen[b];
-        ++p.n_ins;
+        int32_t i = p.n_ins++;
+        for (; i > 0 && p.plen[i - 1] < c->plen[b]; --i) {
+          p.slot[i] = p.slot[i - 1];
+          p.plen[i] = p.plen[i - 1];
+        }
+        p.slot[i] = b;
+        p.plen[i] = c->plen[b];
       }
     if (c->d.head_dim == 64) launch_prefill_d<64>(c, p, stream);
     else launch_prefill_d<128>(c, p, stream);

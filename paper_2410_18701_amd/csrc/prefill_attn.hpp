@@ -42,26 +42,24 @@ struct PrefillArgs {
 };
 
 // The work of this workgroup: query head hq, prefilled query ins, tile.  The
-// grid is one-dimensional, n_tiles per query head.  Workgroups are dealt to
-// the XCDs round-robin by index, and each XCD has its own L2; with xcd_map the
-// index is decoded so that all workgroups reading one kv-head's keys (a unit:
-// its G query heads x all tiles) run on the same XCD.  Within a query head a
-// prefilled query's tiles are handed out last first (the last positions see
-// the most keys).
+// grid is one-dimensional over n_tiles x query heads, tile-major: all query
+// heads of one tile are dealt before the next tile, and the tiles run from
+// the longest (a query's last positions, which see the most keys; the queries
+// are ordered by prompt length, longest first) to the shortest, so that the
+// workgroups that start last are short.  Workgroups are dealt to the XCDs
+// round-robin by index, and each XCD has its own L2; with xcd_map the heads
+// are numbered so that all workgroups reading one kv-head's keys (a unit: its
+// G query heads) run on the same XCD.
 __device__ __forceinline__ void prefill_work(const PrefillArgs& a, int& hq, int32_t& ins,
                                              int32_t& tile) {
-  const int32_t L = blockIdx.x;
-  int32_t g;
+  const int32_t nq = (int32_t)(gridDim.x / a.n_tiles);   // query heads
+  const int32_t g = blockIdx.x / nq, j = blockIdx.x % nq;
   if (a.xcd_map) {
-    const int32_t xcd = L % 8, k = L / 8;
-    const int32_t per_unit = a.n_tiles * a.unit_heads;
-    const int32_t u = xcd + 8 * (k / per_unit);
-    const int32_t r = k % per_unit;
-    hq = u * a.unit_heads + r / a.n_tiles;
-    g = r % a.n_tiles;
+    const int32_t xcd = j % 8, k = j / 8;
+    const int32_t u = xcd + 8 * (k / a.unit_heads);
+    hq = u * a.unit_heads + k % a.unit_heads;
   } else {
-    hq = L / a.n_tiles;
-    g = L % a.n_tiles;
+    hq = j;
   }
   ins = 0;
   while (ins < a.n_ins - 1 && g >= a.tile_end[ins]) ++ins;
