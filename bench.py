@@ -342,6 +342,35 @@ def copy_probe(nbytes, reps=5):
             "GB/s": round(2 * nbytes / t / 1e9, 1)}
 
 
+def read_probe(nbytes, reps=5):
+    """A read-only stream of nbytes (the workload library's reference kernel:
+    64 KiB per workgroup, 16-byte non-temporal loads): what plain reads reach
+    on this GPU, the practical ceiling of a read-dominated kernel such as
+    decode attention."""
+    import ctypes
+    import torch
+    from workload import gen
+    lib = gen.dev_lib()
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    launch = lambda: lib.wl_device_read_stream(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                               ctypes.c_void_p(flag.data_ptr()), stream)
+    if launch() != 0:
+        raise RuntimeError("wl_device_read_stream failed")
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        launch()
+    b.record()
+    torch.cuda.synchronize()
+    t = a.elapsed_time(b) * 1e-3 / reps
+    del buf, flag
+    return {"bytes_per_launch": nbytes, "avg_launch_us": round(t * 1e6, 2), "GB/s": round(nbytes / t / 1e9, 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -368,6 +397,7 @@ def main():
         print(json.dumps(bench_model(args, w)), flush=True)
         return
     copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
+    read_ref = read_probe(2 * args.copy_bytes) if args.copy_bytes > 0 else None
     cache, inputs = driver.open_cache(w, split=args.split)
     cap = cache.capacity
 
@@ -505,7 +535,10 @@ def main():
             "build_mask": {"ms_per_step": round(mask_ms / args.steps, 4)},
         },
         "hbm_copy_reference": copy_ref,
+        "hbm_read_reference": read_ref,
     }
+    if read_ref:
+        result["roofline"]["frac_of_read_reference"] = round(attn_gbs / read_ref["GB/s"], 4)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
     print(json.dumps(result), flush=True)

@@ -35,9 +35,42 @@ __global__ void __launch_bounds__(256) wl_fill_kernel(uint64_t key, void* __rest
   }
 }
 
+// Read-only HBM stream: each workgroup reads one 64 KiB chunk with 16-byte
+// non-temporal loads, eight in flight per thread, and folds them so the loads
+// are kept; the flag is written only if the fold hits a fixed value.  A
+// measurement reference for the bandwidth plain reads reach, not a step of
+// the method.
+typedef uint32_t wl_u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ void __launch_bounds__(256) wl_read_kernel(const wl_u32x4* __restrict__ buf, uint32_t* flag) {
+  const wl_u32x4* chunk = buf + (int64_t)blockIdx.x * 4096;
+  uint32_t x = 0;
+  for (int i = threadIdx.x; i < 4096; i += 256 * 8) {
+    wl_u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(chunk + i + 256 * u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  if (x == 0x9E3779B9u) flag[0] = x;
+}
+
 }  // namespace
 
 extern "C" {
+
+// Enqueues one read of `bytes` (a multiple of 64 KiB) of device memory buf
+// (16-byte aligned); flag: one device uint32 the kernel may write.  Returns
+// 0, -1 on bad arguments, or the hipError_t.
+int wl_device_read_stream(const void* buf, int64_t bytes, uint32_t* flag, hipStream_t stream) {
+  if (!buf || !flag || bytes <= 0 || bytes % 65536 || (reinterpret_cast<uintptr_t>(buf) & 15) ||
+      bytes / 65536 > 0x7FFFFFFF)
+    return -1;
+  hipLaunchKernelGGL(wl_read_kernel, dim3((unsigned)(bytes / 65536)), dim3(256), 0, stream,
+                     static_cast<const wl_u32x4*>(buf), flag);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : (int)e;
+}
 
 // Device twin of wl_host_fill: out is device memory laid out [n0][n1][n2][n3].
 // Enqueued on `stream`; returns 0, -1 on bad arguments, or the hipError_t.

@@ -181,6 +181,8 @@ def dev_lib():
             raise RuntimeError(f"{DEV_LIB} is missing: run workload/build.py")
         lib = ctypes.CDLL(DEV_LIB)
         u64, i64 = ctypes.c_uint64, ctypes.c_int64
+        lib.wl_device_read_stream.restype = ctypes.c_int
+        lib.wl_device_read_stream.argtypes = [ctypes.c_void_p, i64, ctypes.c_void_p, ctypes.c_void_p]
         lib.wl_device_fill.restype = ctypes.c_int
         lib.wl_device_fill.argtypes = [u64, ctypes.c_int, ctypes.c_void_p, i64, i64, i64, i64,
                                        u64, u64, u64, u64, u64, ctypes.c_void_p]
