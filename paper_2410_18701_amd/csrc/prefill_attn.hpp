@@ -160,12 +160,16 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 //    wave's 16 positions; the score of key 4*(l/16) + r (first 16 keys) and
 //    16 + 4*(l/16) + r (next 16) for position l % 16 lands in lane l,
 //    register r.
-//  * PV: A = P with k = 8*(l/16) + e standing for key 4*(l/16) + e (e < 4)
-//    and 16 + 4*(l/16) + e - 4 (e >= 4); B = V rows in that order, read with
-//    the LDS transpose load (ds_read_b64_tr_b16): within a group of 16 lanes,
+//  * PV, transposed: O^T = V^T P^T.  B = P^T with k = 8*(l/16) + e standing
+//    for key 4*(l/16) + e (e < 4) and 16 + 4*(l/16) + e - 4 (e >= 4) -- the
+//    lane's own scores, in place; A = V^T in that key order, read with the
+//    LDS transpose load (ds_read_b64_tr_b16): within a group of 16 lanes,
 //    lane i receives element i % 4 of the 8-byte block addressed by lane
 //    i / 4 + 4e, for e = 0..3; lane m of group g addresses key 4g + m / 4 at
-//    columns 16*dt + 4*(m % 4), so lane i gets V[4g + e][16*dt + i].
+//    columns 16*dt + 4*(m % 4), so lane i gets V[4g + e][16*dt + i].  Lane l
+//    then holds output columns 16*dt + 4*(l/16) + r of position l % 16: a
+//    position's rescale and normalisation stay in its own lanes, and the
+//    max and sum over the four lane groups use the gfx950 row swaps.
 // Rows are padded to 8 dwords past a multiple of 32, so that the 16 rows of a
 // transpose load spread over all banks.
 #ifndef BATON_PREFILL_KT
@@ -173,6 +177,26 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 #endif
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Reductions over the four lane groups of 16 (lanes l, l ^ 16, l ^ 32, l ^ 48)
+// with the gfx950 row swaps: each swap hands every lane its own value and its
+// partner's, without a trip through LDS.
+__device__ __forceinline__ float max_over_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(x);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum_over_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t v = __float_as_uint(x);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 __device__ __forceinline__ s16x4 lds_read_tr16(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -269,8 +293,7 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
       float mx = s[0];
 #pragma unroll
       for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      mx = max_over_groups(mx);
       const float mn = fmaxf(m, mx);
       const float ref = mn == -INFINITY ? 0.f : mn;
       // exponents are <= 0 here: the hardware exp2 (results below the
@@ -286,15 +309,11 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
       }
       lsum = lsum * alpha + psum;
       m = mn;
-      // Rescale the accumulators only when some position's maximum moved
-      // (after the first keys it rarely does).
+      // Rescale the accumulators (this lane's position's own factor) only when
+      // some position's maximum moved (after the first keys it rarely does).
       if (__ballot(alpha != 1.f)) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float ar = __shfl(alpha, 4 * g4 + r, kWave);
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt][r] *= ar;
-        }
+        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
       }
       const uint8_t* vblk = ldsV + kb * ROW + tr_off;
 #pragma unroll
@@ -303,7 +322,7 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
         const s16x4 hi = lds_read_tr16(vblk + 16 * ROW + dt * 32);
         const s16x4 w2[2] = {lo, hi};
         const bf16x8 vb = __builtin_bit_cast(bf16x8, w2);
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pa, o[dt], 0, 0, 0);
       }
     }
   };
@@ -347,28 +366,23 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
         lsum = lsum * fa + src[1] * fb;
         m = mm;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float far = __shfl(fa, 4 * g4 + r, kWave);
-          const float fbr = __shfl(fb, 4 * g4 + r, kWave);
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt][r] = o[dt][r] * far + src[2 + dt * 4 + r] * fbr;
-        }
+          for (int dt = 0; dt < DT; ++dt) o[dt][r] = o[dt][r] * fa + src[2 + dt * 4 + r] * fb;
       }
     }
   }
   if (ks == 0) {
-    lsum += __shfl_xor(lsum, 16, kWave);
-    lsum += __shfl_xor(lsum, 32, kWave);
+    // Lane l holds columns 16 dt + 4 (l / 16) + r of position l % 16.
+    lsum = sum_over_groups(lsum);
+    if (qi < p) {
+      const float inv = 1.f / lsum;
+      uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + qi) * nq + hq) * D + 4 * g4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qr = 4 * g4 + r;
-      const float lr = __shfl(lsum, qr, kWave);
-      if (i0 + qr < p) {
-        const float inv = 1.f / lr;
-        uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + i0 + qr) * nq + hq) * D;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o16[16 * dt + c16] = (uint16_t)f32_to_bf16_rne(o[dt][r] * inv);
-      }
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<uint2*>(o16 + 16 * dt) =
+            make_uint2(f32_to_bf16_rne(o[dt][0] * inv) | (f32_to_bf16_rne(o[dt][1] * inv) << 16),
+                       f32_to_bf16_rne(o[dt][2] * inv) | (f32_to_bf16_rne(o[dt][3] * inv) << 16));
     }
   }
   if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, wg0, min(64, p - wg0), tid, NT);
