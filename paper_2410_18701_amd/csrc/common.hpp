@@ -107,6 +107,26 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// Reductions over the four lane groups of 16 (lanes l, l ^ 16, l ^ 32, l ^ 48)
+// with the gfx950 row swaps: each swap hands every lane its own value and its
+// partner's, without a trip through LDS.
+__device__ __forceinline__ float max_over_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(x);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum_over_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t v = __float_as_uint(x);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Ring column arithmetic: a + b mod cap for 0 <= a, b < cap.
 __device__ __forceinline__ int64_t ring_add(int64_t a, int64_t b, int64_t cap) {
   const int64_t s = a + b;

@@ -11,9 +11,11 @@
 //  * softmax: lane l holds head l%16's scores of 8 tokens; the running max is
 //    shared by the four lane groups (all of them accumulate into the same
 //    output tile), exponentials are base 2, P is rounded to bf16.
-//  * PV: A = P (16 heads x 32 tokens, lane l: head l%16, its own 8 tokens as
-//    k = 8*(l/16) + e), B = V (32 tokens x 16 d) per 16-column slice of
-//    head_dim.  V is staged in LDS row by row (coalesced global loads) and read
+//  * PV, transposed (O^T = V^T P^T): B = P^T (32 tokens x 16 heads, lane l:
+//    head l%16, its own 8 tokens as k = 8*(l/16) + e), A = V^T (16 d x 32
+//    tokens) per 16-column slice of head_dim, so lane l accumulates output
+//    columns 16*dt + 4*(l/16) + r of head l%16 and rescales with its own
+//    factor.  V is staged in LDS row by row (coalesced global loads) and read
 //    back transposed, 2 bytes per lane; the token order above makes the four
 //    lane groups of one read hit consecutive rows, i.e. disjoint banks.
 // The current token (k_new, v_new) is a one-token tile of its own.  As in the
@@ -76,8 +78,7 @@ __device__ __forceinline__ void mfma_block(const u32x4 (&kA)[D / 32], const u32x
   float mx = s[0];
 #pragma unroll
   for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
-  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  mx = max_over_groups(mx);
   const float mn = fmaxf(m, mx);
   const float ref = mn == -INFINITY ? 0.f : mn;
   const float alpha = exp2f(m - ref);
@@ -91,14 +92,12 @@ __device__ __forceinline__ void mfma_block(const u32x4 (&kA)[D / 32], const u32x
   }
   lsum = lsum * alpha + psum;
   m = mn;
-  // Rescale the output rows this lane holds (heads 4*g4 + r).
+  // Rescale the output column this lane holds (head c16).
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float ar = __shfl(alpha, 4 * g4 + r, kWave);
-#pragma unroll
-    for (int dt = 0; dt < Geo::kDt; ++dt) o[dt][r] *= ar;
-  }
-  // PV: B operand = V[token(k)][16*dt + c16], k = 8*g4 + e.
+  for (int dt = 0; dt < Geo::kDt; ++dt) o[dt] *= alpha;
+  // PV, transposed: A = V^T (row 16*dt + c16, keys token(k), k = 8*g4 + e),
+  // B = P^T (this lane's own probabilities); lane l accumulates output
+  // columns 16*dt + 4*g4 + r of head c16.
 #pragma unroll
   for (int dt = 0; dt < Geo::kDt; ++dt) {
     bf16x8 vb;
@@ -107,7 +106,7 @@ __device__ __forceinline__ void mfma_block(const u32x4 (&kA)[D / 32], const u32x
       const int t = e < 4 ? g4 + 4 * e : 16 + g4 + 4 * (e - 4);
       vb[e] = *reinterpret_cast<const __bf16*>(lds + t * Geo::kLdsRow + (16 * dt + c16) * 2);
     }
-    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pa, o[dt], 0, 0, 0);
   }
 }
 
@@ -219,21 +218,18 @@ attn_mfma_kernel(const AttnArgs a) {
     }
   }
 
-  // Row sums over the four lane groups; lane l's output rows are heads
-  // 4*g4 + r.  The wave's state goes to LDS for the workgroup's merge.
-  lsum += __shfl_xor(lsum, 16, kWave);
-  lsum += __shfl_xor(lsum, 32, kWave);
+  // Sums over the four lane groups; lane l holds output columns
+  // 16*dt + 4*g4 + r of head c16.  The wave's state goes to LDS for the
+  // workgroup's merge.
+  lsum = sum_over_groups(lsum);
+  if (c16 < G) {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int head = 4 * g4 + r;
-    const float lr = __shfl(lsum, head, kWave);
-    const float mr = __shfl(m, head, kWave);
-    if (head >= G) continue;
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) sm_acc[w][head][16 * dt + c16] = o[dt][r];
-    if (c16 == 0) {
-      sm_m[w][head] = mr;
-      sm_l[w][head] = lr;
+      for (int r = 0; r < 4; ++r) sm_acc[w][c16][16 * dt + 4 * g4 + r] = o[dt][r];
+    if (g4 == 0) {
+      sm_m[w][c16] = m;
+      sm_l[w][c16] = lsum;
     }
   }
   __syncthreads();

@@ -178,26 +178,6 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-// Reductions over the four lane groups of 16 (lanes l, l ^ 16, l ^ 32, l ^ 48)
-// with the gfx950 row swaps: each swap hands every lane its own value and its
-// partner's, without a trip through LDS.
-__device__ __forceinline__ float max_over_groups(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const uint32_t v = __float_as_uint(x);
-  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-__device__ __forceinline__ float sum_over_groups(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const uint32_t v = __float_as_uint(x);
-  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
 __device__ __forceinline__ s16x4 lds_read_tr16(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (__attribute__((address_space(3))) s16x4*)(__attribute__((address_space(3))) void*)(p));
