@@ -6,7 +6,7 @@ embed the newly prefilled queries end-aligned (growing the batch on the left
 when one is longer), build the mask, then masked decode attention layer by
 layer (appending each layer's new key/value column), then advance.
 
-Default workload (config 3): bf16, 32 layers x 32 heads x head_dim 128
+Default workload (7b-b64-L4096): bf16, 32 layers x 32 heads x head_dim 128
 (7B-shaped attention), batch 64, initial padded length 4096, lengths
 lognormal(6.5, 0.8) clipped to [32, 4096], Poisson(4) arrivals per step with
 as many queries finishing, 64 decode steps (warmup + timed).  All inputs are
@@ -28,6 +28,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
+DEFAULT_WORKLOAD = "7b-b64-L4096"
+GQA_WORKLOAD = "70b-gqa-b128-L8192"   # 80 layers' padded cache exceed HBM: a resident subset
 
 
 def parse():
@@ -35,7 +37,9 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=60)
     p.add_argument("--warmup", type=int, default=4)
-    p.add_argument("--config", default="cfg3", choices=["cfg2", "cfg3", "cfg4", "cfg5", "cfg5b"])
+    p.add_argument("--config", default=DEFAULT_WORKLOAD,
+                   choices=["b32-L2048", "7b-b64-L4096", "70b-gqa-b128-L8192", "skew-b256-L32768",
+                            "skew-growth-b256-L32768"])
     p.add_argument("--layers", type=int, default=None,
                    help="resident layers (config 4's 80-layer padded cache exceeds HBM; default 24 there)")
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
@@ -48,7 +52,7 @@ def parse():
     p.add_argument("--cpu-layers", type=int, default=20, help="layers of step 0 the oracle runs")
     p.add_argument("--copy-bytes", type=int, default=2 << 30,
                    help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
-    p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "decode_attn_cfg3_traffic.json"),
+    p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "decode_attn_7b_b64_L4096_traffic.json"),
                    help="rocprofv3-derived HBM bytes per decode_attn launch (FETCH_SIZE/WRITE_SIZE, "
                         "scaled by a copy of known size); used only for the workload it was measured "
                         "on and while the kernel sources are unchanged")
@@ -190,7 +194,8 @@ def bench_model(args, w):
 
     m = M.LLAMA2_7B
     if (w.n_q_heads, w.n_kv_heads, w.head_dim) != (m.n_q_heads, m.n_kv_heads, m.head_dim):
-        raise SystemExit("--model llama2-7b needs a workload with 32 heads of 128 (cfg2, cfg3, cfg5)")
+        raise SystemExit("--model llama2-7b needs a workload with 32 heads of 128 (b32-L2048, 7b-b64-L4096, "
+                         "skew-b256-L32768)")
     cache, inputs = driver.open_cache(w, split=args.split)
     weights = [M.weights_device(w.seed, m, l) for l in range(w.n_layers)]
     wbytes = sum(t.numel() * 2 for lw in weights for t in lw.values())
@@ -384,12 +389,12 @@ def main():
 
     torch.cuda.set_device(0)
     total_steps = args.warmup + args.steps
-    if args.config == "cfg4":
-        w = configs.cfg4(total_steps, n_layers=args.layers or 24)
+    if args.config == GQA_WORKLOAD:
+        w = configs.gqa70b_b128_l8192(total_steps, n_layers=args.layers or 24)
     else:
         w = configs.CONFIGS[args.config](total_steps)
         if args.layers:
-            raise SystemExit("--layers applies to cfg4 only")
+            raise SystemExit(f"--layers applies to {GQA_WORKLOAD} only")
     if args.no_pd:
         print(json.dumps(bench_no_pd(args, w)), flush=True)
         return
@@ -488,7 +493,7 @@ def main():
     value = live_tokens / (total_ms * 1e-3)
 
     traffic = None
-    if args.traffic and os.path.exists(args.traffic) and args.config == "cfg3" and args.split is None \
+    if args.traffic and os.path.exists(args.traffic) and args.config == DEFAULT_WORKLOAD and args.split is None \
             and (args.steps, args.warmup) == (60, 4):
         with open(args.traffic) as f:
             rec = json.load(f)

@@ -9,7 +9,7 @@ pytestmark = pytest.mark.gpu
 
 SMALL = {
     # fp32, the tiny configuration: 4 slots, 4 heads, D=64, L=128, one insert into slot 2
-    "tiny-f32": (configs.tiny(), {}),
+    "tiny-f32": (configs.tiny_f32(), {}),
     # MHA bf16 D=128, rows spanning three 256-token splits, ragged tails
     "mha-bf16-d128": (configs.small("bf16", 2, 6, 8, 8, 128, L0=600, n_steps=4, n_evict=2, seed=31), {}),
     # GQA 4:1, bf16 D=128

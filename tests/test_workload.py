@@ -78,11 +78,11 @@ def test_schedule_is_valid(name):
 
 
 def test_config_laws():
-    w = configs.cfg5()
+    w = configs.skew_b256_l32768()
     longs = [n for n in w.init_lens if n > 1024]
     assert len(longs) == round(0.1 * w.batch)
     assert all(16384 <= n <= 32768 for n in longs)
-    w3 = configs.cfg3()
+    w3 = configs.llama7b_b64_l4096()
     assert all(32 <= n <= 4096 for n in w3.init_lens)
     ins = [n for e in w3.steps for n in e.insert_lens]
     assert 2.0 < len(ins) / w3.n_steps < 6.5          # Poisson(4) arrivals

@@ -10,7 +10,7 @@ query id (prefill K/V) or from (step, layer, slot, head) (decode inputs).
 The paper evaluates on two simulated query sets it did not release (long-in /
 short-out, short-in / long-out and short/short queries of a few dozen to about
 4,000 words).  These workloads stand in for them: the length laws cover the
-same spans, and config 3 has the attention shape of the 7B model it serves
+same spans, and 7b-b64-L4096 has the attention shape of the 7B model it serves
 (32 layers x 32 heads x 128).
 """
 import math
@@ -134,43 +134,43 @@ def _schedule(w: Workload, n_evict, new_len, d: Draws):
     return w
 
 
-def tiny():
+def tiny_f32():
     """fp32, 1 layer, B=4, 4 heads, D=64, L=128; one EOS in slot 2 replaced by a 40-token query."""
-    w = Workload("tiny", "f32", 1, 4, 4, 4, 64, 128, 1, seed=1001)
+    w = Workload("tiny-f32", "f32", 1, 4, 4, 4, 64, 128, 1, seed=1001)
     d = Draws(w.seed, gen.S_LENS)
     w.init_lens = _pin_max([d.randint(16, 128) for _ in range(w.batch)], w.L0)
     w.steps = [StepEvents(evict=[2], insert=[2], insert_lens=[40], insert_qids=[w.batch])]
     return w
 
 
-def cfg2(n_steps=16):
+def b32_l2048(n_steps=16):
     """bf16, 1 layer, B=32, 32 heads, D=128, L=2048; 2 EOS + 2 inserts of U[64,1024] per step."""
-    w = Workload("cfg2", "bf16", 1, 32, 32, 32, 128, 2048, n_steps, seed=1002)
+    w = Workload("b32-L2048", "bf16", 1, 32, 32, 32, 128, 2048, n_steps, seed=1002)
     d = Draws(w.seed, gen.S_LENS)
     w.init_lens = _pin_max([d.randint(128, 2048) for _ in range(w.batch)], w.L0)
     return _schedule(w, lambda _d: 2, lambda e: e.randint(64, 1024), Draws(w.seed, gen.S_EVENTS))
 
 
-def cfg3(n_steps=64):
+def llama7b_b64_l4096(n_steps=64):
     """bf16, 32 layers x 32 heads x 128 (7B-shaped), B=64, L=4096; lognormal lengths, Poisson(4) arrivals."""
-    w = Workload("cfg3", "bf16", 32, 64, 32, 32, 128, 4096, n_steps, seed=1003)
+    w = Workload("7b-b64-L4096", "bf16", 32, 64, 32, 32, 128, 4096, n_steps, seed=1003)
     d = Draws(w.seed, gen.S_LENS)
     w.init_lens = _pin_max([d.lognormal_int(6.5, 0.8, 32, 4096) for _ in range(w.batch)], w.L0)
     return _schedule(w, lambda e: e.poisson(4.0), lambda e: e.lognormal_int(6.5, 0.8, 32, 4096),
                      Draws(w.seed, gen.S_EVENTS))
 
 
-def cfg4(n_steps=16, n_layers=80):
+def gqa70b_b128_l8192(n_steps=16, n_layers=80):
     """bf16, GQA 64 q-heads / 8 KV heads, D=128, 80 layers, B=128, L=8192; 8 EOS + 8 inserts per step."""
-    w = Workload("cfg4", "bf16", n_layers, 128, 64, 8, 128, 8192, n_steps, seed=1004)
+    w = Workload("70b-gqa-b128-L8192", "bf16", n_layers, 128, 64, 8, 128, 8192, n_steps, seed=1004)
     d = Draws(w.seed, gen.S_LENS)
     w.init_lens = _pin_max([d.randint(256, 8192) for _ in range(w.batch)], w.L0)
     return _schedule(w, lambda _d: 8, lambda e: e.randint(256, 8192), Draws(w.seed, gen.S_EVENTS))
 
 
-def cfg5(n_steps=16):
+def skew_b256_l32768(n_steps=16):
     """Long-skew: bf16, 1 layer, B=256, 32 heads, D=128, L=32768; 90% U[64,1024], 10% U[16384,32768]."""
-    w = Workload("cfg5", "bf16", 1, 256, 32, 32, 128, 32768, n_steps, seed=1005)
+    w = Workload("skew-b256-L32768", "bf16", 1, 256, 32, 32, 128, 32768, n_steps, seed=1005)
     d = Draws(w.seed, gen.S_LENS)
     n_long = round(0.1 * w.batch)
     long_rows = set(d.sample(range(w.batch), n_long))
@@ -180,11 +180,11 @@ def cfg5(n_steps=16):
     return _schedule(w, lambda _d: 4, lambda e: e.randint(64, 16384), Draws(w.seed, gen.S_EVENTS))
 
 
-def cfg5b(n_steps=16):
+def skew_growth_b256_l32768(n_steps=16):
     """Long-skew growth variant: the long rows finish at step 0, then each step inserts a query
     longer than the padded length (1024 + s*960 tokens), so every insert grows the batch."""
-    w = cfg5(0)
-    w.name, w.n_steps = "cfg5b", n_steps + 1
+    w = skew_b256_l32768(0)
+    w.name, w.n_steps = "skew-growth-b256-L32768", n_steps + 1
     d = Draws(w.seed, gen.S_EVENTS)
     long_rows = [b for b in range(w.batch) if w.init_lens[b] > 1024]
     next_qid = w.batch
@@ -212,5 +212,7 @@ def small(dtype="bf16", n_layers=2, batch=5, n_q_heads=4, n_kv_heads=2, head_dim
     return _schedule(w, lambda _d: n_evict, lambda e: e.randint(1, nh), Draws(seed, gen.S_EVENTS))
 
 
-CONFIGS = {"tiny": tiny, "cfg1": tiny, "cfg2": cfg2, "cfg3": cfg3, "cfg4": cfg4, "cfg5": cfg5,
-           "cfg5b": cfg5b}
+# The workloads by name (the name each builds its Workload with).
+CONFIGS = {"tiny-f32": tiny_f32, "b32-L2048": b32_l2048, "7b-b64-L4096": llama7b_b64_l4096,
+           "70b-gqa-b128-L8192": gqa70b_b128_l8192, "skew-b256-L32768": skew_b256_l32768,
+           "skew-growth-b256-L32768": skew_growth_b256_l32768}
