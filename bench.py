@@ -41,7 +41,7 @@ def parse():
                    choices=["b32-L2048", "7b-b64-L4096", "70b-gqa-b128-L8192", "skew-b256-L32768",
                             "skew-growth-b256-L32768"])
     p.add_argument("--layers", type=int, default=None,
-                   help="resident layers (config 4's 80-layer padded cache exceeds HBM; default 24 there)")
+                   help="resident layers (70b-gqa-b128-L8192's 80-layer padded cache exceeds HBM; default 24 there)")
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
     p.add_argument("--no-pd", action="store_true",
                    help="prefill the new queries inside the batch (no prefill/decode separation) "

@@ -135,7 +135,7 @@ __global__ void __launch_bounds__(256) fill_kernel(u32x4* __restrict__ k, u32x4*
 // The step's mask, mask[b * ld + j] for j in [0, L + T): a live row (span n)
 // is 1 on [L - n, L] outside its holes, a row prefilled this step (prompt p)
 // on [L + T - p, L + T), a free row nowhere.  One block row per slot, 4 bytes
-// per thread.
+// per thread (one 4-byte store where the row allows it).
 struct MaskArgs {
   uint8_t* mask;
   int64_t ld, L;
@@ -160,17 +160,32 @@ __global__ void __launch_bounds__(256) mask_kernel(const MaskArgs a) {
     lo = hi = 0;
   }
   const int k0 = n > 0 ? a.first[b] : a.holes.n;
+  const int nh = a.holes.n;
   uint8_t* row = a.mask + (int64_t)b * a.ld;
   for (int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; j0 < W;
        j0 += (int64_t)gridDim.x * blockDim.x * 4) {
+    // The row's holes are sorted and disjoint: the first one ending past j0,
+    // by bisection, then forward as j advances.
+    int k = k0, k_hi = nh;
+    while (k < k_hi) {
+      const int mid = (k + k_hi) / 2;
+      if (a.holes.col[mid][1] <= j0) k = mid + 1;
+      else k_hi = mid;
+    }
+    uint32_t word = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int64_t j = j0 + e;
-      if (j >= W) break;
-      bool one = j >= lo && j < hi;
-      for (int k = k0; one && k < a.holes.n; ++k)
-        one = !(j >= a.holes.col[k][0] && j < a.holes.col[k][1]);
-      row[j] = (uint8_t)one;
+      while (k < nh && a.holes.col[k][1] <= j) ++k;
+      const bool one = j >= lo && j < hi && !(k < nh && j >= a.holes.col[k][0]);
+      word |= (uint32_t)one << (8 * e);
+    }
+    if (j0 + 4 <= W && (reinterpret_cast<uintptr_t>(row + j0) & 3) == 0) {
+      *reinterpret_cast<uint32_t*>(row + j0) = word;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j0 + e < W) row[j0 + e] = (uint8_t)(word >> (8 * e));
     }
   }
 }
