@@ -19,6 +19,7 @@ timed on a bounded sample on this host.
 import argparse
 import gc
 import json
+import math
 import os
 import sys
 import time
@@ -172,9 +173,11 @@ def bench_no_pd(args, w):
         "ops": {
             "prefill_steps": {"layer_calls": len(ev_pf), "ms_per_call": round(pf_ms / max(1, len(ev_pf)), 4),
                               "prompt_tokens": prompt_tokens,
+                              "call_ms": quantiles([x.elapsed_time(y) for x, y in ev_pf]),
                               "prefill_TFLOP/s (calls incl. decode rows)":
                                   round(flops_pf / (pf_ms * 1e-3) / 1e12, 2) if pf_ms else None},
             "decode_steps": {"layer_calls": len(ev_dec), "ms_per_call": round(dec_ms / max(1, len(ev_dec)), 4),
+                             "call_ms": quantiles([x.elapsed_time(y) for x, y in ev_dec]),
                              "GB/s": round(bytes_dec / (dec_ms * 1e-3) / 1e9, 1) if dec_ms else None},
             "final_padded_length": L,
         },
@@ -261,6 +264,7 @@ def bench_model(args, w):
                                f"{m.hidden}, ffn {m.ffn}, batch {w.batch}, initial padded length {w.L0}",
                    "global_batch": w.batch, "seq_len": w.L0, "parallelism": "none (1 GPU)"},
         "ops": {"layer": {"ms_per_call": round(layer_ms / len(ev_layer), 4),
+                          "call_ms": quantiles([a.elapsed_time(b) for a, b in ev_layer]),
                           "weight_bytes_per_layer": int(per_layer_w)},
                 "weights_GB": round(wbytes / 1e9, 2)},
     }
@@ -347,33 +351,59 @@ def copy_probe(nbytes, reps=5):
             "GB/s": round(2 * nbytes / t / 1e9, 1)}
 
 
-def read_probe(nbytes, reps=5):
+def quantiles(xs):
+    """Median and 90th percentile (nearest rank) of a list of timings."""
+    ys = sorted(xs)
+    if not ys:
+        return None
+    rank = lambda q: ys[min(len(ys) - 1, max(0, int(math.ceil(q * len(ys))) - 1))]
+    return {"median": round(rank(0.5), 4), "p90": round(rank(0.9), 4), "n": len(ys)}
+
+
+def read_probe(nbytes, reps=5, per_launch=False, n_bufs=1):
     """A read-only stream of nbytes (the workload library's reference kernel:
     64 KiB per workgroup, 16-byte non-temporal loads): what plain reads reach
     on this GPU, the practical ceiling of a read-dominated kernel such as
-    decode attention."""
+    decode attention.  per_launch: each launch timed between its own events
+    (as the attention calls are), over n_bufs buffers in turn so that no
+    launch finds its bytes in the last-level cache; otherwise reps launches
+    back to back between two events."""
     import ctypes
     import torch
     from workload import gen
     lib = gen.dev_lib()
-    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    buf.fill_(1)
+    nbytes = max(65536, nbytes // 65536 * 65536)
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(n_bufs)]
+    for buf in bufs:
+        buf.fill_(1)
     flag = torch.zeros(1, dtype=torch.int32, device="cuda")
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    launch = lambda: lib.wl_device_read_stream(ctypes.c_void_p(buf.data_ptr()), nbytes,
-                                               ctypes.c_void_p(flag.data_ptr()), stream)
-    if launch() != 0:
-        raise RuntimeError("wl_device_read_stream failed")
+    launch = lambda i: lib.wl_device_read_stream(ctypes.c_void_p(bufs[i % n_bufs].data_ptr()), nbytes,
+                                                 ctypes.c_void_p(flag.data_ptr()), stream)
+    for i in range(n_bufs):
+        if launch(i) != 0:
+            raise RuntimeError("wl_device_read_stream failed")
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
-        launch()
-    b.record()
-    torch.cuda.synchronize()
-    t = a.elapsed_time(b) * 1e-3 / reps
-    del buf, flag
-    return {"bytes_per_launch": nbytes, "avg_launch_us": round(t * 1e6, 2), "GB/s": round(nbytes / t / 1e9, 1)}
+    if per_launch:
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for i, (a, b) in enumerate(evs):
+            a.record()
+            launch(i)
+            b.record()
+        torch.cuda.synchronize()
+        t = sum(a.elapsed_time(b) for a, b in evs) * 1e-3 / reps
+    else:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(reps):
+            launch(i)
+        b.record()
+        torch.cuda.synchronize()
+        t = a.elapsed_time(b) * 1e-3 / reps
+    del bufs, flag
+    return {"bytes_per_launch": nbytes, "avg_launch_us": round(t * 1e6, 2), "GB/s": round(nbytes / t / 1e9, 1),
+            "timing": "per launch" if per_launch else "back to back"}
 
 
 def main():
@@ -438,7 +468,7 @@ def main():
     torch.cuda.synchronize()
     pool_it = iter(pool)
     E = lambda: next(pool_it)
-    ev_attn, ev_embed, ev_evict, ev_mask = [], [], [], []
+    ev_attn, ev_embed, ev_evict, ev_mask, ev_step = [], [], [], [], []
     bytes_attn = bytes_embed = bytes_evict = 0
     live_tokens = 0
     gc.collect()
@@ -478,6 +508,7 @@ def main():
             b.record()
             ev_attn.append((a, b))
             bytes_attn += step_attn
+        ev_step.append((ev_evict[-1][0], ev_attn[-1][1]))
         live_tokens += sum(1 for n in lens if n > 0)
         cache.advance()
     t_end.record()
@@ -539,11 +570,19 @@ def main():
             "kv_evict": {"ms_per_step": round(evict_ms / args.steps, 4)},
             "build_mask": {"ms_per_step": round(mask_ms / args.steps, 4)},
         },
+        "per_step_ms": quantiles([x.elapsed_time(y) for x, y in ev_step]),
+        "decode_attn_call_us": quantiles([x.elapsed_time(y) * 1e3 for x, y in ev_attn]),
         "hbm_copy_reference": copy_ref,
         "hbm_read_reference": read_ref,
     }
     if read_ref:
         result["roofline"]["frac_of_read_reference"] = round(attn_gbs / read_ref["GB/s"], 4)
+        # The same read at the attention's own bytes per call, each launch
+        # timed alone as the calls are: what a single launch of that size
+        # loses to filling and draining the GPU is in both.
+        read_same = read_probe(round(bytes_attn / n_attn), reps=32, per_launch=True, n_bufs=4)
+        result["hbm_read_reference_same_size"] = read_same
+        result["roofline"]["frac_of_read_reference_same_size"] = round(attn_gbs / read_same["GB/s"], 4)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
     print(json.dumps(result), flush=True)
