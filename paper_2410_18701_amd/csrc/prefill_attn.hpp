@@ -263,29 +263,41 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
         sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka), qb[kk], sa, 0, 0, 0);
         sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc), qb[kk], sb, 0, 0, 0);
       }
-      const int32_t lim = qi < p ? qi - tt : -1;       // keys tt .. tt + lim are visible
+      // Unscaled scores; masked keys -inf.  A block whose 32 keys all come
+      // before the wave's first position is visible to every position of the
+      // wave and needs no mask (positions past the prompt are never written).
       float s[8];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        s[r] = 4 * g4 + r <= lim ? sa[r] * a.qscale : -INFINITY;
-        s[4 + r] = 16 + 4 * g4 + r <= lim ? sb[r] * a.qscale : -INFINITY;
+        s[r] = sa[r];
+        s[4 + r] = sb[r];
+      }
+      if (tt + 31 > i0) {                              // wave-uniform
+        const int32_t lim = qi < p ? qi - tt : -1;     // keys tt .. tt + lim are visible
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          s[r] = 4 * g4 + r <= lim ? s[r] : -INFINITY;
+          s[4 + r] = 16 + 4 * g4 + r <= lim ? s[4 + r] : -INFINITY;
+        }
       }
       float mx = s[0];
 #pragma unroll
       for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
-      mx = max_over_groups(mx);
+      mx = max_over_groups(mx) * a.qscale;             // qscale > 0: the max of the scaled scores
       const float mn = fmaxf(m, mx);
       const float ref = mn == -INFINITY ? 0.f : mn;
       // exponents are <= 0 here: the hardware exp2 (results below the
-      // smallest normal flush to 0, which a softmax weight may)
+      // smallest normal flush to 0, which a softmax weight may); the scale is
+      // applied in the exponent's multiply-add, the sum taken before P is
+      // rounded to bf16 for the matrix operation
       const float alpha = __builtin_amdgcn_exp2f(m - ref);
       bf16x8 pa;
       float psum = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const __bf16 pb = (__bf16)__builtin_amdgcn_exp2f(s[e] - ref);
-        pa[e] = pb;
-        psum += (float)pb;
+        const float pf = __builtin_amdgcn_exp2f(fmaf(s[e], a.qscale, -ref));
+        pa[e] = (__bf16)pf;
+        psum += pf;
       }
       lsum = lsum * alpha + psum;
       m = mn;
