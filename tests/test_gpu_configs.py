@@ -33,7 +33,7 @@ def test_sampled(name, steps, layers, kw):
 
 
 def test_70b_gqa_resident_layers():
-    """Config 4's per-layer shape (GQA 64/8, B=128, L=8192) with 24 of its 80
+    """70b-gqa-b128-L8192's per-layer shape (GQA 64/8, B=128, L=8192) with 24 of its 80
     layers resident -- the dense padded 80-layer cache (343.6 GB) exceeds HBM."""
     w = configs.gqa70b_b128_l8192(n_steps=6, n_layers=24)
     print(f"[configs] 70b-gqa-b128-L8192 24 layers sampled", flush=True)
@@ -42,7 +42,7 @@ def test_70b_gqa_resident_layers():
 
 
 def test_b32_l2048_no_pd_sampled():
-    """Config 2's schedule without prefill/decode separation, as bench.py --no-pd
+    """b32-L2048's schedule without prefill/decode separation, as bench.py --no-pd
     runs it (2 + 16 steps, every step prefilling two queries inside the batch)."""
     w = configs.b32_l2048(18)
     print(f"[configs] b32-L2048 no-P&D sampled: capacity {w.capacity_no_pd()}", flush=True)
