@@ -29,7 +29,8 @@ class baton_cache_desc(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("batch", ctypes.c_int32),
                 ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("capacity", ctypes.c_int64),
-                ("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("fill_bits", ctypes.c_uint32)]
+                ("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("fill_bits", ctypes.c_uint32),
+                ("layer_stride", ctypes.c_int64)]
 
 
 class BatonError(RuntimeError):

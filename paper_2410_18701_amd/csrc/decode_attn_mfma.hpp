@@ -145,7 +145,7 @@ attn_mfma_kernel(const AttnArgs a) {
   }
   int32_t t_begin, t_end;            // this wave's share of the item's tokens
   wave_share<NW, 32>(it.y, it.z, w, t_begin, t_end);
-  const int64_t row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
+  const int64_t row = (int64_t)b * a.n_kv_heads + h;   // within the layer's rows
   constexpr uint32_t ROWB = VPT * 16;
   const uint32_t ring_bytes = (uint32_t)a.cap * ROWB;
   const __amdgpu_buffer_rsrc_t rk =

@@ -23,6 +23,7 @@ struct SegArgs {
   uint32_t* k;              // ring buffers, viewed as 32-bit words
   uint32_t* v;
   int64_t cap;              // ring columns
+  int64_t layer_vec;        // 16-byte vectors from one layer's rows to the next layer's
   int32_t n_layers, batch, n_kv_heads;
   int32_t n_segs;
   int32_t extract;          // 1: ring -> ext, 0: ext (or placeholder) -> ring, 2: ring row -> ring row
@@ -59,8 +60,8 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
   const int32_t t0 = tile * TT;
   const int32_t nt = min(TT, len - t0);
 
-  u32x4* ring = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
-               (((int64_t)layer * a.batch + a.slot[i]) * a.n_kv_heads + h) * a.cap * VPT;
+  u32x4* ring = reinterpret_cast<u32x4*>(which ? a.v : a.k) + layer * a.layer_vec +
+               ((int64_t)a.slot[i] * a.n_kv_heads + h) * a.cap * VPT;
   u32x4* ext = reinterpret_cast<u32x4*>(which ? a.vext[i] : a.kext[i]);
   if (ext) ext += (((int64_t)layer * a.n_kv_heads + h) * a.ext_len[i] + a.ext_t0[i] + t0) * VPT;
   const int64_t c0 = ring_add(a.col0[i], t0, a.cap);
@@ -68,8 +69,8 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
   u32x4 val[kCopyVecs];
   const u32x4 fill = {a.fill_word, a.fill_word, a.fill_word, a.fill_word};
   if (a.extract == 2) {     // the same ring columns of another slot's row
-    u32x4* dst = reinterpret_cast<u32x4*>(which ? a.v : a.k) +
-                 (((int64_t)layer * a.batch + a.dst_slot[i]) * a.n_kv_heads + h) * a.cap * VPT;
+    u32x4* dst = reinterpret_cast<u32x4*>(which ? a.v : a.k) + layer * a.layer_vec +
+                 ((int64_t)a.dst_slot[i] * a.n_kv_heads + h) * a.cap * VPT;
 #pragma unroll
     for (int r = 0; r < kCopyVecs; ++r) {
       const int idx = threadIdx.x + r * kCopyThreads;
@@ -121,14 +122,21 @@ __global__ void __launch_bounds__(kCopyThreads) seg_kernel(const SegArgs a) {
   }
 }
 
-// Writes the placeholder over n_vec 16-byte vectors of each of K and V.
+// Writes the placeholder over the n_vec 16-byte vectors of every layer's rows
+// of K and V (layer l at k + l * layer_vec, v + l * layer_vec); blockIdx.y
+// walks the layers.
 __global__ void __launch_bounds__(256) fill_kernel(u32x4* __restrict__ k, u32x4* __restrict__ v,
-                                                   int64_t n_vec, uint32_t fill_word) {
+                                                   int32_t n_layers, int64_t layer_vec, int64_t n_vec,
+                                                   uint32_t fill_word) {
   const u32x4 fill = {fill_word, fill_word, fill_word, fill_word};
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_vec; i += stride) {
-    __builtin_nontemporal_store(fill, k + i);
-    __builtin_nontemporal_store(fill, v + i);
+  for (int32_t layer = blockIdx.y; layer < n_layers; layer += gridDim.y) {
+    u32x4* kl = k + layer * layer_vec;
+    u32x4* vl = v + layer * layer_vec;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_vec; i += stride) {
+      __builtin_nontemporal_store(fill, kl + i);
+      __builtin_nontemporal_store(fill, vl + i);
+    }
   }
 }
 

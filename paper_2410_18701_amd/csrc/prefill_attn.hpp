@@ -24,14 +24,14 @@ namespace baton {
 constexpr int kMaxPrefill = 64;   // == BATON_MAX_PREFILL
 
 struct PrefillArgs {
-  uint32_t* k;              // ring buffers (appended to)
+  uint32_t* k;              // the layer's ring rows [batch][n_kv_heads][cap][D] (appended to)
   uint32_t* v;
   const uint32_t* q;        // [batch][T][n_q_heads][D]
   const uint32_t* knew;     // [batch][T][n_kv_heads][D]
   const uint32_t* vnew;
   uint32_t* out;            // [batch][T][n_q_heads][D]
   int64_t cap, base, L;
-  int32_t T, layer, batch, n_kv_heads, n_ins;
+  int32_t T, batch, n_kv_heads, n_ins;
   int32_t n_tiles;          // tiles over all prefilled queries (per query head)
   int32_t unit_heads;       // query heads that read the same keys (G), or 1
   int32_t xcd_map;          // 1: keep each unit's workgroups on one XCD (units % 8 == 0)
@@ -71,7 +71,7 @@ template <int VPT>
 __device__ __forceinline__ void prefill_append(const PrefillArgs& a, int b, int h, int32_t p,
                                                int64_t row0, int32_t t0, int32_t n, int tid,
                                                int nthr = kWave) {
-  const int64_t ring_row = ((int64_t)a.layer * a.batch + b) * a.n_kv_heads + h;
+  const int64_t ring_row = (int64_t)b * a.n_kv_heads + h;   // within the layer's rows
   u32x4* rk = reinterpret_cast<u32x4*>(a.k) + ring_row * a.cap * VPT;
   u32x4* rv = reinterpret_cast<u32x4*>(a.v) + ring_row * a.cap * VPT;
   const u32x4* kin = reinterpret_cast<const u32x4*>(a.knew);

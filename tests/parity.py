@@ -61,11 +61,11 @@ def max_err(gpu_out, oracle_out, dtype):
     return float(np.max(np.abs(got - oracle_out))) if got.size else 0.0
 
 
-def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale=0.0):
+def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale=0.0, layout="by_layer"):
     """Drive the whole schedule; returns the largest attention error seen."""
     cache = driver.BatonCache(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
                               w.capacity() if capacity is None else capacity, dtype=w.dtype,
-                              fill_bits=fill_bits)
+                              fill_bits=fill_bits, layout=layout)
     if split is not None:
         cache.set_split_tokens(split)
     dev = driver.DeviceInputs(w)
@@ -346,7 +346,7 @@ def run_sampled_no_pd(w, sample_steps, sample_layers=(0,), n_slots=4, n_pos=6, h
 
 
 # ---------------------------------------------------------- scripted mode --
-def run_script(shape, ops, seed=3, capacity=64, split=None):
+def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer"):
     """A scripted sequence on a small batch, GPU and materialized oracle in
     lockstep, everything compared after every operation.
 
@@ -365,7 +365,7 @@ def run_script(shape, ops, seed=3, capacity=64, split=None):
     dtype, NL, B, Hq, Hkv, D = shape
     from workload.configs import Workload
     w = Workload("script", dtype, NL, B, Hq, Hkv, D, 1, 0, seed=seed)
-    cache = driver.BatonCache(NL, B, Hq, Hkv, D, capacity, dtype=dtype)
+    cache = driver.BatonCache(NL, B, Hq, Hkv, D, capacity, dtype=dtype, layout=layout)
     if split is not None:
         cache.set_split_tokens(split)
     dev = driver.DeviceInputs(w)

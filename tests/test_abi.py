@@ -33,7 +33,7 @@ def test_status_strings():
     assert B.baton_status_string(99) == "unknown status"
 
 
-FAKE_K, FAKE_V = 0x10000, 0x20000   # never dereferenced: every call below fails host checks
+FAKE_K, FAKE_V = 0x10000, 0x10000000   # never dereferenced: every call below fails host checks
 
 
 def desc(**kw):
@@ -48,11 +48,26 @@ def desc(**kw):
     (dict(n_q_heads=6, n_kv_heads=4), B.BATON_EDTYPE), (dict(n_q_heads=32, n_kv_heads=2), B.BATON_EDTYPE),
     (dict(batch=0), B.BATON_EINVAL), (dict(batch=513), B.BATON_EINVAL), (dict(capacity=1), B.BATON_EINVAL),
     (dict(n_layers=0), B.BATON_EINVAL), (dict(k=0), B.BATON_EINVAL), (dict(v=FAKE_V + 8), B.BATON_EINVAL),
+    # one layer's rows are 4 x 2 x 300 x 128 elements (307,200 = 614,400 bytes)
+    (dict(layer_stride=307200 - 8), B.BATON_EINVAL),                   # below one layer
+    (dict(layer_stride=307200 + 4), B.BATON_EINVAL),                   # 8 bytes: not whole vectors
+    (dict(v=FAKE_K + 16), B.BATON_EINVAL),                             # overlaps k
+    (dict(v=FAKE_K + 614400, layer_stride=2 * 307200 - 8), B.BATON_EINVAL),   # interleaved, overlapping
 ])
 def test_create_rejects(kw, status):
     with pytest.raises(B.BatonError) as e:
         B.baton_cache_create(desc(**kw), B.BATON_CREATE_ASSUME_FILLED)
     assert e.value.status == status
+
+
+@pytest.mark.parametrize("kw", [
+    dict(v=FAKE_K + 614400, layer_stride=2 * 307200),        # [n_layers][2][...]: v after k's layer
+    dict(v=FAKE_K + 614400 * 4, layer_stride=2 * 307200),    # v after the whole of k
+    dict(v=FAKE_K + 2 * 614400),                               # packed, v right after k
+    dict(layer_stride=307200),                                 # packed, stride given
+])
+def test_create_accepts_layouts(kw):
+    B.baton_cache_destroy(B.baton_cache_create(desc(**kw), B.BATON_CREATE_ASSUME_FILLED))
 
 
 def test_host_checks_leave_state_unchanged():

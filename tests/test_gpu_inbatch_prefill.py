@@ -63,6 +63,15 @@ def test_golden_story(shape):
     print(f"[inbatch golden] {shape}: max abs error {err:.3g}", flush=True)
 
 
+@pytest.mark.parametrize("shape", [s for s in SHAPES if s[1] > 1], ids=_sid)
+def test_random_sequences_separate_buffers(shape):
+    """Prefill steps with K and V in two allocations of their own (packed layers)."""
+    dtype, NL, B, Hq, Hkv, D = shape
+    ops = _random_ops(7, B, steps=10, max_len=70)
+    err = parity.run_script(shape, ops, capacity=2048, split=64, layout="separate")
+    print(f"[inbatch random] {shape} separate buffers: {len(ops)} ops, max abs error {err:.3g}", flush=True)
+
+
 @pytest.mark.parametrize("shape", SHAPES, ids=_sid)
 @pytest.mark.parametrize("seed", [0, 1])
 def test_random_sequences(shape, seed):

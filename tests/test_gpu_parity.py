@@ -36,6 +36,16 @@ def test_schedule_parity(name):
     print(f"[parity] {name}: max abs error {err:.3g}", flush=True)
 
 
+@pytest.mark.parametrize("name", ["tiny-f32", "mha-bf16-d128", "gqa8-bf16-d128-split64", "gqa2-f32-d128-split64"])
+def test_schedule_parity_separate_buffers(name):
+    """The same schedules with K and V in two allocations of their own (packed
+    layers) instead of one allocation interleaved by layer."""
+    w, kw = SMALL[name]
+    print(f"[parity] {name} separate buffers: {w.name}", flush=True)
+    err = parity.run(w, layout="separate", **kw)
+    print(f"[parity] {name} separate buffers: max abs error {err:.3g}", flush=True)
+
+
 def test_ring_wraparound_tight_capacity():
     """Capacity = the most the run can need: releases and growths move the window
     base across the end of the ring again and again."""
