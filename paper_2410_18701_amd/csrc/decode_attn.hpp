@@ -289,13 +289,14 @@ __device__ __forceinline__ void work_unit(const AttnArgs& a, int32_t& item, int3
 
 // Merge of the NW waves of a workgroup, each holding the online-softmax state
 // of its share of the item's tokens for the G query heads: wave w has put its
-// max, sum and accumulator into sm_m[w][gi], sm_l[w][gi], sm_acc[w][gi][D]
-// (a wave with no tokens: max -inf, sum 0).  Every thread of the workgroup
+// max, sum and accumulator into sm_m[w][gi], sm_l[w][gi] and the G x D floats
+// at sm_acc + w * acc_stride ([gi][d]; a wave with no tokens: max -inf, sum
+// 0).  Every thread of the workgroup
 // then merges pairs of output elements with the log-sum-exp rescale and writes
 // the item's output (the item is its row's only one) or its partial record.
 template <typename T, int D, int G, int NW>
 __device__ __forceinline__ void wg_merge_write(const float (&sm_m)[NW][G], const float (&sm_l)[NW][G],
-                                               const float (&sm_acc)[NW][G][D], bool whole_row,
+                                               const float* sm_acc, int acc_stride, bool whole_row,
                                                uint32_t* outw, float* rec0, int tid) {
   constexpr int REC = D + 4;
   for (int p = tid; p < G * D / 2; p += NW * kWave) {
@@ -309,8 +310,8 @@ __device__ __forceinline__ void wg_merge_write(const float (&sm_m)[NW][G], const
       const float mw = sm_m[w][gi];
       const float f = mw == -INFINITY ? 0.f : exp2f(mw - mm);
       l = fmaf(f, sm_l[w][gi], l);
-      o0 = fmaf(f, sm_acc[w][gi][e], o0);
-      o1 = fmaf(f, sm_acc[w][gi][e + 1], o1);
+      o0 = fmaf(f, sm_acc[w * acc_stride + gi * D + e], o0);
+      o1 = fmaf(f, sm_acc[w * acc_stride + gi * D + e + 1], o1);
     }
     if (whole_row) {
       const float inv = 1.f / l;
@@ -494,7 +495,7 @@ attn_kernel(const AttnArgs a) {
   }
   __syncthreads();
   float* rec0 = a.partial + (((int64_t)h * a.n_items + item) * G) * REC;
-  wg_merge_write<T, D, G, NW>(sm_m, sm_l, sm_acc, whole_row, outw, rec0, tid);
+  wg_merge_write<T, D, G, NW>(sm_m, sm_l, &sm_acc[0][0][0], G * D, whole_row, outw, rec0, tid);
 }
 
 // One wave per (row with several items, query head): the log-sum-exp merge
