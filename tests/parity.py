@@ -61,11 +61,29 @@ def max_err(gpu_out, oracle_out, dtype):
     return float(np.max(np.abs(got - oracle_out))) if got.size else 0.0
 
 
+def padded_kv(n_layers, batch, n_kv_heads, capacity, head_dim, dtype, pad=4096 + 16):
+    """K and V as [n_layers][batch][n_kv_heads][capacity][head_dim] views of two
+    buffers whose layers are `pad` elements longer than their rows (a layer
+    stride the library is told, not a packed one); the padding is filled with
+    a marker that the tests check is never written."""
+    per = batch * n_kv_heads * capacity * head_dim
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    bufs = [torch.full((n_layers, per + pad), 7.0, dtype=tdt, device="cuda") for _ in range(2)]
+    views = [b[:, :per].view(n_layers, batch, n_kv_heads, capacity, head_dim) for b in bufs]
+    return views[0], views[1], lambda: all(bool((b[:, per:] == 7.0).all()) for b in bufs)
+
+
 def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale=0.0, layout="by_layer"):
     """Drive the whole schedule; returns the largest attention error seen."""
-    cache = driver.BatonCache(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim,
-                              w.capacity() if capacity is None else capacity, dtype=w.dtype,
-                              fill_bits=fill_bits, layout=layout)
+    cap = w.capacity() if capacity is None else capacity
+    if layout == "padded":
+        # two allocations whose layers are 4096 + 16 elements apart beyond their rows
+        k, v, padding_intact = padded_kv(w.n_layers, w.batch, w.n_kv_heads, cap, w.head_dim, w.dtype)
+        cache = driver.BatonCache(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, cap,
+                                  dtype=w.dtype, fill_bits=fill_bits, k=k, v=v)
+    else:
+        cache = driver.BatonCache(w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, cap,
+                                  dtype=w.dtype, fill_bits=fill_bits, layout=layout)
     if split is not None:
         cache.set_split_tokens(split)
     dev = driver.DeviceInputs(w)
@@ -121,6 +139,9 @@ def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale
         pb.advance()
         if check_every_op or s == len(w.steps) - 1:
             check_ring(cache, pb, f"step {s} advance")
+    if layout == "padded":
+        torch.cuda.synchronize()
+        assert padding_intact(), "a write landed in the padding between layers"
     cache.close()
     return worst
 

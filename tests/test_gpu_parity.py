@@ -46,6 +46,16 @@ def test_schedule_parity_separate_buffers(name):
     print(f"[parity] {name} separate buffers: max abs error {err:.3g}", flush=True)
 
 
+@pytest.mark.parametrize("name", ["mha-bf16-d128", "gqa2-f32-d128-split64"])
+def test_schedule_parity_padded_layer_stride(name):
+    """K and V with a layer stride beyond their rows (padding between layers):
+    results as above, and the padding is never written."""
+    w, kw = SMALL[name]
+    print(f"[parity] {name} padded layer stride: {w.name}", flush=True)
+    err = parity.run(w, layout="padded", **kw)
+    print(f"[parity] {name} padded layer stride: max abs error {err:.3g}", flush=True)
+
+
 def test_ring_wraparound_tight_capacity():
     """Capacity = the most the run can need: releases and growths move the window
     base across the end of the ring again and again."""
