@@ -385,9 +385,15 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   // One layer's rows, [batch][n_kv_heads][capacity][head_dim], are dense; the
   // layers are layer_stride elements apart (0: packed), a whole number of
   // 16-byte vectors, and K's and V's layers must not overlap.
-  const int64_t layer_elems = (int64_t)d.batch * d.n_kv_heads * d.capacity * d.head_dim;
+  // Sizes are bounded first so that the byte arithmetic below cannot
+  // overflow: K (and V) must span less than 2^56 bytes.
+  const __int128 layer_elems_w = (__int128)d.batch * d.n_kv_heads * d.capacity * d.head_dim;
+  if (d.layer_stride < 0 || layer_elems_w * esz >= ((__int128)1 << 56)) return BATON_EINVAL;
+  const int64_t layer_elems = (int64_t)layer_elems_w;
   const int64_t stride = d.layer_stride == 0 ? layer_elems : d.layer_stride;
-  if (stride < layer_elems || (stride * esz) % 16) return BATON_EINVAL;
+  if (stride < layer_elems || (__int128)stride * esz * d.n_layers >= ((__int128)1 << 56) ||
+      (stride * esz) % 16)
+    return BATON_EINVAL;
   {
     const int64_t lb = layer_elems * esz, sb = stride * esz;
     const int64_t span = (int64_t)(d.n_layers - 1) * sb + lb;   // bytes from k to its last row's end

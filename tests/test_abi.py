@@ -53,6 +53,9 @@ def desc(**kw):
     (dict(layer_stride=307200 + 4), B.BATON_EINVAL),                   # 8 bytes: not whole vectors
     (dict(v=FAKE_K + 16), B.BATON_EINVAL),                             # overlaps k
     (dict(v=FAKE_K + 614400, layer_stride=2 * 307200 - 8), B.BATON_EINVAL),   # interleaved, overlapping
+    (dict(layer_stride=-307200), B.BATON_EINVAL),                      # negative
+    (dict(layer_stride=1 << 60), B.BATON_EINVAL),                      # spans beyond any memory
+    (dict(n_kv_heads=1 << 30, n_q_heads=1 << 30), B.BATON_EINVAL),     # rows beyond any memory
 ])
 def test_create_rejects(kw, status):
     with pytest.raises(B.BatonError) as e:
