@@ -53,9 +53,11 @@ struct baton_cache {
   int64_t L = 0;           // padded length
   int64_t base = 0;        // physical column of logical column 0
   std::vector<int32_t> lens;
-  // Placeholder writes still owed by evictions: pending[s] tokens of slot s,
-  // ending at ring column base + L (which neither release nor growth moves).
-  std::vector<int32_t> pending;
+  // Placeholder writes still owed by evictions: per slot, the runs [a0, a1)
+  // of absolute columns its finished query's tokens occupied (its holes are
+  // placeholders already).  Absolute column a lies at ring column
+  // base + L - vend + a, which neither release, growth nor a step moves.
+  std::vector<std::vector<std::pair<int64_t, int64_t>>> owed;
   std::vector<uint8_t> layer_done;
   int32_t n_done = 0;      // layers decoded in the current step
   // Columns appended since creation; the absolute column of logical column L.
@@ -334,17 +336,42 @@ int32_t auto_split(const baton_cache* c) {
   return (int32_t)std::min(kAutoSplitMax, std::max(kAutoSplitMin, s));
 }
 
+// Ring column of absolute column a.
+int64_t abs_ring(const baton_cache* c, int64_t a) {
+  return ring(c->base + c->L - c->vend + a, c->d.capacity);
+}
+
+// Slot b's finished query is owed placeholders: the runs of its tokens
+// (its span [L - len, L) without its holes), in absolute columns.
+void owe_row(baton_cache* c, int32_t b) {
+  const baton::HoleList hl = hole_list(c);
+  const int32_t len = c->lens[b];
+  const int64_t a_row = c->vend - len;   // absolute column of the row's first token
+  auto& o = c->owed[b];
+  baton::row_runs(hl, first_hole(c, b), c->L, len, [&](int32_t t0, int32_t t1) {
+    t1 = std::min(t1, len);   // the current column holds no token yet
+    if (t1 > t0) o.push_back({a_row + t0, a_row + t1});
+  });
+}
+
+// The placeholder writes slot b owes over absolute columns below `limit`
+// (the rest is about to be overwritten), one segment per run.
+void owed_segs(const baton_cache* c, int32_t b, int64_t limit, std::vector<Seg>& segs) {
+  for (const auto& r : c->owed[b]) {
+    const int64_t a1 = std::min(r.second, limit);
+    if (a1 > r.first)
+      segs.push_back({b, (int32_t)(a1 - r.first), abs_ring(c, r.first), nullptr, nullptr});
+  }
+}
+
 // Enqueues the placeholder writes evictions still owe.
 baton_status flush_pending(baton_cache* c, hipStream_t stream) {
-  const int64_t end = ring(c->base + c->L, c->d.capacity);
   std::vector<Seg> segs;
-  for (int32_t b = 0; b < c->d.batch; ++b)
-    if (c->pending[b] > 0)
-      segs.push_back({b, c->pending[b], ring(end - c->pending[b], c->d.capacity), nullptr, nullptr});
+  for (int32_t b = 0; b < c->d.batch; ++b) owed_segs(c, b, INT64_MAX, segs);
   if (segs.empty()) return BATON_OK;
   const baton_status st = launch_segs(c, segs, stream);
   if (st != BATON_OK) return st;
-  std::fill(c->pending.begin(), c->pending.end(), 0);
+  for (auto& o : c->owed) o.clear();
   return BATON_OK;
 }
 
@@ -412,7 +439,7 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
   c->group = g;
   c->split = 0;
   c->lens.assign(d.batch, 0);
-  c->pending.assign(d.batch, 0);
+  c->owed.assign(d.batch, {});
   c->epoch.assign(d.batch, 0);
   c->plen.assign(d.batch, 0);
   c->layer_done.assign(d.n_layers, 0);
@@ -455,7 +482,7 @@ baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uin
   // which skips the columns its own query overwrites, or to the next step.
   (void)stream;
   for (int32_t i = 0; i < n; ++i) {
-    c->pending[slots[i]] = c->lens[slots[i]];
+    owe_row(c, slots[i]);
     c->lens[slots[i]] = 0;
   }
   if (flags & BATON_RELEASE) {
@@ -493,16 +520,14 @@ baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, con
   // the ring, which holds placeholders in every row already.
   const int64_t base_new = ring(c->base - (L_new - c->L), c->d.capacity);
   // One launch: each query's copy, and the placeholders its slot still owes
-  // over the columns in front of the new query (both end at base + L).
-  const int64_t end = ring(c->base + c->L, c->d.capacity);
+  // in front of the new query (the query ends at absolute column vend, and
+  // overwrites whatever is owed behind that).
   std::vector<Seg> segs;
   segs.reserve(2 * n);
   for (int32_t i = 0; i < n; ++i) {
     segs.push_back({slots[i], lens[i], ring(base_new + L_new - lens[i], c->d.capacity), k_src[i],
                     v_src[i]});
-    const int32_t owed = c->pending[slots[i]];
-    if (owed > lens[i])
-      segs.push_back({slots[i], owed - lens[i], ring(end - owed, c->d.capacity), nullptr, nullptr});
+    owed_segs(c, slots[i], c->vend - lens[i], segs);
   }
   const baton_status st = launch_segs(c, segs, stream);
   if (st != BATON_OK) return st;
@@ -510,7 +535,7 @@ baton_status baton_kv_embed(baton_cache* c, const int32_t* slots, int32_t n, con
   c->L = L_new;
   for (int32_t i = 0; i < n; ++i) {
     c->lens[slots[i]] = lens[i];
-    c->pending[slots[i]] = 0;
+    c->owed[slots[i]].clear();
     c->epoch[slots[i]] = c->next_hole;   // no earlier hole lies in its row
   }
   c->meta_valid = false;
@@ -575,18 +600,17 @@ baton_status baton_kv_move(baton_cache* c, const int32_t* src, const int32_t* ds
     Seg g{src[i], len, ring(end - len, c->d.capacity), nullptr, nullptr};
     g.dst_slot = dst[i];
     copies.push_back(g);
-    const int32_t owed = c->pending[dst[i]];
-    if (owed > len) fills.push_back({dst[i], owed - len, ring(end - owed, c->d.capacity), nullptr, nullptr});
+    owed_segs(c, dst[i], c->vend - len, fills);
   }
   baton_status st = launch_segs(c, copies, stream, /*mode=*/2);
   if (st == BATON_OK && !fills.empty()) st = launch_segs(c, fills, stream);
   if (st != BATON_OK) return st;
   for (int32_t i = 0; i < n; ++i) {
     const int32_t s = src[i], d = dst[i];
+    c->owed[d].clear();
+    owe_row(c, s);   // the source's tokens are owed placeholders now
     c->lens[d] = c->lens[s];
     c->epoch[d] = c->epoch[s];
-    c->pending[d] = 0;
-    c->pending[s] = c->lens[s];   // the source's tokens are owed placeholders now
     c->lens[s] = 0;
   }
   c->meta_valid = false;
