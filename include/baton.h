@@ -129,7 +129,8 @@ baton_status baton_cache_destroy(baton_cache* cache);
  * paragraphs: the finished query's cached keys/values are overwritten with the
  * placeholder and its mask row zeroed).  slots: host array of n distinct live
  * slot indices (n may be 0); the slots become free.  The placeholder write over
- * each finished query's tokens (every layer and head) is owed, not enqueued
+ * each finished query's tokens (every layer and head; the holes of its row
+ * hold placeholders already and are skipped) is owed, not enqueued
  * here: the next baton_kv_embed into the slot performs it over the columns in
  * front of its new query (the new query overwrites the rest), and the first
  * baton_decode_attn of the next step, or baton_cache_flush, performs whatever
