@@ -367,7 +367,7 @@ def run_sampled_no_pd(w, sample_steps, sample_layers=(0,), n_slots=4, n_pos=6, h
 
 
 # ---------------------------------------------------------- scripted mode --
-def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer"):
+def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", log=None):
     """A scripted sequence on a small batch, GPU and materialized oracle in
     lockstep, everything compared after every operation.
 
@@ -380,6 +380,9 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer"):
       ("move", src, dst)             live queries change slots
       ("step", s)                    mask, every layer with step-s inputs, advance
       ("flush",)                     the placeholder writes evictions still owe
+      ("scale", max_cells)           BatchScaler.shrink then grow at this threshold (the
+                                     oracle repeats its parks and returns; `log` gets
+                                     ("scale", parked slots, returned slots))
     After a step or a flush the whole ring is compared; after the other
     operations the live rows (evicted rows may still hold old tokens).
     """
@@ -392,6 +395,7 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer"):
     dev = driver.DeviceInputs(w)
     pb = O.PaddedBatch(NL, B, Hq, Hkv, D, dtype, fill_bits=cache.fill_bits)
     saved_gpu, saved_cpu = {}, {}
+    scaler, parked_cpu = None, []
     shaped = []
     worst = 0.0
     for op in ops:
@@ -460,10 +464,26 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer"):
             shaped = []
         elif kind == "flush":
             cache.flush()
+        elif kind == "scale":
+            from paper_2410_18701_amd.scaling import BatchScaler
+            if scaler is None:
+                scaler = BatchScaler(cache, op[1])
+            scaler.max_cells = op[1]
+            parked = scaler.shrink()
+            for b in parked:                     # the oracle, in the same order
+                parked_cpu.append(pb.extract([b])[0])
+                pb.evict([b], release=True)
+            back = scaler.grow()
+            for b in back:
+                kh, vh = parked_cpu.pop(0)
+                pb.embed([b], [kh.shape[2]], [kh], [vh])
+            if log is not None:
+                log.append(("scale", parked, back))
         else:
             raise ValueError(kind)
         torch.cuda.synchronize()
-        check_ring(cache, pb, str(op), live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape", "move"))
+        check_ring(cache, pb, str(op),
+                   live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape", "move", "scale"))
         want_tok = [pb.hist_k[b].shape[2] if pb.lens[b] > 0 else 0 for b in range(B)]
         assert cache.tokens() == want_tok, (op, cache.tokens(), want_tok)
     cache.close()

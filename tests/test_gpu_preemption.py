@@ -37,6 +37,28 @@ def test_preempt_and_resume(shape):
     print(f"[preempt] {shape}: max abs error {err:.3g}", flush=True)
 
 
+def test_batch_scaler_threshold():
+    """Batch-size scaling driven by a threshold (sec. 4.3): with live rows x
+    padded length past it the query whose leaving shrinks that most -- the
+    longest -- goes to pinned host memory and its columns are released; it
+    stays parked while taking it back would pass the threshold again, and
+    returns, into another slot, once a query has finished.  Bit-exact against
+    the oracle after every operation, and the returned query decodes as the
+    oracle says."""
+    ops = [("embed", [0, 1, 2], [30, 95, 20], [0, 1, 2])]
+    ops += [("step", s) for s in range(6)]        # L 101: 3 x 101 = 303 cells
+    ops += [("scale", 300),                       # slot 1 (101 tokens) leaves: 2 x 36
+            ("step", 6), ("step", 7),
+            ("scale", 300),                       # 3 x 101 with it back: it stays out
+            ("evict", [0]),                       # a query finishes: 1 x 28
+            ("scale", 300),                       # 2 x 101: it returns, into slot 0
+            ("step", 8), ("step", 9)]
+    log = []
+    err = parity.run_script(("bf16", 2, 4, 8, 2, 128), ops, capacity=256, split=64, log=log)
+    assert log == [("scale", [1], []), ("scale", [], []), ("scale", [], [0])], log
+    print(f"[scaler] {log}: max abs error {err:.3g}", flush=True)
+
+
 def test_host_round_trip():
     """Batch-size scaling through host memory: extract, copy to pinned host
     memory, evict, copy back, re-embed -- the cache returns bit for bit."""
