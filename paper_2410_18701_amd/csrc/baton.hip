@@ -152,7 +152,7 @@ constexpr int64_t kAutoSplitMin = BATON_AUTO_SPLIT_MIN, kAutoSplitMax = 4096, kA
 // [dispatch order: max_items int32]
 // [partials: n_kv_heads][max_items][group][head_dim + 4] fp32.
 struct WsLayout {
-  size_t items_off, multi_off, order_off, partial_off, total;
+  size_t items_off, multi_off, partial_off, total;
   int64_t max_items;
 };
 
@@ -165,8 +165,7 @@ WsLayout ws_layout(const baton_cache* c) {
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   w.items_off = 0;
   w.multi_off = up(w.items_off + sizeof(baton::Item) * w.max_items);
-  w.order_off = up(w.multi_off + sizeof(int4) * B);
-  w.partial_off = up(w.order_off + sizeof(int32_t) * w.max_items);
+  w.partial_off = up(w.multi_off + sizeof(int4) * B);
   w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * w.max_items * c->group *
                                    (c->d.head_dim + 4));
   return w;
@@ -704,8 +703,7 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     if (items > w.max_items) return BATON_EINVAL;   // cannot happen: the layout bounds every row
     hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, m,
                        reinterpret_cast<baton::Item*>(wsb + w.items_off),
-                       reinterpret_cast<int4*>(wsb + w.multi_off),
-                       reinterpret_cast<int32_t*>(wsb + w.order_off));
+                       reinterpret_cast<int4*>(wsb + w.multi_off));
     const baton_status st = hip_status(hipGetLastError());
     if (st != BATON_OK) return st;
     c->n_items = (int32_t)items;
@@ -726,7 +724,6 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   a.out = static_cast<uint32_t*>(out);
   a.items = reinterpret_cast<const baton::Item*>(wsb + w.items_off);
   a.multi = reinterpret_cast<const int4*>(wsb + w.multi_off);
-  a.order = reinterpret_cast<const int32_t*>(wsb + w.order_off);
   a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
   a.cap = c->d.capacity;
   a.base = c->base;

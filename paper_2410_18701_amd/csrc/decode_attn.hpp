@@ -46,7 +46,7 @@ struct MetaArgs {
 // many there are.
 struct Item {
   int4 span;     // (b, t_begin, t_end, n)
-  int4 row;      // (first item of the row, items of the row, 0, 0)
+  int4 row;      // (first item of the row, items of the row, this item's index, 0)
 };
 
 // Items of a live row: each run of tokens cut into pieces of at most `split`.
@@ -68,15 +68,16 @@ __device__ __forceinline__ int32_t size_class(int32_t t, int32_t split) {
   return (int32_t)((int64_t)t * kSizeClasses / (split + 1));
 }
 
-// Builds the per-step work list in the workspace: one descriptor per item, so
-// that an item needs a single load to start; the list of rows with several
-// items (first item, item count, slot) for combine_kernel; and the dispatch
-// order, the items from the most tokens to the fewest (a counting sort over
-// size classes; the order within a class is arbitrary and affects no result).
+// Builds the per-step work list in the workspace: one descriptor per item,
+// stored in the dispatch order -- the items from the most tokens to the fewest
+// (a counting sort over size classes; the order within a class is arbitrary
+// and affects no result) -- so that a workgroup needs a single load to start;
+// and the list of rows with several items (first item, item count, slot) for
+// combine_kernel.
 // The attention workgroups are then dealt largest first, so that the ones that
 // start last are short and the launch ends with little of the GPU idle.
 __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, Item* ws_items,
-                                                            int4* ws_multi, int32_t* ws_order) {
+                                                            int4* ws_multi) {
   __shared__ int32_t scan[kMetaThreads];
   __shared__ int32_t scan_multi[kMetaThreads];
   __shared__ int32_t cursor[kSizeClasses];
@@ -97,18 +98,12 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   }
   const int32_t first = scan[b] - cnt;
   if (b < a.batch && cnt > 0) {
-    const int4 row = make_int4(first, cnt, 0, 0);
     if (n == 0) {
-      ws_items[first] = Item{make_int4(b, 0, 0, -1), row};
       atomicAdd(&cursor[0], 1);
     } else {
-      int32_t c = first;
       row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
-        for (int32_t t = t0; t < t1; t += a.split) {
-          const int32_t te = min(t + a.split, t1);
-          ws_items[c++] = Item{make_int4(b, t, te, n), row};
-          atomicAdd(&cursor[size_class(te - t, a.split)], 1);
-        }
+        for (int32_t t = t0; t < t1; t += a.split)
+          atomicAdd(&cursor[size_class(min(t + a.split, t1) - t, a.split)], 1);
       });
     }
     if (cnt > 1) ws_multi[scan_multi[b] - 1] = make_int4(first, cnt, b, 0);
@@ -123,14 +118,20 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
     }
   }
   __syncthreads();
+  // The descriptors, each at its place in the dispatch order; an item's own
+  // index (its row's first item + its rank in the row) numbers its partial
+  // record.
   if (b < a.batch && cnt > 0) {
     if (n == 0) {
-      ws_order[atomicAdd(&cursor[0], 1)] = first;
+      ws_items[atomicAdd(&cursor[0], 1)] = Item{make_int4(b, 0, 0, -1), make_int4(first, cnt, first, 0)};
     } else {
       int32_t c = first;
       row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
-        for (int32_t t = t0; t < t1; t += a.split, ++c)
-          ws_order[atomicAdd(&cursor[size_class(min(t + a.split, t1) - t, a.split)], 1)] = c;
+        for (int32_t t = t0; t < t1; t += a.split, ++c) {
+          const int32_t te = min(t + a.split, t1);
+          ws_items[atomicAdd(&cursor[size_class(te - t, a.split)], 1)] =
+              Item{make_int4(b, t, te, n), make_int4(first, cnt, c, 0)};
+        }
       });
     }
   }
@@ -144,9 +145,8 @@ struct AttnArgs {
   const uint32_t* knew;      // [batch][tw][n_kv_heads][D]
   const uint32_t* vnew;
   uint32_t* out;             // [batch][tw][n_q_heads][D]
-  const Item* items;         // workspace
+  const Item* items;         // workspace: the work list in dispatch order
   const int4* multi;         // rows with several items: (first item, count, slot)
-  const int32_t* order;      // dispatch order of the items
   float* partial;            // [n_kv_heads][n_items][G][D + 4]
   int64_t cap, base, L;
   int32_t batch, n_kv_heads, split, n_items;
@@ -279,12 +279,14 @@ __device__ __forceinline__ void merge_row(const float* base, int32_t count, uint
 #endif
 
 // The work unit (item, kv-head) of this workgroup: workgroups are dealt in
-// the order of the work list's dispatch order (largest items first), all
-// kv-heads of an item next to each other.
-__device__ __forceinline__ void work_unit(const AttnArgs& a, int32_t& item, int32_t& h) {
+// the work list's dispatch order (largest items first), all kv-heads of an
+// item next to each other; one load gives the item's descriptor.
+__device__ __forceinline__ Item work_unit(const AttnArgs& a, int32_t& item, int32_t& h) {
   const int32_t k = blockIdx.x;
-  item = a.order[k / a.n_kv_heads];
+  const Item d = a.items[k / a.n_kv_heads];
+  item = d.row.z;
   h = k % a.n_kv_heads;
+  return d;
 }
 
 // Merge of the NW waves of a workgroup, each holding the online-softmax state
@@ -356,7 +358,7 @@ attn_kernel(const AttnArgs a) {
   __shared__ float sm_m[NW][G], sm_l[NW][G];
   __shared__ float sm_acc[NW][G][D];
   int32_t item, h;
-  work_unit(a, item, h);
+  const Item desc = work_unit(a, item, h);
   const int tid = threadIdx.x;
   // wave of the workgroup, as a scalar: the loop bounds derived from it are uniform
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -364,8 +366,8 @@ attn_kernel(const AttnArgs a) {
   const int r = lane / LPT;        // token row within an instruction
   const int cl = lane % LPT;       // 16-byte slice of the row
 
-  const int4 it = a.items[item].span;
-  const int4 rw = a.items[item].row;
+  const int4 it = desc.span;
+  const int4 rw = desc.row;
   const int b = it.x;
   const int32_t n = it.w;          // cached tokens; token n is the current one
   const int64_t bt = (int64_t)b * a.tw;   // input row of the slot's position 0

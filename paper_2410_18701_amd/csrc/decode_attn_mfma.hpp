@@ -140,7 +140,7 @@ attn_mfma_kernel(const AttnArgs a) {
   __shared__ float sm_m[NW][G], sm_l[NW][G];
   static_assert(G * D * 4 <= 32 * Geo::kLdsRow, "merge area");
   int32_t item, h;
-  work_unit(a, item, h);
+  const Item desc = work_unit(a, item, h);
   const int tid = threadIdx.x;
   // wave of the workgroup, as a scalar: the loop bounds derived from it are uniform
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
@@ -148,8 +148,8 @@ attn_mfma_kernel(const AttnArgs a) {
   uint8_t* lds = lds_v[w];
   uint8_t* ldk = lds_k[w];
 
-  const int4 it = a.items[item].span;
-  const int4 rw = a.items[item].row;
+  const int4 it = desc.span;
+  const int4 rw = desc.row;
   const int b = it.x;
   const int32_t n = it.w;
   const int64_t bt = (int64_t)b * a.tw;   // input row of the slot's position 0
