@@ -50,8 +50,9 @@ class BatchScaler:
                 return _cells(len(live) - 1, max(lens[s] for s in live if s != b))
             b = min(live, key=lambda s: (after(s), -lens[s], s))
             ks, vs = self.cache.extract([b])
-            hk = torch.empty(ks[0].shape, dtype=ks[0].dtype, pin_memory=True)
-            hv = torch.empty(vs[0].shape, dtype=vs[0].dtype, pin_memory=True)
+            pin = ks[0].is_cuda   # pinned host memory for device data
+            hk = torch.empty(ks[0].shape, dtype=ks[0].dtype, pin_memory=pin)
+            hv = torch.empty(vs[0].shape, dtype=vs[0].dtype, pin_memory=pin)
             hk.copy_(ks[0], non_blocking=True)
             hv.copy_(vs[0], non_blocking=True)
             self.cache.evict([b], release=True)
