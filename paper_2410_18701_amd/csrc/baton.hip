@@ -291,7 +291,7 @@ bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, hipStream_t s) 
 template <int D, int G>
 void launch_prefill_g(const baton_cache* c, baton::PrefillArgs& a, hipStream_t s) {
   const bool fa = BATON_PREFILL_MFMA && c->d.dtype == BATON_BF16;
-  const int32_t per_tile = fa ? 64 : baton::kWave / (D * c->esz / 16);
+  const int32_t per_tile = fa ? baton::kPrefillTile : baton::kWave / (D * c->esz / 16);
   int32_t tiles = 0;
   for (int32_t i = 0; i < a.n_ins; ++i) {
     tiles += (a.plen[i] + per_tile - 1) / per_tile;

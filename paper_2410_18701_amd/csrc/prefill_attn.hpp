@@ -151,15 +151,20 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 }
 
 // bf16 on the matrix cores, flash-attention style: a workgroup of 4*S waves
-// takes 64 prompt positions of one query head; four waves cover the positions
-// (16 each) and S such quartets split the keys, each walking every S-th tile
-// of KT keys (S tiles staged in LDS per iteration, K and V both as rows,
-// 16-byte stores), and the quartets' softmax states merge through LDS at the
-// end -- S shortens the longest causal tile's chain of iterations.
-//  * QK^T: A = 16 key rows (lane l: key l % 16 of the half tile), B = the
-//    wave's 16 positions; the score of key 4*(l/16) + r (first 16 keys) and
-//    16 + 4*(l/16) + r (next 16) for position l % 16 lands in lane l,
-//    register r.
+// takes kPrefillTile prompt positions of one query head; four waves cover the
+// positions (QG groups of 16 each) and S such quartets split the keys, each
+// walking every S-th tile of KT keys (S tiles staged in LDS per iteration, K
+// and V both as rows, 16-byte stores), and the quartets' softmax states merge
+// through LDS at the end -- S shortens the longest causal tile's chain of
+// iterations.  Every key and value fragment a wave reads from LDS serves its
+// QG position groups: the kernel's limit is the LDS read bandwidth (each
+// 32-key block costs a wave 16 KB of LDS reads, as many bytes as the matrix
+// operations on one group take cycles), so QG = 2 halves the LDS bytes per
+// multiply-add.
+//  * QK^T: A = 16 key rows (lane l: key l % 16 of the half tile), B = 16 of
+//    the wave's positions; the score of key 4*(l/16) + r (first 16 keys) and
+//    16 + 4*(l/16) + r (next 16) for position l % 16 of the group lands in
+//    lane l, register r.
 //  * PV, transposed: O^T = V^T P^T.  B = P^T with k = 8*(l/16) + e standing
 //    for key 4*(l/16) + e (e < 4) and 16 + 4*(l/16) + e - 4 (e >= 4) -- the
 //    lane's own scores, in place; A = V^T in that key order, read with the
@@ -167,14 +172,19 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 //    lane i receives element i % 4 of the 8-byte block addressed by lane
 //    i / 4 + 4e, for e = 0..3; lane m of group g addresses key 4g + m / 4 at
 //    columns 16*dt + 4*(m % 4), so lane i gets V[4g + e][16*dt + i].  Lane l
-//    then holds output columns 16*dt + 4*(l/16) + r of position l % 16: a
-//    position's rescale and normalisation stay in its own lanes, and the
-//    max and sum over the four lane groups use the gfx950 row swaps.
+//    then holds output columns 16*dt + 4*(l/16) + r of position l % 16 of the
+//    group: a position's rescale and normalisation stay in its own lanes, and
+//    the max and sum over the four lane groups use the gfx950 row swaps.
 // Rows are padded to 8 dwords past a multiple of 32, so that the 16 rows of a
 // transpose load spread over all banks.
 #ifndef BATON_PREFILL_KT
 #define BATON_PREFILL_KT 64
 #endif
+#ifndef BATON_PREFILL_QG
+#define BATON_PREFILL_QG 1
+#endif
+constexpr int kPrefillGroups = BATON_PREFILL_QG;     // groups of 16 positions per wave
+constexpr int kPrefillTile = 64 * kPrefillGroups;    // positions per workgroup
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -183,18 +193,24 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint8_t* p) {
       (__attribute__((address_space(3))) s16x4*)(__attribute__((address_space(3))) void*)(p));
 }
 
+// Registers capped so that two workgroups share a CU (one group per wave: 128
+// per lane, four waves per SIMD; two groups: 256, two waves per SIMD).
 template <int D, int G, int S>
-__global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a) {
+__global__ void __launch_bounds__(256 * S) __attribute__((amdgpu_waves_per_eu(kPrefillGroups == 1 ? 4 : 2)))
+prefill_fa_kernel(const PrefillArgs a) {
   constexpr int VPT = D / 8, KK = D / 32, DT = D / 16;
+  constexpr int QG = kPrefillGroups, TILE = kPrefillTile;
   constexpr int KT = BATON_PREFILL_KT;       // keys per LDS tile and key stream
   constexpr int ROW = D * 2 + 32;            // bytes per staged key / value row
   constexpr int NT = 256 * S;                // threads
   constexpr int NLD = KT * VPT / 256;        // 16-byte vectors per thread per stage, K and V each
-  constexpr int REC = DT * 4 + 2;            // floats per lane of a merged softmax state
+  constexpr int GREC = DT * 4 + 2;           // floats of one group's softmax state per lane
+  constexpr int REC = QG * GREC;
   static_assert((ROW / 4) % 32 == 8, "row padding");
-  static_assert(S == 1 || (S - 1) * 4 * kWave * REC * 4 <= S * KT * ROW, "merge area");
-  __shared__ __attribute__((aligned(16))) uint8_t ldsK[S * KT * ROW];
-  __shared__ __attribute__((aligned(16))) uint8_t ldsV[S * KT * ROW];
+  static_assert(S == 1 || (S - 1) * 4 * kWave * REC * 4 <= 2 * S * KT * ROW, "merge area");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * S * KT * ROW];
+  uint8_t* const ldsK = lds;
+  uint8_t* const ldsV = lds + S * KT * ROW;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
   const int ks = wave / 4;                             // key stream of this wave
@@ -205,8 +221,8 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
   const int h = hq / G;
   const int b = a.slot[ins];
   const int32_t p = a.plen[ins];
-  const int32_t wg0 = tile * 64;                       // first position of the workgroup
-  const int32_t i0 = wg0 + (wave % 4) * 16;            // first position of this wave
+  const int32_t wg0 = tile * TILE;                     // first position of the workgroup
+  const int32_t i0 = wg0 + (wave % 4) * 16 * QG;       // first position of this wave
   const int64_t row0 = (int64_t)b * a.T + (a.T - p);
   const int nkv = a.n_kv_heads, nq = nkv * G;
   const u32x4* qin = reinterpret_cast<const u32x4*>(a.q);
@@ -214,19 +230,28 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
   const u32x4* vin = reinterpret_cast<const u32x4*>(a.vnew);
   const u32x4 zero = {0, 0, 0, 0};
 
-  const int32_t qi = i0 + c16;
-  bf16x8 qb[KK];
+  bf16x8 qb[QG][KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk)
-    qb[kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] : zero);
-
-  float m = -INFINITY, lsum = 0.f;
-  f32x4 o[DT];
+  for (int gq = 0; gq < QG; ++gq) {
+    const int32_t qi = i0 + 16 * gq + c16;
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < KK; ++kk)
+      qb[gq][kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] : zero);
+  }
 
-  const int32_t wg_last = min(wg0 + 63, p - 1);
-  const int32_t w_last = min(i0 + 15, p - 1);
+  float m[QG], lsum[QG];
+  f32x4 o[QG][DT];
+#pragma unroll
+  for (int gq = 0; gq < QG; ++gq) {
+    m[gq] = -INFINITY;
+    lsum[gq] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[gq][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int32_t wg_last = min(wg0 + TILE - 1, p - 1);
+  // the wave's last position; a wave wholly past the prompt computes nothing
+  const int32_t w_last = i0 < p ? min(i0 + 16 * QG - 1, p - 1) : -1;
   // This lane's transpose-load address within a value row block: key offset
   // 4*g4 + c16/4, columns 4*(c16 % 4).
   const int tr_off = (4 * g4 + c16 / 4) * ROW + (c16 % 4) * 8;
@@ -255,57 +280,72 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
       const int kb = ks * KT + 32 * half;              // key row of the block in the stage
       const int32_t tt = k0 + kb;
       if (tt > w_last) break;                          // wave-uniform
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+      f32x4 sa[QG], sb[QG];
+#pragma unroll
+      for (int gq = 0; gq < QG; ++gq) {
+        sa[gq] = f32x4{0.f, 0.f, 0.f, 0.f};
+        sb[gq] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         const u32x4 ka = *reinterpret_cast<const u32x4*>(ldsK + (kb + c16) * ROW + (kk * 4 + g4) * 16);
         const u32x4 kc = *reinterpret_cast<const u32x4*>(ldsK + (kb + 16 + c16) * ROW + (kk * 4 + g4) * 16);
-        sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka), qb[kk], sa, 0, 0, 0);
-        sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc), qb[kk], sb, 0, 0, 0);
-      }
-      // Unscaled scores; masked keys -inf.  A block whose 32 keys all come
-      // before the wave's first position is visible to every position of the
-      // wave and needs no mask (positions past the prompt are never written).
-      float s[8];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        s[r] = sa[r];
-        s[4 + r] = sb[r];
-      }
-      if (tt + 31 > i0) {                              // wave-uniform
-        const int32_t lim = qi < p ? qi - tt : -1;     // keys tt .. tt + lim are visible
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          s[r] = 4 * g4 + r <= lim ? s[r] : -INFINITY;
-          s[4 + r] = 16 + 4 * g4 + r <= lim ? s[4 + r] : -INFINITY;
+        for (int gq = 0; gq < QG; ++gq) {
+          sa[gq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka), qb[gq][kk], sa[gq], 0, 0, 0);
+          sb[gq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc), qb[gq][kk], sb[gq], 0, 0, 0);
         }
       }
-      float mx = s[0];
+      bf16x8 pa[QG];
 #pragma unroll
-      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
-      mx = max_over_groups(mx) * a.qscale;             // qscale > 0: the max of the scaled scores
-      const float mn = fmaxf(m, mx);
-      const float ref = mn == -INFINITY ? 0.f : mn;
-      // exponents are <= 0 here: the hardware exp2 (results below the
-      // smallest normal flush to 0, which a softmax weight may); the scale is
-      // applied in the exponent's multiply-add, the sum taken before P is
-      // rounded to bf16 for the matrix operation
-      const float alpha = __builtin_amdgcn_exp2f(m - ref);
-      bf16x8 pa;
-      float psum = 0.f;
+      for (int gq = 0; gq < QG; ++gq) {
+        const int32_t ig = i0 + 16 * gq;               // the group's first position
+        const int32_t qi = ig + c16;
+        // Unscaled scores; masked keys -inf.  A block whose 32 keys all come
+        // before the group's first position is visible to every position of
+        // the group and needs no mask (positions past the prompt are never
+        // written).
+        float s[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pf = __builtin_amdgcn_exp2f(fmaf(s[e], a.qscale, -ref));
-        pa[e] = (__bf16)pf;
-        psum += pf;
-      }
-      lsum = lsum * alpha + psum;
-      m = mn;
-      // Rescale the accumulators (this lane's position's own factor) only when
-      // some position's maximum moved (after the first keys it rarely does).
-      if (__ballot(alpha != 1.f)) {
+        for (int r = 0; r < 4; ++r) {
+          s[r] = sa[gq][r];
+          s[4 + r] = sb[gq][r];
+        }
+        if (tt + 31 > ig) {                            // wave-uniform
+          const int32_t lim = qi < p ? qi - tt : -1;   // keys tt .. tt + lim are visible
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+          for (int r = 0; r < 4; ++r) {
+            s[r] = 4 * g4 + r <= lim ? s[r] : -INFINITY;
+            s[4 + r] = 16 + 4 * g4 + r <= lim ? s[4 + r] : -INFINITY;
+          }
+        }
+        float mx = s[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
+        mx = max_over_groups(mx) * a.qscale;           // qscale > 0: the max of the scaled scores
+        const float mn = fmaxf(m[gq], mx);
+        const float ref = mn == -INFINITY ? 0.f : mn;
+        // exponents are <= 0 here: the hardware exp2 (results below the
+        // smallest normal flush to 0, which a softmax weight may); the scale
+        // is applied in the exponent's multiply-add, the sum taken before P is
+        // rounded to bf16 for the matrix operation
+        const float alpha = __builtin_amdgcn_exp2f(m[gq] - ref);
+        float psum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pf = __builtin_amdgcn_exp2f(fmaf(s[e], a.qscale, -ref));
+          pa[gq][e] = (__bf16)pf;
+          psum += pf;
+        }
+        lsum[gq] = lsum[gq] * alpha + psum;
+        m[gq] = mn;
+        // Rescale the accumulators (this lane's position's own factor) only
+        // when some position's maximum moved (after the first keys it rarely
+        // does).
+        if (__ballot(alpha != 1.f)) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[gq][dt] *= alpha;
+        }
       }
       const uint8_t* vblk = ldsV + kb * ROW + tr_off;
 #pragma unroll
@@ -314,7 +354,9 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
         const s16x4 hi = lds_read_tr16(vblk + 16 * ROW + dt * 32);
         const s16x4 w2[2] = {lo, hi};
         const bf16x8 vb = __builtin_bit_cast(bf16x8, w2);
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pa, o[dt], 0, 0, 0);
+#pragma unroll
+        for (int gq = 0; gq < QG; ++gq)
+          o[gq][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pa[gq], o[gq][dt], 0, 0, 0);
       }
     }
   };
@@ -337,47 +379,59 @@ __global__ void __launch_bounds__(256 * S) prefill_fa_kernel(const PrefillArgs a
   if constexpr (S > 1) {
     // Key streams 1.. hand their states to stream 0 (same positions, same lane).
     __syncthreads();                                   // the stage buffers are free
-    float* mrg = reinterpret_cast<float*>(ldsK) + ((ks - 1) * 4 + wave % 4) * kWave * REC + lane * REC;
+    float* mrg = reinterpret_cast<float*>(lds) + ((ks - 1) * 4 + wave % 4) * kWave * REC + lane * REC;
     if (ks > 0) {
-      mrg[0] = m;
-      mrg[1] = lsum;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+      for (int gq = 0; gq < QG; ++gq) {
+        mrg[gq * GREC] = m[gq];
+        mrg[gq * GREC + 1] = lsum[gq];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mrg[2 + dt * 4 + r] = o[dt][r];
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mrg[gq * GREC + 2 + dt * 4 + r] = o[gq][dt][r];
+      }
     }
     __syncthreads();
     if (ks == 0) {
 #pragma unroll
       for (int k = 1; k < S; ++k) {
-        const float* src = reinterpret_cast<const float*>(ldsK) + ((k - 1) * 4 + wave % 4) * kWave * REC + lane * REC;
-        const float m2 = src[0];
-        const float mm = fmaxf(m, m2);
-        const float fa = m == -INFINITY ? 0.f : exp2f(m - mm);
-        const float fb = m2 == -INFINITY ? 0.f : exp2f(m2 - mm);
-        lsum = lsum * fa + src[1] * fb;
-        m = mm;
+        const float* src = reinterpret_cast<const float*>(lds) + ((k - 1) * 4 + wave % 4) * kWave * REC + lane * REC;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int gq = 0; gq < QG; ++gq) {
+          const float* sg = src + gq * GREC;
+          const float m2 = sg[0];
+          const float mm = fmaxf(m[gq], m2);
+          const float fa = m[gq] == -INFINITY ? 0.f : exp2f(m[gq] - mm);
+          const float fb = m2 == -INFINITY ? 0.f : exp2f(m2 - mm);
+          lsum[gq] = lsum[gq] * fa + sg[1] * fb;
+          m[gq] = mm;
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt][r] = o[dt][r] * fa + src[2 + dt * 4 + r] * fb;
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[gq][dt][r] = o[gq][dt][r] * fa + sg[2 + dt * 4 + r] * fb;
+        }
       }
     }
   }
   if (ks == 0) {
-    // Lane l holds columns 16 dt + 4 (l / 16) + r of position l % 16.
-    lsum = sum_over_groups(lsum);
-    if (qi < p) {
-      const float inv = 1.f / lsum;
-      uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + qi) * nq + hq) * D + 4 * g4;
+    // Lane l holds columns 16 dt + 4 (l / 16) + r of position l % 16 of each group.
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<uint2*>(o16 + 16 * dt) =
-            make_uint2(f32_to_bf16_rne(o[dt][0] * inv) | (f32_to_bf16_rne(o[dt][1] * inv) << 16),
-                       f32_to_bf16_rne(o[dt][2] * inv) | (f32_to_bf16_rne(o[dt][3] * inv) << 16));
+    for (int gq = 0; gq < QG; ++gq) {
+      const int32_t qi = i0 + 16 * gq + c16;
+      const float ls = sum_over_groups(lsum[gq]);
+      if (qi < p) {
+        const float inv = 1.f / ls;
+        uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + qi) * nq + hq) * D + 4 * g4;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<uint2*>(o16 + 16 * dt) =
+              make_uint2(f32_to_bf16_rne(o[gq][dt][0] * inv) | (f32_to_bf16_rne(o[gq][dt][1] * inv) << 16),
+                         f32_to_bf16_rne(o[gq][dt][2] * inv) | (f32_to_bf16_rne(o[gq][dt][3] * inv) << 16));
+      }
     }
   }
-  if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, wg0, min(64, p - wg0), tid, NT);
+  if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, wg0, min(TILE, p - wg0), tid, NT);
 }
 
 }  // namespace baton
+
