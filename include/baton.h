@@ -386,6 +386,21 @@ baton_status baton_linear_packed(int32_t dtype, const void* x, const void* wp, v
                                  hipStream_t stream);
 
 /*
+ * baton_linear_packed, then the RMS norm of its output (the layer's residual
+ * add followed by the next normalisation, as a llama2 decoder layer runs
+ * them): y as baton_linear_packed leaves it, and y_norm (device
+ * [rows][out_dim], 16-byte aligned, may alias y) = baton_rmsnorm(y, gain,
+ * eps), bit for bit.  When the product splits along in_dim one kernel adds the
+ * partial sums (and y with accumulate) and normalises each row, in place of
+ * the addition's launch and the norm's launch.
+ * Errors: those of baton_linear_packed and baton_rmsnorm (null or misaligned
+ * gain / y_norm, eps < 0 or not finite: EINVAL).
+ */
+baton_status baton_linear_packed_rmsnorm(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                         int32_t out_dim, int32_t in_dim, int32_t accumulate, const void* gain,
+                                         float eps, void* y_norm, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * y[r] = x[r] / sqrt(mean_j x[r][j]^2 + eps) * gain: x, y device [rows][dim],
  * gain device [dim]; dim a multiple of 8.  y may alias x.
  * Errors: EINVAL (null or misaligned pointer, bad sizes, eps < 0), EDTYPE.

@@ -139,10 +139,19 @@ baton_status baton_linear_pack(int32_t dtype, const void* w, void* wp, int32_t o
   return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
 }
 
-baton_status baton_linear_packed(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
-                                 int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws, size_t ws_bytes,
-                                 hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// baton_linear_packed, and with gain the RMS norm of its output rows into
+// y_norm (the split sums added and each row normalised by one kernel when the
+// product splits along k).
+baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows, int32_t out_dim,
+                           int32_t in_dim, int32_t accumulate, const void* gain, float eps, void* y_norm, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
   if (!x || !wp || !y || rows < 1 || rows > 64 || out_dim < 1 || in_dim < 1 || (ws_bytes && !ws))
+    return BATON_EINVAL;
+  if (gain && (!y_norm || !aligned16(gain) || !aligned16(y_norm) || !(eps >= 0.f) || !std::isfinite(eps)))
     return BATON_EINVAL;
   if (accumulate != 0 && accumulate != 1) return BATON_EINVAL;
   if (dtype != BATON_BF16) return BATON_EDTYPE;
@@ -180,12 +189,40 @@ baton_status baton_linear_packed(int32_t dtype, const void* x, const void* wp, v
     case 3: launch_skinny_mg<3>(a, grid, stream); break;
     default: launch_skinny_mg<4>(a, grid, stream); break;
   }
-  if (S > 1) {
-    const int64_t n_out = (int64_t)rows * out_dim;
-    hipLaunchKernelGGL(baton::gemm_reduce_kernel, dim3((unsigned)((n_out / 4 + 255) / 256)), dim3(256), 0, stream,
-                       a.part, a.y, S, n_out, accumulate);
+  const int64_t n_out = (int64_t)rows * out_dim;
+  if (S > 1 && gain) {
+    hipLaunchKernelGGL(baton::reduce_rmsnorm_kernel, dim3(rows), dim3(baton::kRowThreads), 0, stream, a.part, a.y, S,
+                       n_out, accumulate, static_cast<const baton::u32x4*>(gain),
+                       static_cast<baton::u32x4*>(y_norm), out_dim / 8, 1.0f / out_dim, eps);
+  } else {
+    if (S > 1)
+      hipLaunchKernelGGL(baton::gemm_reduce_kernel, dim3((unsigned)((n_out / 4 + 255) / 256)), dim3(256), 0, stream,
+                         a.part, a.y, S, n_out, accumulate);
+    if (gain)
+      hipLaunchKernelGGL(baton::rmsnorm_kernel, dim3(rows), dim3(baton::kRowThreads), 0, stream,
+                         static_cast<const baton::u32x4*>(y), static_cast<const baton::u32x4*>(gain),
+                         static_cast<baton::u32x4*>(y_norm), out_dim / 8, 1.0f / out_dim, eps);
   }
   return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+baton_status baton_linear_packed(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                 int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  return linear_packed(dtype, x, wp, y, rows, out_dim, in_dim, accumulate, nullptr, 0.f, nullptr, ws, ws_bytes,
+                       stream);
+}
+
+baton_status baton_linear_packed_rmsnorm(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                         int32_t out_dim, int32_t in_dim, int32_t accumulate, const void* gain,
+                                         float eps, void* y_norm, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!gain) return BATON_EINVAL;
+  return linear_packed(dtype, x, wp, y, rows, out_dim, in_dim, accumulate, gain, eps, y_norm, ws, ws_bytes,
+                       stream);
 }
 
 baton_status baton_rmsnorm(int32_t dtype, const void* x, const void* gain, void* y, int32_t rows, int32_t dim,

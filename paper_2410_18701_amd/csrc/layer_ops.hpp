@@ -319,5 +319,61 @@ __global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* __restric
   *yp = make_uint2(pack_bf16(v.x, v.y), pack_bf16(v.z, v.w));
 }
 
+// The split sums of a projection's output added up (and to the residual y
+// with accumulate) as gemm_reduce_kernel does, then each row's RMS norm as
+// rmsnorm_kernel does, element for element and in the same order: one
+// workgroup per row, thread t owning the row's 8-element groups t, t +
+// kRowThreads, ...  The result is bit-identical to the two launches, without
+// the second one's read of y.
+__global__ void __launch_bounds__(kRowThreads) reduce_rmsnorm_kernel(
+    const float* __restrict__ part, uint16_t* __restrict__ y, int32_t S, int64_t n_out, int32_t accumulate,
+    const u32x4* __restrict__ g, u32x4* __restrict__ yn, int32_t vec_per_row, float inv_dim, float eps) {
+  __shared__ float psum[kRowThreads / kWave];
+  const int64_t row = blockIdx.x;
+  u32x4* yr = reinterpret_cast<u32x4*>(y) + row * vec_per_row;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < vec_per_row; i += kRowThreads) {
+    const int64_t e0 = (row * vec_per_row + i) * 8;   // the group's first element
+    const u32x4 old = accumulate ? yr[i] : u32x4{0, 0, 0, 0};
+    u32x4 w;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      float4 v = *reinterpret_cast<const float4*>(part + e0 + 4 * hf);
+      for (int32_t s = 1; s < S; ++s) {
+        const float4 q = *reinterpret_cast<const float4*>(part + s * n_out + e0 + 4 * hf);
+        v.x += q.x; v.y += q.y; v.z += q.z; v.w += q.w;
+      }
+      if (accumulate) {
+        v.x += bf16_lo(old[2 * hf]); v.y += bf16_hi(old[2 * hf]);
+        v.z += bf16_lo(old[2 * hf + 1]); v.w += bf16_hi(old[2 * hf + 1]);
+      }
+      w[2 * hf] = pack_bf16(v.x, v.y);
+      w[2 * hf + 1] = pack_bf16(v.z, v.w);
+    }
+    yr[i] = w;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float a = bf16_lo(w[j]), b = bf16_hi(w[j]);
+      ss = fmaf(a, a, fmaf(b, b, ss));
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) ss += __shfl_xor(ss, off, kWave);
+  if (threadIdx.x % kWave == 0) psum[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kRowThreads / kWave; ++w) tot += psum[w];
+  const float inv = 1.0f / sqrtf(tot * inv_dim + eps);
+  for (int i = threadIdx.x; i < vec_per_row; i += kRowThreads) {
+    const u32x4 w = yr[i], gw = g[i];   // this thread's own stores above
+    u32x4 o;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o[j] = pack_bf16(bf16_lo(w[j]) * inv * bf16_lo(gw[j]), bf16_hi(w[j]) * inv * bf16_hi(gw[j]));
+    yn[row * vec_per_row + i] = o;
+  }
+}
+
 }  // namespace
 }  // namespace baton

@@ -66,6 +66,20 @@ class Gemm:
                               self.ws.numel(), _stream())
         return y
 
+    def linear_packed_rmsnorm(self, x, wp, y, gain, eps, y_norm, accumulate=False):
+        """linear_packed, then y_norm = rmsnorm(y, gain, eps) (bit for bit; one
+        kernel adds the split sums and normalises when the product splits)."""
+        rows, in_dim = x.shape
+        if in_dim != wp.in_dim or tuple(y.shape) != (rows, wp.out_dim) or tuple(y_norm.shape) != tuple(y.shape) \
+                or gain.numel() != wp.out_dim:
+            raise ValueError("linear_packed_rmsnorm: shapes do not match")
+        for t in (x, y, y_norm, gain):
+            if not t.is_contiguous():
+                raise ValueError("linear_packed_rmsnorm: contiguous tensors only")
+        B.baton_linear_packed_rmsnorm(B.BATON_BF16, x, wp.data, y, rows, wp.out_dim, in_dim, accumulate, gain,
+                                      eps, y_norm, self.ws, self.ws.numel(), _stream())
+        return y
+
     def close(self):
         if self.handle:
             B.baton_gemm_destroy(self.handle)
@@ -104,7 +118,10 @@ class DecodeLayers:
     weights[layer]: dict of bf16 device tensors norm1 [hid], qkv [(Hq + 2 Hkv) D][hid],
     o [hid][Hq D], norm2 [hid], gate_up [2 F][hid], down [hid][F].  Up to 64 slots
     the projections run on the weight-streaming GEMM over packed copies of the
-    weights, made here once (packed=False keeps hipBLASLt on the stored weights)."""
+    weights, made here once (packed=False keeps hipBLASLt on the stored weights).
+    On the packed path each residual add is fused with the normalisation that
+    follows it (the output projection with norm2, the down projection with the
+    next layer's norm1), so layer(l + 1) expects x as layer(l) returned it."""
 
     PROJ = ("qkv", "o", "gate_up", "down")
 
@@ -120,6 +137,7 @@ class DecodeLayers:
         self.h, self.qkv = e(Bt, hid), e(Bt, (Hq + 2 * Hkv) * D)
         self.q, self.k, self.v, self.att = e(Bt, Hq, D), e(Bt, Hkv, D), e(Bt, Hkv, D), e(Bt, Hq, D)
         self.gu, self.act = e(Bt, 2 * F), e(Bt, F)
+        self._normed = None   # (layer, x) whose norm1 input h already holds
 
     def layer(self, layer, x):
         """One layer of the decode step on the residual stream x [batch][hid] (in place)."""
@@ -128,13 +146,24 @@ class DecodeLayers:
             wp, lin = self.wp[layer], self.gemm.linear_packed
         else:
             wp, lin = w, self.gemm.linear
-        rmsnorm(x, w["norm1"], self.h, self.eps)
+        if self._normed != (layer, x.data_ptr()):   # h holds norm1(x) after the previous layer
+            rmsnorm(x, w["norm1"], self.h, self.eps)
+        self._normed = None
         lin(self.h, wp["qkv"], self.qkv)
         rope_qkv(self.cache, self.qkv, self.q, self.k, self.v, self.theta)
         self.cache.decode_attn(layer, self.q, self.k, self.v, out=self.att)
-        lin(self.att.view(self.att.shape[0], -1), wp["o"], x, accumulate=True)
-        rmsnorm(x, w["norm2"], self.h, self.eps)
+        att = self.att.view(self.att.shape[0], -1)
+        if self.packed:
+            self.gemm.linear_packed_rmsnorm(att, wp["o"], x, w["norm2"], self.eps, self.h, accumulate=True)
+        else:
+            lin(att, wp["o"], x, accumulate=True)
+            rmsnorm(x, w["norm2"], self.h, self.eps)
         lin(self.h, wp["gate_up"], self.gu)
         silu_mul(self.gu, self.act)
-        lin(self.act, wp["down"], x, accumulate=True)
+        if self.packed and layer + 1 < len(self.w):
+            self.gemm.linear_packed_rmsnorm(self.act, wp["down"], x, self.w[layer + 1]["norm1"], self.eps, self.h,
+                                            accumulate=True)
+            self._normed = (layer + 1, x.data_ptr())
+        else:
+            lin(self.act, wp["down"], x, accumulate=True)
         return x

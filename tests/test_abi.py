@@ -161,3 +161,11 @@ def test_packed_linear_host_checks():
     assert status(lp, B.BATON_BF16, X, W, Y, 8, 64, 64, 2, 0, 0) == B.BATON_EINVAL            # accumulate
     assert status(lp, B.BATON_BF16, X, W, Y, 8, 64, 64, 0, 0, 1024) == B.BATON_EINVAL         # ws_bytes, no ws
     assert status(lp, B.BATON_F32, X, W, Y, 8, 64, 64, 0, 0, 0) == B.BATON_EDTYPE
+    G, N = 0x40000, 0x50000
+    lpn = B.baton_linear_packed_rmsnorm
+    assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, 0, 1e-5, N, 0, 0) == B.BATON_EINVAL      # null gain
+    assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G, 1e-5, 0, 0, 0) == B.BATON_EINVAL      # null y_norm
+    assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G + 8, 1e-5, N, 0, 0) == B.BATON_EINVAL  # misaligned
+    assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G, -1.0, N, 0, 0) == B.BATON_EINVAL      # eps < 0
+    assert status(lpn, B.BATON_BF16, X, W, Y, 65, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EINVAL     # rows > 64
+    assert status(lpn, B.BATON_F32, X, W, Y, 8, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EDTYPE

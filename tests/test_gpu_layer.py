@@ -101,6 +101,38 @@ def test_linear_packed(rows, out_dim, in_dim, ws):
     g.close()
 
 
+# The fused projection + RMS norm against the two calls it replaces, bit for
+# bit, on shapes that split along in_dim (the output and down projections of
+# llama2-7b at 64 and 8 rows, 17 rows of a smaller one) and ones that do not
+# (many output slices, or no workspace), with and without accumulate; and
+# against the oracle's norm of the oracle's product.
+@pytest.mark.parametrize("rows,out_dim,in_dim,ws", [
+    (64, 4096, 4096, 32 << 20), (8, 4096, 11008, 32 << 20), (17, 1024, 1000, 32 << 20),
+    (33, 12288, 4096, 32 << 20), (64, 4096, 4096, 0)])
+def test_linear_packed_rmsnorm(rows, out_dim, in_dim, ws):
+    rng = np.random.default_rng(rows + out_dim + 13)
+    k = round(np.log2(in_dim) / 2)
+    xb, wb, yb, gb = (_bits(rng, (rows, in_dim)), _bits(rng, (out_dim, in_dim), k), _bits(rng, (rows, out_dim)),
+                      _bits(rng, (out_dim,)))
+    g = PL.Gemm(ws_bytes=ws)
+    wp = g.pack(_dev(wb))
+    x, gain = _dev(xb), _dev(gb)
+    for acc in (False, True):
+        y_ref, y = _dev(yb), _dev(yb)
+        n_ref = torch.empty_like(y)
+        n = torch.full_like(y, float("nan"))
+        g.linear_packed(x, wp, y_ref, accumulate=acc)
+        PL.rmsnorm(y_ref, gain, n_ref, 1e-5)
+        g.linear_packed_rmsnorm(x, wp, y, gain, 1e-5, n, accumulate=acc)
+        torch.cuda.synchronize()
+        assert np.array_equal(parity.host_bits(y), parity.host_bits(y_ref)), f"y (accumulate={acc})"
+        assert np.array_equal(parity.host_bits(n), parity.host_bits(n_ref)), f"y_norm (accumulate={acc})"
+        want = LL.linear(O.widen(xb, O.BF16), O.widen(wb, O.BF16)) + (O.widen(yb, O.BF16) if acc else 0.0)
+        _close(_val(y), want, what="linear_packed_rmsnorm y")
+        _close(_val(n), LL.rmsnorm(_val(y), O.widen(gb, O.BF16), 1e-5), atol=1e-6, what="y_norm")
+    g.close()
+
+
 def test_rmsnorm_and_silu_mul():
     rng = np.random.default_rng(11)
     xb, gb = _bits(rng, (7, 4096)), _bits(rng, (4096,))
