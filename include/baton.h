@@ -401,6 +401,21 @@ baton_status baton_linear_packed_rmsnorm(int32_t dtype, const void* x, const voi
                                          float eps, void* y_norm, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The gated feed-forward's first half in one call: y[r][j] = silu(g) * u with
+ * g = x[r] . W[j], u = x[r] . W[F + j] (each rounded to bf16 as
+ * baton_linear_packed would round them), silu(z) = z / (1 + e^-z), for
+ * j < F = out_dim / 2 -- bit for bit baton_linear_packed with ws_bytes = 0
+ * (the k-sum unsplit) into a [rows][out_dim] buffer followed by
+ * baton_silu_mul, without writing or reading that buffer or a second launch.  W is [gate; up] ([out_dim][in_dim],
+ * gate rows first) in its packed form wp; x device [rows <= 64][in_dim], y
+ * device [rows][F].  Never splits along in_dim (no workspace).
+ * Errors: EINVAL (null or misaligned pointer, rows outside 1..64, out_dim not a
+ * positive multiple of 32, in_dim < 8 or not a multiple of 8), EDTYPE, EHIP.
+ */
+baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                      int32_t out_dim, int32_t in_dim, hipStream_t stream);
+
+/*
  * y[r] = x[r] / sqrt(mean_j x[r][j]^2 + eps) * gain: x, y device [rows][dim],
  * gain device [dim]; dim a multiple of 8.  y may alias x.
  * Errors: EINVAL (null or misaligned pointer, bad sizes, eps < 0), EDTYPE.

@@ -78,6 +78,7 @@ def lib():
         L.baton_linear_packed.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, vp, ctypes.c_size_t, vp]
         L.baton_linear_packed_rmsnorm.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, vp, ctypes.c_float, vp,
                                                   vp, ctypes.c_size_t, vp]
+        L.baton_linear_packed_silu.argtypes = [i32, vp, vp, vp, i32, i32, i32, vp]
         L.baton_rmsnorm.argtypes = [i32, vp, vp, vp, i32, i32, ctypes.c_float, vp]
         L.baton_rope_qkv.argtypes = [vp, vp, vp, vp, vp, ctypes.c_float, vp]
         L.baton_silu_mul.argtypes = [i32, vp, vp, i32, i32, vp]
@@ -89,7 +90,7 @@ def lib():
                      "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
                      "baton_shape_insert", "baton_cache_tokens", "baton_kv_move", "baton_gemm_create",
                      "baton_gemm_destroy", "baton_linear", "baton_linear_pack", "baton_linear_packed",
-                     "baton_linear_packed_rmsnorm",
+                     "baton_linear_packed_rmsnorm", "baton_linear_packed_silu",
                      "baton_rmsnorm", "baton_rope_qkv", "baton_silu_mul"):
             getattr(L, name).restype = st
         _lib = L
@@ -255,6 +256,11 @@ def baton_linear_packed_rmsnorm(dtype, x, wp, y, rows, out_dim, in_dim, accumula
     _check(lib().baton_linear_packed_rmsnorm(dtype, _ptr(x), _ptr(wp), _ptr(y), rows, out_dim, in_dim,
                                              int(accumulate), _ptr(gain), float(eps), _ptr(y_norm), _ptr(ws),
                                              ws_bytes, _stream(stream)), "baton_linear_packed_rmsnorm")
+
+
+def baton_linear_packed_silu(dtype, x, wp, y, rows, out_dim, in_dim, stream=None):
+    _check(lib().baton_linear_packed_silu(dtype, _ptr(x), _ptr(wp), _ptr(y), rows, out_dim, in_dim,
+                                          _stream(stream)), "baton_linear_packed_silu")
 
 
 def baton_rmsnorm(dtype, x, gain, y, rows, dim, eps, stream=None):

@@ -182,6 +182,7 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   a.kt = kt;
   a.tc = tc;
   a.accumulate = accumulate;
+  a.gated = 0;
   const dim3 grid((unsigned)((slices + baton::kGemmWaves - 1) / baton::kGemmWaves), (unsigned)S);
   switch ((rows + 15) / 16) {
     case 1: launch_skinny_mg<1>(a, grid, stream); break;
@@ -223,6 +224,35 @@ baton_status baton_linear_packed_rmsnorm(int32_t dtype, const void* x, const voi
   if (!gain) return BATON_EINVAL;
   return linear_packed(dtype, x, wp, y, rows, out_dim, in_dim, accumulate, gain, eps, y_norm, ws, ws_bytes,
                        stream);
+}
+
+baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
+                                      int32_t out_dim, int32_t in_dim, hipStream_t stream) {
+  if (!x || !wp || !y || rows < 1 || rows > 64 || out_dim < 32 || out_dim % 32 || in_dim < 8 || in_dim % 8 ||
+      in_dim > (1 << 24))
+    return BATON_EINVAL;
+  if (dtype != BATON_BF16) return BATON_EDTYPE;
+  if (!aligned16(x) || !aligned16(wp) || !aligned16(y)) return BATON_EINVAL;
+  baton::SkinnyArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.wp = static_cast<const uint16_t*>(wp);
+  a.y = static_cast<uint16_t*>(y);
+  a.part = nullptr;
+  a.rows = rows;
+  a.N = out_dim;
+  a.K = in_dim;
+  a.kt = (in_dim + 31) / 32;
+  a.tc = a.kt;   // never split along k: the epilogue needs the whole sum
+  a.accumulate = 0;
+  a.gated = out_dim / 2;
+  const dim3 grid((unsigned)((out_dim / 32 + 1) / 2), 1);   // two gate slices per workgroup
+  switch ((rows + 15) / 16) {
+    case 1: launch_skinny_mg<1>(a, grid, stream); break;
+    case 2: launch_skinny_mg<2>(a, grid, stream); break;
+    case 3: launch_skinny_mg<3>(a, grid, stream); break;
+    default: launch_skinny_mg<4>(a, grid, stream); break;
+  }
+  return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
 }
 
 baton_status baton_rmsnorm(int32_t dtype, const void* x, const void* gain, void* y, int32_t rows, int32_t dim,

@@ -141,6 +141,7 @@ struct SkinnyArgs {
   int32_t kt;            // blocks per slice, ceil(K / 32)
   int32_t tc;            // blocks per split
   int32_t accumulate;    // 1: y += x . w^T
+  int32_t gated;         // F > 0: w is [gate; up] (2F rows), y [rows][F] = silu(x . gate^T) * (x . up^T)
 };
 
 #ifndef BATON_GEMM_WAVES
@@ -185,7 +186,11 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave, c16 = lane % 16, g4 = lane / 16;
-  const int32_t slice = blockIdx.x * kGemmWaves + w;
+  // Gated: waves 0 and 1 take gate slices 2 x and 2 x + 1, waves 2 and 3 the
+  // up slices of the same output columns (F / 16 further).
+  static_assert(kGemmWaves == 4, "the gated epilogue pairs two gate and two up slices");
+  const int32_t slice = a.gated ? (w < 2 ? 2 * (int32_t)blockIdx.x + w : a.gated / 16 + 2 * (int32_t)blockIdx.x + w - 2)
+                                : (int32_t)blockIdx.x * kGemmWaves + w;
   const int32_t n0 = slice * 16;
   const int32_t n_rows = max(0, min(16, a.N - n0));   // 0: a wave past N (loads nothing, writes nothing)
   const int32_t t_begin = blockIdx.y * a.tc, t_end = min(a.kt, t_begin + a.tc);
@@ -280,6 +285,39 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
 #undef BATON_GEMM_STEP
   }
   const int32_t n = n0 + 4 * g4;
+  if (a.gated) {
+    // The up waves hand their outputs, rounded to bf16 as the product's output
+    // would be, to the gate waves through LDS (free: the loop ended on a
+    // barrier); lane l of both holds the same (row, column).  The activation
+    // is then silu_mul_kernel's arithmetic on the rounded values.
+    uint2* ex = reinterpret_cast<uint2*>(&xs[0][0]);   // [2 waves][MG][64 lanes]
+    if (w >= 2) {
+#pragma unroll
+      for (int j = 0; j < MG; ++j)
+        ex[((w - 2) * MG + j) * kWave + lane] =
+            make_uint2(pack_bf16(acc[j][0], acc[j][1]), pack_bf16(acc[j][2], acc[j][3]));
+    }
+    __syncthreads();
+    if (w < 2 && n < a.gated) {
+#pragma unroll
+      for (int j = 0; j < MG; ++j) {
+        const int32_t m = 16 * j + c16;
+        if (m >= a.rows) continue;
+        const uint2 u = ex[(w * MG + j) * kWave + lane];
+        const uint32_t gw[2] = {pack_bf16(acc[j][0], acc[j][1]), pack_bf16(acc[j][2], acc[j][3])};
+        const uint32_t uw[2] = {u.x, u.y};
+        uint32_t o[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const float g0 = bf16_lo(gw[q]), g1 = bf16_hi(gw[q]);
+          const float s0 = g0 / (1.f + expf(-g0)), s1 = g1 / (1.f + expf(-g1));
+          o[q] = pack_bf16(s0 * bf16_lo(uw[q]), s1 * bf16_hi(uw[q]));
+        }
+        *reinterpret_cast<uint2*>(a.y + (int64_t)m * a.gated + n) = make_uint2(o[0], o[1]);
+      }
+    }
+    return;
+  }
   if (n >= a.N) return;
 #pragma unroll
   for (int j = 0; j < MG; ++j) {

@@ -66,6 +66,18 @@ class Gemm:
                               self.ws.numel(), _stream())
         return y
 
+    def linear_packed_silu(self, x, wp, out):
+        """out = silu(x . gate^T) * (x . up^T) for the packed [gate; up] weight wp
+        (bit for bit linear_packed unsplit, then silu_mul, in one kernel)."""
+        rows, in_dim = x.shape
+        if in_dim != wp.in_dim or tuple(out.shape) != (rows, wp.out_dim // 2):
+            raise ValueError("linear_packed_silu: shapes do not match")
+        for t in (x, out):
+            if not t.is_contiguous():
+                raise ValueError("linear_packed_silu: contiguous tensors only")
+        B.baton_linear_packed_silu(B.BATON_BF16, x, wp.data, out, rows, wp.out_dim, in_dim, _stream())
+        return out
+
     def linear_packed_rmsnorm(self, x, wp, y, gain, eps, y_norm, accumulate=False):
         """linear_packed, then y_norm = rmsnorm(y, gain, eps) (bit for bit; one
         kernel adds the split sums and normalises when the product splits)."""
@@ -121,7 +133,8 @@ class DecodeLayers:
     weights, made here once (packed=False keeps hipBLASLt on the stored weights).
     On the packed path each residual add is fused with the normalisation that
     follows it (the output projection with norm2, the down projection with the
-    next layer's norm1), so layer(l + 1) expects x as layer(l) returned it."""
+    next layer's norm1), so layer(l + 1) expects x as layer(l) returned it, and
+    the gate/up projection with the gated activation."""
 
     PROJ = ("qkv", "o", "gate_up", "down")
 
@@ -158,8 +171,11 @@ class DecodeLayers:
         else:
             lin(att, wp["o"], x, accumulate=True)
             rmsnorm(x, w["norm2"], self.h, self.eps)
-        lin(self.h, wp["gate_up"], self.gu)
-        silu_mul(self.gu, self.act)
+        if self.packed and wp["gate_up"].out_dim % 32 == 0:
+            self.gemm.linear_packed_silu(self.h, wp["gate_up"], self.act)
+        else:
+            lin(self.h, wp["gate_up"], self.gu)
+            silu_mul(self.gu, self.act)
         if self.packed and layer + 1 < len(self.w):
             self.gemm.linear_packed_rmsnorm(self.act, wp["down"], x, self.w[layer + 1]["norm1"], self.eps, self.h,
                                             accumulate=True)

@@ -169,3 +169,10 @@ def test_packed_linear_host_checks():
     assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G, -1.0, N, 0, 0) == B.BATON_EINVAL      # eps < 0
     assert status(lpn, B.BATON_BF16, X, W, Y, 65, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EINVAL     # rows > 64
     assert status(lpn, B.BATON_F32, X, W, Y, 8, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EDTYPE
+    lps = B.baton_linear_packed_silu
+    assert status(lps, B.BATON_BF16, X, W, 0, 8, 64, 64) == B.BATON_EINVAL       # null y
+    assert status(lps, B.BATON_BF16, X, W, Y, 8, 48, 64) == B.BATON_EINVAL       # out % 32
+    assert status(lps, B.BATON_BF16, X, W, Y, 65, 64, 64) == B.BATON_EINVAL      # rows > 64
+    assert status(lps, B.BATON_BF16, X, W + 8, Y, 8, 64, 64) == B.BATON_EINVAL   # misaligned
+    assert status(lps, B.BATON_BF16, X, W, Y, 8, 64, 60) == B.BATON_EINVAL       # in % 8
+    assert status(lps, B.BATON_F32, X, W, Y, 8, 64, 64) == B.BATON_EDTYPE

@@ -133,6 +133,36 @@ def test_linear_packed_rmsnorm(rows, out_dim, in_dim, ws):
     g.close()
 
 
+# The gate/up projection with the gated activation in its epilogue against
+# linear_packed (unsplit) into a [gate; up] buffer then silu_mul, bit for bit
+# (33 x 2048 x 1000 is a product linear_packed would split): llama2-7b's
+# gate/up at 64 and 8 rows, an odd number of 16-column gate slices (48 columns:
+# the last workgroup's second gate wave has none), rows not a multiple of 16;
+# and against the oracle.
+@pytest.mark.parametrize("rows,F,in_dim", [(64, 11008, 4096), (8, 11008, 4096), (17, 48, 136), (33, 1024, 1000)])
+def test_linear_packed_silu(rows, F, in_dim):
+    rng = np.random.default_rng(rows + F + 17)
+    k = round(np.log2(in_dim) / 2)
+    xb, wb = _bits(rng, (rows, in_dim)), _bits(rng, (2 * F, in_dim), k)
+    g = PL.Gemm()
+    g0 = PL.Gemm(ws_bytes=0)   # the reference product unsplit, as the fused kernel sums it
+    wp = g.pack(_dev(wb))
+    x = _dev(xb)
+    gu = torch.empty((rows, 2 * F), dtype=torch.bfloat16, device="cuda")
+    ref = torch.empty((rows, F), dtype=torch.bfloat16, device="cuda")
+    g0.linear_packed(x, wp, gu)
+    PL.silu_mul(gu, ref)
+    out = torch.full((rows, F), float("nan"), dtype=torch.bfloat16, device="cuda")
+    g.linear_packed_silu(x, wp, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(parity.host_bits(out), parity.host_bits(ref)), "fused against linear_packed + silu_mul"
+    guv = _val(gu)
+    _close(guv, LL.linear(O.widen(xb, O.BF16), O.widen(wb, O.BF16)), what="gate_up")
+    _close(_val(out), LL.silu(guv[:, :F]) * guv[:, F:], atol=1e-6, what="silu(gate) * up")
+    g.close()
+    g0.close()
+
+
 def test_rmsnorm_and_silu_mul():
     rng = np.random.default_rng(11)
     xb, gb = _bits(rng, (7, 4096)), _bits(rng, (4096,))
