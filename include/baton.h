@@ -327,9 +327,11 @@ baton_status baton_set_split_tokens(baton_cache* cache, int32_t tokens);
  * The paper serves llama2-7b (sec. 5; its layers as sec. 2.1 describes them:
  * W^Q, W^K, W^V projections, attention, feed-forward networks between).
  * These calls are the rest of such a layer, so that a decode step runs end to
- * end: RMS normalisation, the projections (hipBLASLt GEMMs), rotary position
- * embedding at each query's own position, the gated feed-forward.  bf16 only;
- * every output is rounded to nearest even.
+ * end: RMS normalisation, the projections (the library's weight-streaming
+ * kernel on packed weights up to 64 rows, hipBLASLt GEMMs on stored weights),
+ * rotary position embedding at each query's own position, the gated
+ * feed-forward, and fused forms of the projections with the step that follows
+ * them.  bf16 only; every output is rounded to nearest even.
  */
 typedef struct baton_gemm baton_gemm; /* opaque: a hipBLASLt handle and its cached algorithm choices */
 
