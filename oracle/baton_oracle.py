@@ -74,7 +74,9 @@ NEG_INF_BITS = {F32: 0xFF800000, BF16: 0xFF80}
 
 # ----------------------------------------------------------------- numbers --
 def widen(bits, dtype):
-    """Stored bits (uint32 fp32 / uint16 bf16) -> float64, exactly."""
+    """Stored bits (uint32 fp32 / uint16 bf16) -> float64, exactly.  A bf16
+    value is the upper half of the fp32 word with the same bits (sign, 8
+    exponent bits, 7 mantissa bits), so its widening is a 16-bit shift."""
     bits = np.asarray(bits)
     if dtype == BF16:
         return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
@@ -119,23 +121,14 @@ def expected_row_masked(mask_row, hist_row, fill_bits, dtype):
     return out
 
 
-def expected_row(L, n, hist_row, fill_bits, dtype):
-    """A live row of the aligned cache: L - n placeholders, then the n history rows."""
-    hist_row = np.asarray(hist_row)
-    D = hist_row.shape[-1]
-    out = np.full((L, D), fill_bits, dtype=STORAGE[dtype])
-    out[L - n:] = hist_row
-    return out
-
-
 # ------------------------------------------------------------ padded batch --
 class PaddedBatch:
     """The paper's batch: aligned KV_Cache + attention_mask + per-query histories.
 
     K, V: [n_layers][batch][n_kv_heads][L][head_dim] stored bits.  With
     materialize=False only the lengths are tracked -- no tensors, no histories --
-    for large workloads whose rows are checked one at a time with expected_row
-    and attend.
+    for large workloads whose rows are checked one at a time against histories
+    rebuilt from the input generator, with attend.
     """
 
     def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, dtype,

@@ -18,6 +18,51 @@ def _load(name):
         return json.load(f)
 
 
+# ---------------------------------------------------------------- numbers --
+def pin_widen_worked(O):
+    """Stored bit patterns widened by hand.  bf16 (sign, 8 exponent bits, bias
+    127, 7 mantissa bits): 0x3F80 = +2^0 x 1.0; 0xC020 = -2^1 x 1.25; 0x0001 is
+    the smallest subnormal, 2^-126 x 2^-7; 0x0080 the smallest normal, 2^-126;
+    0x7F7F the largest finite, 2^127 x (2 - 2^-7); 0x4049 = 2^1 x (1 + 73/128).
+    fp32 the same with 23 mantissa bits."""
+    inf = math.inf
+    bf16 = [(0x3F80, 1.0), (0xC020, -2.5), (0x0001, 2.0 ** -133), (0x0080, 2.0 ** -126),
+            (0x7F7F, (2.0 - 2.0 ** -7) * 2.0 ** 127), (0xFF80, -inf), (0x7F80, inf), (0x4049, 3.140625),
+            (0x3F81, 1.0 + 2.0 ** -7), (0x3F7F, 1.0 - 2.0 ** -8), (0x8001, -(2.0 ** -133))]
+    f32 = [(0x3F800000, 1.0), (0xC0200000, -2.5), (0x00000001, 2.0 ** -149), (0x00800000, 2.0 ** -126),
+           (0x7F7FFFFF, (2.0 - 2.0 ** -23) * 2.0 ** 127), (0xFF800000, -inf), (0x3F800001, 1.0 + 2.0 ** -23)]
+    for dtype, cases, st in ((O.BF16, bf16, np.uint16), (O.F32, f32, np.uint32)):
+        got = O.widen(np.array([b for b, _ in cases], st), dtype)
+        want = np.array([v for _, v in cases])
+        assert np.array_equal(got, want), (dtype, got, want)
+    # the sign of zero is kept, and NaN patterns stay NaN
+    z = O.widen(np.array([0x8000, 0x0000], np.uint16), O.BF16)
+    assert z[0] == 0.0 and math.copysign(1.0, z[0]) == -1.0 and math.copysign(1.0, z[1]) == 1.0
+    assert np.all(np.isnan(O.widen(np.array([0x7FC0, 0xFFC1, 0x7F81], np.uint16), O.BF16)))
+
+
+def pin_widen_exhaustive(O):
+    """Every one of the 65,536 bf16 patterns against torch's bfloat16 type read
+    as float64 (a library routine), and a sample of fp32 patterns against the
+    C library's single-precision unpacking (struct)."""
+    import struct
+
+    import torch
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).double().numpy()
+    got = O.widen(bits, O.BF16)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan]) and np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+    rng = np.random.default_rng(17)
+    words = np.concatenate([rng.integers(0, 1 << 32, 4096, dtype=np.uint64).astype(np.uint32),
+                            np.array([0, 1, 0x7F7FFFFF, 0x80000000, 0x00800000, 0xFF800000], np.uint32)])
+    ref32 = np.array([struct.unpack("<f", struct.pack("<I", int(u)))[0] for u in words])
+    got32 = O.widen(words, O.F32)
+    nan = np.isnan(ref32)
+    assert np.array_equal(np.isnan(got32), nan) and np.array_equal(got32[~nan], ref32[~nan])
+
+
 # ------------------------------------------------------------- attention --
 def pin_attention_worked(O):
     """Hand-worked single-query cases (tests/golden/attention_worked.json, sec. 2.1)."""
@@ -365,7 +410,7 @@ def pin_error_paths(O):
         assert (pb.L, list(pb.lens)) == before[:2] and np.array_equal(pb.K, before[2])
 
 
-ALL_PINS = [pin_attention_worked, pin_attention_closed_forms, pin_attention_sdpa,
+ALL_PINS = [pin_widen_worked, pin_widen_exhaustive, pin_attention_worked, pin_attention_closed_forms, pin_attention_sdpa,
             pin_attention_permutation, pin_insertion_replay, pin_gqa_mapping,
             pin_isolation_invariant, pin_layout_invariants, pin_embed_order_and_release,
             pin_brute_force_small, pin_placeholder_poison, pin_error_paths]

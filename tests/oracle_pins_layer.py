@@ -139,5 +139,33 @@ def pin_layer_mlp(L):
     assert np.allclose(out, want, atol=1e-12)
 
 
+def pin_layer_stored_bf16(L):
+    """decode_layer(stored=bf16) rounds where the GPU stores, worked by hand on
+    one query of one cached token (D = hidden = 8, every element alike).
+    x = 1.2578125 (bf16 exact), unit gains, eps = 0: the normalised stream is
+    exactly 1.  Zero q and k rows make both tokens weigh 1/2; the v rows are
+    1.015625 on the diagonal, the cached value 1.0078125, so the attention is
+    1.01171875 = 1 + 2^-7 + 2^-8, halfway between two bf16 values: stored, it
+    rounds to the even one, 1.015625.  The identity output projection adds it:
+    2.2734375, halfway between 2.265625 and 2.28125 (spacing 2^-6 above 2), so
+    2.28125.  The zero feed-forward adds nothing.  Unrounded the layer gives
+    2.26953125."""
+    import oracle.baton_oracle as O
+    D = 8
+    pb = O.PaddedBatch(1, 1, 1, 1, D, O.BF16)
+    pb.embed([0], [1], [np.zeros((1, 1, 1, D), np.uint16)], [np.full((1, 1, 1, D), 0x3F81, np.uint16)])
+    qkv = np.zeros((3 * D, D))
+    qkv[2 * D:] = np.eye(D) * 1.015625
+    w = {"norm1": np.ones(D), "qkv": qkv, "o": np.eye(D), "norm2": np.ones(D),
+         "gate_up": np.zeros((2 * D, D)), "down": np.zeros((D, D))}
+    x = np.full((1, D), 1.2578125)
+    out = L.decode_layer(pb, 0, x, w, [1], 10000.0, 0.0, stored=L.BF16)
+    assert np.array_equal(out, np.full((1, D), 2.28125)), out
+    pb2 = O.PaddedBatch(1, 1, 1, 1, D, O.BF16)
+    pb2.embed([0], [1], [np.zeros((1, 1, 1, D), np.uint16)], [np.full((1, 1, 1, D), 0x3F81, np.uint16)])
+    assert np.array_equal(L.decode_layer(pb2, 0, x, w, [1], 10000.0, 0.0), np.full((1, D), 2.26953125))
+
+
 ALL_PINS = [pin_rmsnorm, pin_rope, pin_silu, pin_linear_and_split, pin_to_bits, pin_layer_residual,
             pin_layer_mlp]
+ALL_PINS.append(pin_layer_stored_bf16)

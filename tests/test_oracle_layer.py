@@ -59,6 +59,12 @@ def _bits_truncate(x, dtype):
     return f.copy() if dtype == L.F32 else (f >> np.uint32(16)).astype(np.uint16)
 
 
+def _widen_bf16_as_fp16(bits, dtype):
+    if dtype == L.BF16:
+        return np.asarray(bits).astype(np.uint16).view(np.float16).astype(np.float64)
+    return L.widen(bits, dtype)
+
+
 MUTANTS = {
     "rope pairs interleaved": dict(rope=_rope_interleaved),
     "rope rotates backwards": dict(rope=_rope_backwards),
@@ -66,6 +72,7 @@ MUTANTS = {
     "silu is a sigmoid": dict(silu=_silu_sigmoid),
     "k and v swapped in the fused projection": dict(split_qkv=_split_kv_swapped),
     "bf16 by truncation": dict(to_bits=_bits_truncate),
+    "stored bf16 read back as fp16": dict(widen=_widen_bf16_as_fp16),
 }
 
 

@@ -195,6 +195,23 @@ def _advance_span_by_one(self):
         self.lens[b] -= T - 1
 
 
+def _widen_bf16_as_fp16(bits, dtype):
+    if dtype == O.BF16:
+        return np.asarray(bits).astype(np.uint16).view(np.float16).astype(np.float64)
+    return O.widen(bits, dtype)
+
+
+def _widen_shift_15(bits, dtype):
+    if dtype == O.BF16:
+        return (np.asarray(bits).astype(np.uint32) << np.uint32(15)).view(np.float32).astype(np.float64)
+    return O.widen(bits, dtype)
+
+
+def _widen_flush_subnormals(bits, dtype):
+    x = O.widen(bits, dtype)
+    return np.where(np.abs(x) < 2.0 ** -126, 0.0 * x, x)
+
+
 MUTANTS = {
     "scale dropped": dict(attend=_attend_no_scale),
     "keys and values swapped": dict(attend=_attend_kv_swapped),
@@ -215,6 +232,9 @@ MUTANTS = {
     "padding in front of the latest token": dict(PB_mask=_mask_padding_in_front),
     "shorter prompt start-aligned": dict(PB__positions=_positions_start_aligned),
     "span grows by one in a prefill step": dict(PB_advance=_advance_span_by_one),
+    "bf16 bits read as fp16": dict(widen=_widen_bf16_as_fp16),
+    "bf16 widened by a 15-bit shift": dict(widen=_widen_shift_15),
+    "subnormals flushed to zero": dict(widen=_widen_flush_subnormals),
 }
 
 
