@@ -6,15 +6,20 @@ embed the newly prefilled queries end-aligned (growing the batch on the left
 when one is longer), build the mask, then masked decode attention layer by
 layer (appending each layer's new key/value column), then advance.
 
-Default workload (7b-b64-L4096): bf16, 32 layers x 32 heads x head_dim 128
-(7B-shaped attention), batch 64, initial padded length 4096, lengths
-lognormal(6.5, 0.8) clipped to [32, 4096], Poisson(4) arrivals per step with
-as many queries finishing, 64 decode steps (warmup + timed).  All inputs are
-synthetic and seeded, generated into HBM before the timed region.
+Default workload (70b-gqa-b128-L8192), the largest configuration: bf16,
+grouped-query attention with 64 query heads over 8 kv-heads, head_dim 128,
+batch 128, initial padded length 8192, lengths uniform in [256, 8192], 8
+queries finishing and 8 prefilled queries inserted per step.  The dense
+padded cache of all 80 layers (343.6 GB) exceeds the GPU's 288 GB, so 24 of
+the 80 layers are resident and each step decodes those 24, each at the real
+per-layer shape.  All inputs are synthetic and seeded, generated into HBM
+before the timed region.  The 7B-shaped workload (7b-b64-L4096: 32 layers x 32
+heads, batch 64, L 4096) runs after it and is reported under "also".
 
 Prints one JSON line: query-tokens/s of whole steps, the dominant kernel's
-roofline (decode attention, HBM-bound), per-op HBM GB/s, and the CPU oracle
-timed on a bounded sample on this host.
+roofline (decode attention, HBM-bound), per-op HBM GB/s (kv_embed with and
+without the placeholder writes of scrubbing evictions), and the CPU oracle
+timed on a bounded sample on this host's cores.
 """
 import argparse
 import gc
@@ -29,20 +34,27 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-DEFAULT_WORKLOAD = "7b-b64-L4096"
 GQA_WORKLOAD = "70b-gqa-b128-L8192"   # 80 layers' padded cache exceed HBM: a resident subset
+GQA_LAYERS, GQA_RESIDENT = 80, 24
+DEFAULT_WORKLOAD = GQA_WORKLOAD
+SECONDARY_WORKLOAD = "7b-b64-L4096"
+# rocprofv3 FETCH_SIZE / WRITE_SIZE records of decode attention, by workload:
+# traffic over algorithmic bytes, valid for the kernel sources they were taken on
+TRAFFIC = {GQA_WORKLOAD: "decode_attn_70b_gqa_b128_L8192_traffic.json",
+           "7b-b64-L4096": "decode_attn_7b_b64_L4096_traffic.json"}
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=60)
+    p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=4)
     p.add_argument("--config", default=DEFAULT_WORKLOAD,
                    choices=["b32-L2048", "7b-b64-L4096", "70b-gqa-b128-L8192", "skew-b256-L32768",
                             "skew-growth-b256-L32768"])
     p.add_argument("--layers", type=int, default=None,
-                   help="resident layers (70b-gqa-b128-L8192's 80-layer padded cache exceeds HBM; default 24 there)")
+                   help=f"resident layers (70b-gqa-b128-L8192's 80-layer padded cache exceeds HBM; "
+                        f"default {GQA_RESIDENT} there)")
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
     p.add_argument("--no-pd", action="store_true",
                    help="prefill the new queries inside the batch (no prefill/decode separation) "
@@ -50,14 +62,24 @@ def parse():
     p.add_argument("--model", default=None, choices=["llama2-7b"],
                    help="run whole decode layers of this model (synthetic weights) around the attention")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=20, help="layers of step 0 the oracle runs")
+    p.add_argument("--cpu-workers", type=int, default=16,
+                   help="most worker processes of the CPU oracle's all-cores run (the host's cores, at most this)")
+    p.add_argument("--no-scrub-steps", type=int, default=8,
+                   help="steps after the timed ones whose evictions do not scrub, timed for kv_embed alone (0: skip)")
+    p.add_argument("--no-secondary", action="store_true",
+                   help=f"skip the {SECONDARY_WORKLOAD} run reported under 'also'")
     p.add_argument("--copy-bytes", type=int, default=2 << 30,
                    help="size of the plain device copy timed as the achievable-bandwidth reference (0: skip)")
-    p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "decode_attn_7b_b64_L4096_traffic.json"),
-                   help="rocprofv3-derived HBM bytes per decode_attn launch (FETCH_SIZE/WRITE_SIZE, "
-                        "scaled by a copy of known size); used only for the workload it was measured "
-                        "on and while the kernel sources are unchanged")
+    p.add_argument("--traffic-dir", default=os.path.join(ROOT, "profiles"),
+                   help="where the rocprofv3-derived traffic records of decode attention are (FETCH_SIZE/"
+                        "WRITE_SIZE scaled by a copy of known size, as a ratio to the algorithmic bytes); a "
+                        "record is used only for its workload and while the kernel sources are unchanged")
     return p.parse_args()
+
+
+def log(msg):
+    """A progress line on stderr (the JSON result is the only line on stdout)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def attn_bytes(w, lens):
@@ -270,52 +292,104 @@ def bench_model(args, w):
     }
 
 
-def cpu_baseline(w, n_layers):
-    """The oracle, timed on this host over step 0 of the workload for n_layers
-    layers (one layer of the batch at a time), scaled to query-tokens/s of the
-    whole step.  Input generation is outside the timed part."""
-    import numpy as np
+def _oracle_share(w, share, n_shares, barrier, out):
+    """One worker of the CPU baseline (a forked process, one thread): the
+    oracle over the slots b with b % n_shares == share of layer 0 of the
+    workload's initial batch, then step 0 (evict, embed, mask, attention,
+    advance) timed.  Worker 0 first runs its share alone (on a copy), while
+    the others wait: the single-thread figure."""
+    import copy
+
     from threadpoolctl import threadpool_limits
 
     import oracle.baton_oracle as O
     from workload import gen
 
-    ev = w.steps[0]
-    elapsed = 0.0
-    live_after = None
     with threadpool_limits(limits=1):
-        for layer in range(n_layers):
-            pb = O.PaddedBatch(1, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype)
+        layer = 0
+        mine = [b for b in range(w.batch) if b % n_shares == share]
+        ev = w.steps[0]
+        pb = O.PaddedBatch(1, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype)
 
-            def layer_src(qid, n):
-                c0, st = gen.prefill_counter(qid, w.n_layers, w.n_kv_heads, w.head_dim, layer0=layer)
-                shp = (1, w.n_kv_heads, n, w.head_dim)
-                return (gen.fill_host(w.seed, gen.S_PREFILL_K, w.dtype, shp, c0, st),
-                        gen.fill_host(w.seed, gen.S_PREFILL_V, w.dtype, shp, c0, st))
+        def layer_src(qid, n):
+            c0, st = gen.prefill_counter(qid, w.n_layers, w.n_kv_heads, w.head_dim, layer0=layer)
+            shp = (1, w.n_kv_heads, n, w.head_dim)
+            return (gen.fill_host(w.seed, gen.S_PREFILL_K, w.dtype, shp, c0, st),
+                    gen.fill_host(w.seed, gen.S_PREFILL_V, w.dtype, shp, c0, st))
 
-            # the initial batch, longest query first so the batch grows once
-            order = sorted(range(w.batch), key=lambda b: -w.init_lens[b])
-            init = [layer_src(b, w.init_lens[b]) for b in order]
-            pb.embed(order, [w.init_lens[b] for b in order], [x[0] for x in init], [x[1] for x in init])
-            del init
-            ins = [layer_src(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
-            dec = [gen.decode_host(w.seed, sid, 0, layer, w.n_layers, w.batch, h, w.head_dim, w.dtype)
-                   for sid, h in ((gen.S_Q, w.n_q_heads), (gen.S_KNEW, w.n_kv_heads),
-                                  (gen.S_VNEW, w.n_kv_heads))]
+        order = sorted(mine, key=lambda b: -w.init_lens[b])       # the longest first: one growth
+        init = [layer_src(b, w.init_lens[b]) for b in order]
+        pb.embed(order, [w.init_lens[b] for b in order], [x[0] for x in init], [x[1] for x in init])
+        del init
+        ev_slots = [b for b in ev.evict if b in mine]
+        ins = [(b, q, n) for b, q, n in zip(ev.insert, ev.insert_qids, ev.insert_lens) if b in mine]
+        srcs = [layer_src(q, n) for _, q, n in ins]
+        dec = [gen.decode_host(w.seed, sid, 0, layer, w.n_layers, w.batch, h, w.head_dim, w.dtype)
+               for sid, h in ((gen.S_Q, w.n_q_heads), (gen.S_KNEW, w.n_kv_heads), (gen.S_VNEW, w.n_kv_heads))]
+
+        def step(batch):
             t0 = time.perf_counter()
-            pb.evict(ev.evict, release=True)
-            pb.embed(ev.insert, ev.insert_lens, [x[0] for x in ins], [x[1] for x in ins])
-            pb.mask()
-            pb.decode_layer(0, dec[0], dec[1], dec[2])
-            pb.advance()
-            elapsed += time.perf_counter() - t0
-            live_after = len(pb.live())
-            del pb, ins
-    per_step = elapsed / n_layers * w.n_layers
-    return {"value": live_after / per_step, "unit": "query-tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"step 0 of {w.name} (evict, embed, mask, attention, advance) for layers "
-                      f"0..{n_layers - 1}, one layer at a time, numpy float64 on 1 thread; "
-                      f"{elapsed:.1f} s measured, scaled by {w.n_layers}/{n_layers} layers"}
+            batch.evict(ev_slots, release=True)
+            batch.embed([b for b, _, _ in ins], [n for _, _, n in ins], [x[0] for x in srcs], [x[1] for x in srcs])
+            batch.mask()
+            batch.decode_layer(0, dec[0], dec[1], dec[2])
+            batch.advance()
+            return t0, time.perf_counter(), len(batch.live())
+
+        barrier.wait()
+        if share == 0:
+            out.put(("solo",) + step(copy.deepcopy(pb)))
+        barrier.wait()
+        out.put(("all",) + step(pb))
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(w, max_workers):
+    """The oracle as it stands, timed on this host's cores over a bounded
+    sample of the workload: step 0 of layer 0 (evict, embed, mask, attention,
+    advance over the query histories), its 128 slots dealt over worker
+    processes of one thread each, all run together (the all-cores figure); the
+    first worker's share also run alone (the single-thread figure, scaled by
+    the number of shares).  Scaled to query-tokens/s of the benchmark's step
+    (all resident layers).  Runs before the GPU is initialised: the workers
+    are forked."""
+    import multiprocessing as mp
+    n = max(1, min(max_workers, len(os.sched_getaffinity(0)), w.batch))
+    ctx = mp.get_context("fork")
+    barrier, out = ctx.Barrier(n), ctx.Queue()
+    procs = [ctx.Process(target=_oracle_share, args=(w, i, n, barrier, out)) for i in range(n)]
+    for p in procs:
+        p.start()
+    res = [out.get() for _ in range(n + 1)]
+    for p in procs:
+        p.join()
+        if p.exitcode != 0:
+            raise RuntimeError(f"CPU oracle worker failed ({p.exitcode})")
+    solo = [r for r in res if r[0] == "solo"][0]
+    allr = [r for r in res if r[0] == "all"]
+    live = sum(r[3] for r in allr)
+    t_all = max(r[2] for r in allr) - min(r[1] for r in allr)     # one layer of the whole batch
+    t_solo = (solo[2] - solo[1]) * n                               # the share alone, scaled to the batch
+    step_all, step_solo = t_all * w.n_layers, t_solo * w.n_layers
+    return {"value": round(live / step_all, 3), "unit": "query-tokens/s", "cores": n, "kind": "oracle",
+            "single_thread_value": round(live / step_solo, 3),
+            "host": {"nproc": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()},
+            "sample": f"step 0 of {w.name}, layer 0 only (evict, embed, mask, attention over each query's "
+                      f"history, advance; numpy float64): its {w.batch} slots dealt over {n} single-thread "
+                      f"worker processes run together, {t_all:.2f} s wall; the first worker's share "
+                      f"({len(range(0, w.batch, n))} slots) alone {solo[2] - solo[1]:.2f} s, x{n} for the "
+                      f"single-thread figure; both x{w.n_layers} resident layers for the step.  Input "
+                      f"generation and the initial batch's embedding are outside the timed part."}
 
 
 def kernel_sources_sha256():
@@ -406,131 +480,145 @@ def read_probe(nbytes, reps=5, per_launch=False, n_bufs=1):
             "timing": "per launch" if per_launch else "back to back"}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); "
-              "the batch shards by slot or by kv-head with no exchange on this path.", file=sys.stderr)
-        sys.exit(2)
+def traffic_record(args, w):
+    """The decode-attention traffic ratio measured with rocprofv3 on this
+    workload, if it was taken on the current kernel sources."""
+    name = TRAFFIC.get(w.name)
+    if not name or args.split is not None:
+        return None
+    path = os.path.join(args.traffic_dir, name)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sources_sha256") != kernel_sources_sha256() or "traffic_over_algorithmic" not in rec:
+        return None
+    return rec
 
+
+def bench_decode(args, w, probes=True, no_scrub_steps=0):
+    """The timed decode steps of workload w (its schedule's first warmup +
+    steps steps, evictions scrubbing and releasing), then no_scrub_steps more
+    whose evictions leave their tokens (kv_embed timed without placeholder
+    writes).  Returns the result dict of the JSON line."""
     import torch
 
-    from workload import configs, driver
+    from workload import driver
 
-    torch.cuda.set_device(0)
+    copy_ref = copy_probe(args.copy_bytes) if probes and args.copy_bytes > 0 else None
+    read_ref = read_probe(2 * args.copy_bytes) if probes and args.copy_bytes > 0 else None
     total_steps = args.warmup + args.steps
-    if args.config == GQA_WORKLOAD:
-        w = configs.gqa70b_b128_l8192(total_steps, n_layers=args.layers or 24)
-    else:
-        w = configs.CONFIGS[args.config](total_steps)
-        if args.layers:
-            raise SystemExit(f"--layers applies to {GQA_WORKLOAD} only")
-    if args.no_pd:
-        print(json.dumps(bench_no_pd(args, w)), flush=True)
-        return
-    if args.model:
-        print(json.dumps(bench_model(args, w)), flush=True)
-        return
-    copy_ref = copy_probe(args.copy_bytes) if args.copy_bytes > 0 else None
-    read_ref = read_probe(2 * args.copy_bytes) if args.copy_bytes > 0 else None
+    log(f"{w.name}: building the initial batch ({w.n_layers} layers, {w.batch} slots)")
     cache, inputs = driver.open_cache(w, split=args.split)
     cap = cache.capacity
 
-    # Inputs of the timed steps, generated into HBM now.
-    need = sum(driver.prefill_bytes(w, n) for e in w.steps[args.warmup:] for n in e.insert_lens)
-    need += args.steps * w.n_layers * w.batch * (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes
-    free, _ = torch.cuda.mem_get_info()
-    if need + (2 << 30) > free:
-        sys.exit(f"timed inputs need {need / 1e9:.1f} GB, {free / 1e9:.1f} GB free: use fewer --steps")
+    def inputs_of(steps):
+        need = sum(driver.prefill_bytes(w, n) for s in steps for n in w.steps[s].insert_lens)
+        need += len(steps) * w.n_layers * w.batch * (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * w.elem_bytes
+        free, _ = torch.cuda.mem_get_info()
+        if need + (2 << 30) > free:
+            sys.exit(f"timed inputs need {need / 1e9:.1f} GB, {free / 1e9:.1f} GB free: use fewer --steps")
+        out = []
+        for s in steps:
+            ev = w.steps[s]
+            srcs = [inputs.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+            dec = [inputs.decode(s, layer) for layer in range(w.n_layers)]
+            out.append((srcs, dec))
+        return out
 
     for s in range(args.warmup):
         driver.run_step(cache, inputs, s, w.steps[s])
     torch.cuda.synchronize()
 
-    pre = []
-    for s in range(args.warmup, total_steps):
-        ev = w.steps[s]
-        srcs = [inputs.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
-        dec = [inputs.decode(s, layer) for layer in range(w.n_layers)]
-        pre.append((srcs, dec))
+    log(f"{w.name}: {args.warmup} warmup steps done; generating the timed steps' inputs")
+    pre = inputs_of(range(args.warmup, total_steps))
     mask_buf = torch.empty((w.batch, cap + 1), dtype=torch.uint8, device="cuda")
     ws = cache.workspace()
     outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=inputs.tdt, device="cuda")
             for _ in range(2)]
     torch.cuda.synchronize()
 
-    # Every event of the timed region exists (and has been recorded once) before
-    # it starts, and the collector is off, so the host never stalls the stream.
-    n_ev = 2 * args.steps * (3 + w.n_layers) + 2
-    pool = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
-    for e in pool:
-        e.record()
-    torch.cuda.synchronize()
-    pool_it = iter(pool)
-    E = lambda: next(pool_it)
-    ev_attn, ev_embed, ev_evict, ev_mask, ev_step = [], [], [], [], []
-    bytes_attn = bytes_embed = bytes_evict = 0
-    live_tokens = 0
-    gc.collect()
-    gc.disable()
-    t_start, t_end = E(), E()
-    torch.cuda.synchronize()
-    t_start.record()
-    for i, s in enumerate(range(args.warmup, total_steps)):
-        ev = w.steps[s]
-        srcs, dec = pre[i]
-        _, _, lens = cache.query()
-        a, b = E(), E()
-        a.record()
-        cache.evict(ev.evict, release=True)
-        b.record()
-        ev_evict.append((a, b))
-        bytes_evict += placeholder_bytes(w, lens, ev)
-        if ev.insert:
+    def timed(steps, pre, scrub):
+        """Runs the steps between events; every event exists (and has been
+        recorded once) before the timed region starts, and the collector is
+        off, so the host never stalls the stream."""
+        n_ev = 2 * len(steps) * (3 + w.n_layers) + 2
+        pool = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+        for e in pool:
+            e.record()
+        torch.cuda.synchronize()
+        pool_it = iter(pool)
+        E = lambda: next(pool_it)
+        r = {"attn": [], "embed": [], "evict": [], "mask": [], "step": [],
+             "bytes_attn": 0, "bytes_embed": 0, "bytes_evict": 0, "live": 0}
+        gc.collect()
+        gc.disable()
+        t_start, t_end = E(), E()
+        torch.cuda.synchronize()
+        t_start.record()
+        for i, s in enumerate(steps):
+            ev = w.steps[s]
+            srcs, dec = pre[i]
+            _, _, lens = cache.query()
             a, b = E(), E()
             a.record()
-            cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+            cache.evict(ev.evict, release=True, scrub=scrub)
             b.record()
-            ev_embed.append((a, b))
-            bytes_embed += embed_bytes(w, ev.insert_lens)
-        a, b = E(), E()
-        a.record()
-        cache.build_mask(out=mask_buf)
-        b.record()
-        ev_mask.append((a, b))
-        _, _, lens = cache.query()
-        step_attn = attn_bytes(w, lens)
-        for layer in range(w.n_layers):
-            q, kn, vn = dec[layer]
+            r["evict"].append((a, b))
+            if scrub:
+                r["bytes_evict"] += placeholder_bytes(w, lens, ev)
+            if ev.insert:
+                a, b = E(), E()
+                a.record()
+                cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+                b.record()
+                r["embed"].append((a, b))
+                r["bytes_embed"] += embed_bytes(w, ev.insert_lens)
             a, b = E(), E()
             a.record()
-            cache.decode_attn(layer, q, kn, vn, out=outs[layer & 1])
+            cache.build_mask(out=mask_buf)
             b.record()
-            ev_attn.append((a, b))
-            bytes_attn += step_attn
-        ev_step.append((ev_evict[-1][0], ev_attn[-1][1]))
-        live_tokens += sum(1 for n in lens if n > 0)
-        cache.advance()
-    t_end.record()
-    torch.cuda.synchronize()
-    gc.enable()
+            r["mask"].append((a, b))
+            _, _, lens = cache.query()
+            step_attn = attn_bytes(w, lens)
+            for layer in range(w.n_layers):
+                q, kn, vn = dec[layer]
+                a, b = E(), E()
+                a.record()
+                cache.decode_attn(layer, q, kn, vn, out=outs[layer & 1])
+                b.record()
+                r["attn"].append((a, b))
+                r["bytes_attn"] += step_attn
+            r["step"].append((r["evict"][-1][0], r["attn"][-1][1]))
+            r["live"] += sum(1 for n in lens if n > 0)
+            cache.advance()
+        t_end.record()
+        torch.cuda.synchronize()
+        gc.enable()
+        r["total_ms"] = t_start.elapsed_time(t_end)
+        return r
 
-    total_ms = t_start.elapsed_time(t_end)
+    main = timed(range(args.warmup, total_steps), pre, scrub=True)
+    log(f"{w.name}: {args.steps} timed steps done, {main['total_ms']:.1f} ms")
+    del pre
     ms = lambda evs: sum(x.elapsed_time(y) for x, y in evs)
-    attn_ms, embed_ms, evict_ms, mask_ms = ms(ev_attn), ms(ev_embed), ms(ev_evict), ms(ev_mask)
-    n_attn = len(ev_attn)
+    attn_ms, embed_ms, evict_ms, mask_ms = ms(main["attn"]), ms(main["embed"]), ms(main["evict"]), ms(main["mask"])
+    total_ms = main["total_ms"]
+    n_attn = len(main["attn"])
+    bytes_attn, bytes_embed, bytes_evict = main["bytes_attn"], main["bytes_embed"], main["bytes_evict"]
     attn_gbs = bytes_attn / (attn_ms * 1e-3) / 1e9
     embed_gbs = bytes_embed / (embed_ms * 1e-3) / 1e9 if embed_ms > 0 else None
+    live_tokens = main["live"]
     value = live_tokens / (total_ms * 1e-3)
 
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic) and args.config == DEFAULT_WORKLOAD and args.split is None \
-            and (args.steps, args.warmup) == (60, 4):
-        with open(args.traffic) as f:
-            rec = json.load(f)
-        if rec.get("kernel_sources_sha256") == kernel_sources_sha256():
-            traffic = rec.get("bytes_per_launch")
+    rec = traffic_record(args, w)
+    traffic = round(rec["traffic_over_algorithmic"] * bytes_attn / n_attn) if rec else None
 
+    resident = ""
+    if w.name == GQA_WORKLOAD:
+        resident = (f" ({w.n_layers} of its {GQA_LAYERS} layers resident: the dense padded cache of all "
+                    f"{GQA_LAYERS} exceeds HBM; each step decodes the {w.n_layers}, each at the real per-layer shape)")
+    attn_kernel = "attn_mfma_kernel" if w.n_q_heads > w.n_kv_heads and w.dtype == "bf16" else "attn_kernel"
     result = {
         "metric": "decode-attention query-tokens/s + achieved HBM GB/s (attn, kv_embed) at 1 GPU",
         "value": round(value, 1),
@@ -545,7 +633,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic (seeded counter-based generator, values ~N(0,1))",
         "config": {
-            "workload": f"{w.name}: {w.dtype}, {w.n_layers} layers x {w.n_q_heads} q-heads / "
+            "workload": f"{w.name}{resident}: {w.dtype}, {w.n_layers} layers x {w.n_q_heads} q-heads / "
                         f"{w.n_kv_heads} kv-heads x head_dim {w.head_dim}, batch {w.batch}, "
                         f"initial padded length {w.L0}, ring capacity {cap}, "
                         f"{total_steps} decode steps with re-batching",
@@ -553,38 +641,123 @@ def main():
             "split_tokens": args.split,
         },
         "roofline": {
-            "bound": "hbm", "kernel": "decode_attn (attn_kernel + combine_kernel)",
+            "bound": "hbm", "kernel": f"decode_attn ({attn_kernel} + combine_kernel + the step's meta_kernel)",
             "achieved": round(attn_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(attn_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
             "bytes_per_launch": round(bytes_attn / n_attn), "avg_launch_us": round(attn_ms / n_attn * 1e3, 2),
         },
         "ops": {
             "decode_attn": {"ms_per_step": round(attn_ms / args.steps, 4), "GB/s": round(attn_gbs, 1),
+                            "frac_of_peak": round(attn_gbs / PEAK_HBM_GBS, 4),
                             "query_tokens_per_s": round(live_tokens / (attn_ms * 1e-3), 1)},
             "kv_embed": {"ms_per_step": round(embed_ms / args.steps, 4),
                          "GB/s": round(embed_gbs, 1) if embed_gbs else None,
+                         "frac_of_peak": round(embed_gbs / PEAK_HBM_GBS, 4) if embed_gbs else None,
                          "bytes_per_step": round(bytes_embed / args.steps),
                          "placeholder_bytes_per_step": round(bytes_evict / args.steps),
                          "GB/s_with_placeholders": round((bytes_embed + bytes_evict) / (embed_ms * 1e-3) / 1e9, 1)
-                         if embed_ms > 0 else None},
+                         if embed_ms > 0 else None,
+                         "note": "evictions scrub (BATON_SCRUB): the placeholder writes they owe run in "
+                                 "the same launch as the copy; GB/s counts the copied bytes only"},
             "kv_evict": {"ms_per_step": round(evict_ms / args.steps, 4)},
             "build_mask": {"ms_per_step": round(mask_ms / args.steps, 4)},
         },
-        "per_step_ms": quantiles([x.elapsed_time(y) for x, y in ev_step]),
-        "decode_attn_call_us": quantiles([x.elapsed_time(y) * 1e3 for x, y in ev_attn]),
-        "hbm_copy_reference": copy_ref,
-        "hbm_read_reference": read_ref,
+        "per_step_ms": quantiles([x.elapsed_time(y) for x, y in main["step"]]),
+        "decode_attn_call_us": quantiles([x.elapsed_time(y) * 1e3 for x, y in main["attn"]]),
     }
-    if read_ref:
+    if rec:
+        result["roofline"]["traffic_over_algorithmic"] = rec["traffic_over_algorithmic"]
+        result["roofline"]["traffic_source"] = "profiles/" + TRAFFIC[w.name]
+    if w.name == GQA_WORKLOAD:
+        # the same step with all 80 layers: attention and embedding scale with the layers
+        layer_ms = (attn_ms + embed_ms) / args.steps
+        ms80 = evict_ms / args.steps + mask_ms / args.steps + layer_ms * GQA_LAYERS / w.n_layers
+        result["ops"]["estimate_80_layers"] = {
+            "ms_per_step": round(ms80, 4), "query_tokens_per_s": round(live_tokens / args.steps / (ms80 * 1e-3), 1),
+            "how": f"measured evict and mask per step, plus decode_attn and kv_embed per step x "
+                   f"{GQA_LAYERS}/{w.n_layers} layers (a derived figure, not timed)"}
+
+    if no_scrub_steps > 0:
+        extra = range(total_steps, total_steps + no_scrub_steps)
+        pre2 = inputs_of(extra)
+        torch.cuda.synchronize()
+        r2 = timed(extra, pre2, scrub=False)
+        log(f"{w.name}: {no_scrub_steps} steps without scrubbing done")
+        del pre2
+        e_ms = ms(r2["embed"])
+        result["ops"]["kv_embed_no_scrub"] = {
+            "steps": no_scrub_steps, "ms_per_step": round(e_ms / no_scrub_steps, 4),
+            "GB/s": round(r2["bytes_embed"] / (e_ms * 1e-3) / 1e9, 1) if e_ms > 0 else None,
+            "frac_of_peak": round(r2["bytes_embed"] / (e_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if e_ms > 0 else None,
+            "bytes_per_step": round(r2["bytes_embed"] / no_scrub_steps),
+            "note": f"steps {extra.start}..{extra.stop - 1} after the timed ones, evictions without "
+                    "BATON_SCRUB (the mask alone excludes the finished tokens): the launch copies only"}
+
+    if probes and copy_ref:
+        result["hbm_copy_reference"] = copy_ref
+        result["hbm_read_reference"] = read_ref
         result["roofline"]["frac_of_read_reference"] = round(attn_gbs / read_ref["GB/s"], 4)
         # The same read at the attention's own bytes per call, each launch
         # timed alone as the calls are: what a single launch of that size
         # loses to filling and draining the GPU is in both.
+        del cache, inputs, outs, ws, mask_buf
+        gc.collect()
+        torch.cuda.empty_cache()
         read_same = read_probe(round(bytes_attn / n_attn), reps=32, per_launch=True, n_bufs=4)
         result["hbm_read_reference_same_size"] = read_same
         result["roofline"]["frac_of_read_reference_same_size"] = round(attn_gbs / read_same["GB/s"], 4)
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
+    return result
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); "
+              "the batch shards by slot or by kv-head with no exchange on this path.", file=sys.stderr)
+        sys.exit(2)
+
+    from workload import configs
+
+    total_steps = args.warmup + args.steps
+
+    def workload(name, extra_steps=0):
+        if name == GQA_WORKLOAD:
+            return configs.gqa70b_b128_l8192(total_steps + extra_steps, n_layers=args.layers or GQA_RESIDENT)
+        if args.layers:
+            raise SystemExit(f"--layers applies to {GQA_WORKLOAD} only")
+        return configs.CONFIGS[name](total_steps + extra_steps)
+
+    plain = not args.no_pd and not args.model
+    extra = args.no_scrub_steps if plain else 0
+    w = workload(args.config, extra)
+    # The CPU baseline first, while no GPU is initialised (its workers are forked).
+    if plain and not args.no_cpu_baseline:
+        log("CPU oracle baseline")
+    cpu = cpu_baseline(w, args.cpu_workers) if plain and not args.no_cpu_baseline else None
+    if cpu:
+        log(f"CPU oracle baseline: {cpu['value']} query-tokens/s on {cpu['cores']} cores")
+
+    import torch
+    torch.cuda.set_device(0)
+    if args.no_pd:
+        print(json.dumps(bench_no_pd(args, w)), flush=True)
+        return
+    if args.model:
+        print(json.dumps(bench_model(args, w)), flush=True)
+        return
+    result = bench_decode(args, w, probes=True, no_scrub_steps=extra)
+    if not args.no_secondary and args.config == DEFAULT_WORKLOAD and args.split is None:
+        gc.collect()
+        torch.cuda.empty_cache()
+        w2 = workload(SECONDARY_WORKLOAD)
+        r2 = bench_decode(args, w2, probes=False)
+        result["also"] = {SECONDARY_WORKLOAD: {
+            "workload": r2["config"]["workload"], "value": r2["value"], "unit": r2["unit"],
+            "ms_per_step": r2["ms_per_step"], "decode_attn": r2["ops"]["decode_attn"],
+            "kv_embed": r2["ops"]["kv_embed"], "roofline": r2["roofline"],
+            "per_step_ms": r2["per_step_ms"], "decode_attn_call_us": r2["decode_attn_call_us"]}}
+    if cpu is not None:
+        result["cpu_baseline"] = cpu
     print(json.dumps(result), flush=True)
 
 

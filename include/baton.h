@@ -39,12 +39,15 @@
  *     [n_layers][batch][n_kv_heads][capacity][head_dim]
  * contiguous elements.  The `capacity` columns of a row form a ring: logical
  * column j of the aligned cache (0 <= j < L) lives at physical column
- * (base + j) mod capacity, where base is reported by baton_cache_query.  Every
- * physical position that is not a live token holds the placeholder bits
+ * (base + j) mod capacity, where base is reported by baton_cache_query.  As
+ * long as every eviction since the handle was created asked for BATON_SCRUB,
+ * every physical position that is not a live token holds the placeholder bits
  * (fill_bits) -- free rows, the placeholder fronts of live rows and the
  * capacity - L unused columns alike -- except the tokens of slots evicted since
  * the last decode step began, whose placeholder write is deferred (see
- * baton_kv_evict).
+ * baton_kv_evict).  An eviction without BATON_SCRUB leaves its query's tokens
+ * in place as stale bytes; no kernel ever reads a position that is not a live
+ * token, so results do not depend on what such positions hold.
  */
 #ifndef BATON_H
 #define BATON_H
@@ -84,6 +87,7 @@ typedef enum baton_dtype { BATON_F32 = 0, BATON_BF16 = 1 } baton_dtype;
 
 /* baton_kv_evict flags */
 #define BATON_RELEASE 1u /* then release the leading columns that are placeholders in every live row */
+#define BATON_SCRUB 2u   /* overwrite the finished queries' tokens with the placeholder */
 
 typedef struct baton_cache_desc {
   int32_t dtype;      /* baton_dtype of K, V, sources, q, k_new, v_new and out */
@@ -126,18 +130,24 @@ baton_status baton_cache_destroy(baton_cache* cache);
 
 /*
  * Finished queries leave their slots (sec. 4.1, Attention_mask and KV_Cache
- * paragraphs: the finished query's cached keys/values are overwritten with the
- * placeholder and its mask row zeroed).  slots: host array of n distinct live
- * slot indices (n may be 0); the slots become free.  The placeholder write over
- * each finished query's tokens (every layer and head; the holes of its row
- * hold placeholders already and are skipped) is owed, not enqueued
- * here: the next baton_kv_embed into the slot performs it over the columns in
- * front of its new query (the new query overwrites the rest), and the first
- * baton_decode_attn of the next step, or baton_cache_flush, performs whatever
- * is still owed.  With BATON_RELEASE, the columns [0 : min over live rows of
- * (L - len)] are then released (sec. 4.1, "Resources releasing"): L becomes
- * the longest live span (0 when no slot is live).  Release moves no data.
- * Nothing is enqueued.
+ * paragraphs: the finished query's mask row is zeroed, which alone keeps its
+ * tokens out of every later attention; overwriting its cached keys/values
+ * with the placeholder is the further safeguard the paper recommends).
+ * slots: host array of n distinct live slot indices (n may be 0); the slots
+ * become free.
+ * With BATON_SCRUB, the placeholder write over each finished query's tokens
+ * (every layer and head; the holes of its row hold placeholders already and
+ * are skipped) is owed, not enqueued here: the next baton_kv_embed into the
+ * slot performs it over the columns in front of its new query (the new query
+ * overwrites the rest), and the first baton_decode_attn of the next step, or
+ * baton_cache_flush, performs whatever is still owed.  Without BATON_SCRUB no
+ * placeholder byte is written: the tokens stay as stale bytes that the mask
+ * excludes and no kernel reads.
+ * With BATON_RELEASE, the columns [0 : min over live rows of (L - len)] are
+ * then released (sec. 4.1, "Resources releasing"): L becomes the longest live
+ * span (0 when no slot is live).  Without it L is unchanged; release is
+ * optional and may come with any later eviction (including one of no slot).
+ * Release moves no data.  Nothing is enqueued.
  * Errors: EINVAL (n < 0, null slots with n > 0, index out of range, duplicate,
  * unknown flag), ESLOT (a slot is free), ESTATE (inside a decode step).
  */

@@ -23,6 +23,7 @@ BATON_MAX_PREFILL = 64
 BATON_MAX_HOLES = 64
 BATON_CREATE_ASSUME_FILLED = 1
 BATON_RELEASE = 1
+BATON_SCRUB = 2
 
 
 class baton_cache_desc(ctypes.Structure):
@@ -139,7 +140,7 @@ def baton_cache_destroy(cache):
     _check(lib().baton_cache_destroy(cache), "baton_cache_destroy")
 
 
-def baton_kv_evict(cache, slots, flags=BATON_RELEASE, stream=None):
+def baton_kv_evict(cache, slots, flags=BATON_RELEASE | BATON_SCRUB, stream=None):
     arr, n = _i32s(slots)
     _check(lib().baton_kv_evict(cache, arr, n, flags, _stream(stream)), "baton_kv_evict")
 

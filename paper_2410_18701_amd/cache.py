@@ -76,9 +76,12 @@ class BatonCache:
         B.baton_set_split_tokens(self.handle, tokens)
 
     # -- the step --
-    def evict(self, slots, release=True, stream=None):
-        B.baton_kv_evict(self.handle, slots, B.BATON_RELEASE if release else 0,
-                         stream if stream is not None else _cur_stream())
+    def evict(self, slots, release=True, scrub=True, stream=None):
+        """Finished queries leave; scrub: their tokens become placeholders (else
+        they stay as stale bytes the mask excludes); release: drop the leading
+        columns that are placeholders in every live row."""
+        flags = (B.BATON_RELEASE if release else 0) | (B.BATON_SCRUB if scrub else 0)
+        B.baton_kv_evict(self.handle, slots, flags, stream if stream is not None else _cur_stream())
 
     def embed(self, slots, lens, k_src, v_src, stream=None):
         B.baton_kv_embed(self.handle, slots, lens, k_src, v_src,

@@ -374,6 +374,123 @@ baton_status flush_pending(baton_cache* c, hipStream_t stream) {
   return BATON_OK;
 }
 
+
+// ------------------------------------------------------------ decode step --
+// Argument checks shared by the decode entry points.
+baton_status attn_check(const baton_cache* c, int32_t layer, const void* q, const void* k_new,
+                        const void* v_new, void* out, float scale) {
+  if (!c || layer < 0 || layer >= c->d.n_layers) return BATON_EINVAL;
+  if (!q || !k_new || !v_new || !out) return BATON_EINVAL;
+  if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out)) return BATON_EINVAL;
+  if (!std::isfinite(scale)) return BATON_EINVAL;
+  if (c->layer_done[layer]) return BATON_ESTATE;
+  if (c->L + c->step_T > c->d.capacity) return BATON_ECAPACITY;
+  return BATON_OK;
+}
+
+// The step's work list: meta_kernel's arguments and the counts it will produce.
+void plan_items(baton_cache* c, baton::MetaArgs& m, int64_t& items, int64_t& multi) {
+  std::memset(&m, 0, sizeof(m));
+  m.L = c->L;
+  m.batch = c->d.batch;
+  c->step_split = c->split > 0 ? c->split : auto_split(c);
+  m.split = c->step_split;
+  m.holes = hole_list(c);
+  items = multi = 0;   // as meta_kernel counts them
+  for (int32_t b = 0; b < c->d.batch; ++b) {
+    m.lens[b] = c->plen[b] > 0 ? -1 : c->lens[b];   // a row prefilled this step has no item
+    m.first[b] = (uint8_t)first_hole(c, b);
+    const int64_t cnt = baton::row_items(m, b);
+    items += cnt;
+    multi += cnt > 1;
+  }
+}
+
+// One layer of the step, after the checks: the owed placeholder writes (first
+// layer), the work list when `m` is given (written into the workspace at wsb
+// with layout w), the attention launches, and the prefill of new queries.
+baton_status attn_run(baton_cache* c, int32_t layer, const void* q, const void* k_new, const void* v_new,
+                      void* out, float scale, char* wsb, const WsLayout& w, const baton::MetaArgs* m,
+                      int64_t items, int64_t multi, hipStream_t stream) {
+  if (c->n_done == 0) {
+    const baton_status st = flush_pending(c, stream);
+    if (st != BATON_OK) return st;
+  }
+  if (m) {
+    hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, *m,
+                       reinterpret_cast<baton::Item*>(wsb + w.items_off),
+                       reinterpret_cast<int4*>(wsb + w.multi_off));
+    const baton_status st = hip_status(hipGetLastError());
+    if (st != BATON_OK) return st;
+    c->n_items = (int32_t)items;
+    c->n_multi = (int32_t)multi;
+    c->meta_ws = wsb;
+    c->meta_valid = true;
+  }
+  baton::AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  // the layer's own rows
+  const int64_t lw = (int64_t)layer * c->layer_vec * 4;   // 32-bit words
+  a.k = static_cast<const uint32_t*>(c->d.k) + lw;
+  a.k_w = static_cast<uint32_t*>(c->d.k) + lw;
+  a.v = static_cast<uint32_t*>(c->d.v) + lw;
+  a.q = static_cast<const uint32_t*>(q);
+  a.knew = static_cast<const uint32_t*>(k_new);
+  a.vnew = static_cast<const uint32_t*>(v_new);
+  a.out = static_cast<uint32_t*>(out);
+  a.items = reinterpret_cast<const baton::Item*>(wsb + w.items_off);
+  a.multi = reinterpret_cast<const int4*>(wsb + w.multi_off);
+  a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
+  a.cap = c->d.capacity;
+  a.base = c->base;
+  a.L = c->L;
+  a.batch = c->d.batch;
+  a.n_kv_heads = c->d.n_kv_heads;
+  a.split = c->step_split;
+  a.n_items = c->n_items;
+  a.tw = c->step_T;
+  const float sc = scale == 0.f ? 1.0f / std::sqrt((float)c->d.head_dim) : scale;
+  a.qscale = sc * 1.4426950408889634f;
+  if (c->n_items > 0 && !launch_attn(c, a, stream)) return BATON_EDTYPE;
+  baton_status st = hip_status(hipGetLastError());
+  if (st != BATON_OK) return st;
+  if (c->n_prefill > 0) {
+    baton::PrefillArgs p;
+    std::memset(&p, 0, sizeof(p));
+    p.k = static_cast<uint32_t*>(c->d.k) + lw;
+    p.v = static_cast<uint32_t*>(c->d.v) + lw;
+    p.q = a.q;
+    p.knew = a.knew;
+    p.vnew = a.vnew;
+    p.out = a.out;
+    p.cap = c->d.capacity;
+    p.base = c->base;
+    p.L = c->L;
+    p.T = c->step_T;
+    p.batch = c->d.batch;
+    p.n_kv_heads = c->d.n_kv_heads;
+    p.qscale = a.qscale;
+    // the prefilled queries, longest prompt first (their longest tiles are dealt first)
+    for (int32_t b = 0; b < c->d.batch; ++b)
+      if (c->plen[b] > 0) {
+        int32_t i = p.n_ins++;
+        for (; i > 0 && p.plen[i - 1] < c->plen[b]; --i) {
+          p.slot[i] = p.slot[i - 1];
+          p.plen[i] = p.plen[i - 1];
+        }
+        p.slot[i] = b;
+        p.plen[i] = c->plen[b];
+      }
+    if (c->d.head_dim == 64) launch_prefill_d<64>(c, p, stream);
+    else launch_prefill_d<128>(c, p, stream);
+    st = hip_status(hipGetLastError());
+    if (st != BATON_OK) return st;
+  }
+  c->layer_done[layer] = 1;
+  ++c->n_done;
+  return BATON_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -466,7 +583,7 @@ baton_status baton_cache_destroy(baton_cache* c) {
 
 baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uint32_t flags,
                             hipStream_t stream) {
-  if (!c || n < 0 || (n > 0 && !slots) || (flags & ~BATON_RELEASE)) return BATON_EINVAL;
+  if (!c || n < 0 || (n > 0 && !slots) || (flags & ~(BATON_RELEASE | BATON_SCRUB))) return BATON_EINVAL;
   if (c->n_done || c->n_prefill) return BATON_ESTATE;
   std::vector<uint8_t> seen(c->d.batch, 0);
   for (int32_t i = 0; i < n; ++i) {
@@ -476,12 +593,13 @@ baton_status baton_kv_evict(baton_cache* c, const int32_t* slots, int32_t n, uin
   }
   for (int32_t i = 0; i < n; ++i)
     if (c->lens[slots[i]] == 0) return BATON_ESLOT;
-  // The finished queries' tokens are owed placeholders (the rest of their rows
-  // already holds them); the write is left to the next embed into the slot,
-  // which skips the columns its own query overwrites, or to the next step.
+  // With SCRUB the finished queries' tokens are owed placeholders (the rest of
+  // their rows already holds them); the write is left to the next embed into
+  // the slot, which skips the columns its own query overwrites, or to the next
+  // step.  Without it they stay as they are: the mask alone excludes them.
   (void)stream;
   for (int32_t i = 0; i < n; ++i) {
-    owe_row(c, slots[i]);
+    if (flags & BATON_SCRUB) owe_row(c, slots[i]);
     c->lens[slots[i]] = 0;
   }
   if (flags & BATON_RELEASE) {
@@ -670,109 +788,20 @@ size_t baton_decode_attn_workspace_bytes(const baton_cache* c) {
 baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, const void* k_new,
                                const void* v_new, void* out, float scale, void* ws,
                                size_t ws_bytes, hipStream_t stream) {
-  if (!c || layer < 0 || layer >= c->d.n_layers) return BATON_EINVAL;
-  if (!q || !k_new || !v_new || !out || !ws) return BATON_EINVAL;
-  if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out) || !aligned16(ws))
-    return BATON_EINVAL;
-  if (!std::isfinite(scale)) return BATON_EINVAL;
+  baton_status st = attn_check(c, layer, q, k_new, v_new, out, scale);
+  if (st != BATON_OK) return st;
+  if (!ws || !aligned16(ws)) return BATON_EINVAL;
   const WsLayout w = ws_layout(c);
   if (ws_bytes < w.total) return BATON_EINVAL;
-  if (c->layer_done[layer]) return BATON_ESTATE;
-  if (c->L + c->step_T > c->d.capacity) return BATON_ECAPACITY;
-  if (c->n_done == 0) {
-    const baton_status st = flush_pending(c, stream);
-    if (st != BATON_OK) return st;
-  }
   char* wsb = static_cast<char*>(ws);
   if (!c->meta_valid || c->meta_ws != ws) {
     baton::MetaArgs m;
-    std::memset(&m, 0, sizeof(m));
-    m.L = c->L;
-    m.batch = c->d.batch;
-    c->step_split = c->split > 0 ? c->split : auto_split(c);
-    m.split = c->step_split;
-    m.holes = hole_list(c);
-    int64_t items = 0, multi = 0;   // as meta_kernel counts them
-    for (int32_t b = 0; b < c->d.batch; ++b) {
-      m.lens[b] = c->plen[b] > 0 ? -1 : c->lens[b];   // a row prefilled this step has no item
-      m.first[b] = (uint8_t)first_hole(c, b);
-      const int64_t cnt = baton::row_items(m, b);
-      items += cnt;
-      multi += cnt > 1;
-    }
+    int64_t items, multi;
+    plan_items(c, m, items, multi);
     if (items > w.max_items) return BATON_EINVAL;   // cannot happen: the layout bounds every row
-    hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, m,
-                       reinterpret_cast<baton::Item*>(wsb + w.items_off),
-                       reinterpret_cast<int4*>(wsb + w.multi_off));
-    const baton_status st = hip_status(hipGetLastError());
-    if (st != BATON_OK) return st;
-    c->n_items = (int32_t)items;
-    c->n_multi = (int32_t)multi;
-    c->meta_ws = ws;
-    c->meta_valid = true;
+    return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, stream);
   }
-  baton::AttnArgs a;
-  std::memset(&a, 0, sizeof(a));
-  // the layer's own rows
-  const int64_t lw = (int64_t)layer * c->layer_vec * 4;   // 32-bit words
-  a.k = static_cast<const uint32_t*>(c->d.k) + lw;
-  a.k_w = static_cast<uint32_t*>(c->d.k) + lw;
-  a.v = static_cast<uint32_t*>(c->d.v) + lw;
-  a.q = static_cast<const uint32_t*>(q);
-  a.knew = static_cast<const uint32_t*>(k_new);
-  a.vnew = static_cast<const uint32_t*>(v_new);
-  a.out = static_cast<uint32_t*>(out);
-  a.items = reinterpret_cast<const baton::Item*>(wsb + w.items_off);
-  a.multi = reinterpret_cast<const int4*>(wsb + w.multi_off);
-  a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
-  a.cap = c->d.capacity;
-  a.base = c->base;
-  a.L = c->L;
-  a.batch = c->d.batch;
-  a.n_kv_heads = c->d.n_kv_heads;
-  a.split = c->step_split;
-  a.n_items = c->n_items;
-  a.tw = c->step_T;
-  const float sc = scale == 0.f ? 1.0f / std::sqrt((float)c->d.head_dim) : scale;
-  a.qscale = sc * 1.4426950408889634f;
-  if (c->n_items > 0 && !launch_attn(c, a, stream)) return BATON_EDTYPE;
-  baton_status st = hip_status(hipGetLastError());
-  if (st != BATON_OK) return st;
-  if (c->n_prefill > 0) {
-    baton::PrefillArgs p;
-    std::memset(&p, 0, sizeof(p));
-    p.k = static_cast<uint32_t*>(c->d.k) + lw;
-    p.v = static_cast<uint32_t*>(c->d.v) + lw;
-    p.q = a.q;
-    p.knew = a.knew;
-    p.vnew = a.vnew;
-    p.out = a.out;
-    p.cap = c->d.capacity;
-    p.base = c->base;
-    p.L = c->L;
-    p.T = c->step_T;
-    p.batch = c->d.batch;
-    p.n_kv_heads = c->d.n_kv_heads;
-    p.qscale = a.qscale;
-    // the prefilled queries, longest prompt first (their longest tiles are dealt first)
-    for (int32_t b = 0; b < c->d.batch; ++b)
-      if (c->plen[b] > 0) {
-        int32_t i = p.n_ins++;
-        for (; i > 0 && p.plen[i - 1] < c->plen[b]; --i) {
-          p.slot[i] = p.slot[i - 1];
-          p.plen[i] = p.plen[i - 1];
-        }
-        p.slot[i] = b;
-        p.plen[i] = c->plen[b];
-      }
-    if (c->d.head_dim == 64) launch_prefill_d<64>(c, p, stream);
-    else launch_prefill_d<128>(c, p, stream);
-    st = hip_status(hipGetLastError());
-    if (st != BATON_OK) return st;
-  }
-  c->layer_done[layer] = 1;
-  ++c->n_done;
-  return BATON_OK;
+  return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, nullptr, 0, 0, stream);
 }
 
 baton_status baton_cache_flush(baton_cache* c, hipStream_t stream) {

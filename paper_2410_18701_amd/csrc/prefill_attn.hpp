@@ -230,13 +230,19 @@ prefill_fa_kernel(const PrefillArgs a) {
   const u32x4* vin = reinterpret_cast<const u32x4*>(a.vnew);
   const u32x4 zero = {0, 0, 0, 0};
 
+  // A negative scale's sign is folded into q (negating a bf16 value is
+  // exact), so that the softmax below always works with a positive factor:
+  // the largest scaled score is then the scale times the largest score.
+  const float qscale = fabsf(a.qscale);
+  const uint32_t qsw = a.qscale < 0.f ? 0x80008000u : 0u;
+  const u32x4 qsign = {qsw, qsw, qsw, qsw};
   bf16x8 qb[QG][KK];
 #pragma unroll
   for (int gq = 0; gq < QG; ++gq) {
     const int32_t qi = i0 + 16 * gq + c16;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk)
-      qb[gq][kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] : zero);
+      qb[gq][kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] ^ qsign : zero);
   }
 
   float m[QG], lsum[QG];
@@ -322,7 +328,7 @@ prefill_fa_kernel(const PrefillArgs a) {
         float mx = s[0];
 #pragma unroll
         for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
-        mx = max_over_groups(mx) * a.qscale;           // qscale > 0: the max of the scaled scores
+        mx = max_over_groups(mx) * qscale;             // qscale >= 0: the max of the scaled scores
         const float mn = fmaxf(m[gq], mx);
         const float ref = mn == -INFINITY ? 0.f : mn;
         // exponents are <= 0 here: the hardware exp2 (results below the
@@ -333,7 +339,7 @@ prefill_fa_kernel(const PrefillArgs a) {
         float psum = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float pf = __builtin_amdgcn_exp2f(fmaf(s[e], a.qscale, -ref));
+          const float pf = __builtin_amdgcn_exp2f(fmaf(s[e], qscale, -ref));
           pa[gq][e] = (__bf16)pf;
           psum += pf;
         }

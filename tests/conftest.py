@@ -8,3 +8,12 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (runs through the C-ABI on the GPU)")
+
+
+def pytest_sessionfinish(session, exitstatus):
+    """Keep the parity runs' largest attention errors (and their fraction of
+    the tolerance) in gpurun_out/parity_margins.json when any ran."""
+    parity = sys.modules.get("tests.parity")
+    if parity is not None:
+        parity.write_margins(os.environ.get("BATON_MARGINS_OUT",
+                                            os.path.join(ROOT, "gpurun_out", "parity_margins.json")))

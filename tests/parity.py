@@ -9,7 +9,9 @@ the device generator), comparing after every operation:
   * the mask, bit for bit;
   * every layer's attention output, within the element type's tolerance.
 """
+import json
 import math
+import os
 
 import numpy as np
 import torch
@@ -18,6 +20,32 @@ import oracle.baton_oracle as O
 from workload import driver, gen
 
 TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+# Largest attention error of each parity run, by test: written at the end of
+# the session (tests/conftest.py) so that the margins to the tolerances are kept.
+MARGINS = []
+
+
+def note_margin(worst, dtype, what=""):
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" (")[0]
+    MARGINS.append({"test": test, "what": what, "dtype": dtype, "max_abs_err": float(worst),
+                    "tol": TOL[dtype], "frac_of_tol": round(float(worst) / TOL[dtype], 4)})
+
+
+def write_margins(path):
+    """Adds this session's margins to those already in the file."""
+    if not MARGINS:
+        return
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    old = []
+    if os.path.exists(path):
+        try:
+            with open(path) as f:
+                old = json.load(f)
+        except (OSError, ValueError):
+            old = []
+    with open(path, "w") as f:
+        json.dump(old + MARGINS, f, indent=1)
 
 
 def host_bits(t):
@@ -36,9 +64,12 @@ def ring_to_logical(ring, base, L):
     return ring[:, :, :, idx], ring[:, :, :, rest]
 
 
-def check_ring(cache, pb, where, live_only=False):
+def check_ring(cache, pb, where, live_only=False, tokens_only=False):
     """live_only: compare the live rows' windows only (between an eviction and
-    the next step, evicted rows may still hold their old tokens)."""
+    the next step, evicted rows may still hold their old tokens).  tokens_only:
+    compare the live rows' tokens only, the columns the oracle's mask holds 1
+    on (after an eviction without scrubbing, every other position may hold
+    stale bytes)."""
     L, base, lens = cache.query()
     assert L == pb.L, (where, L, pb.L)
     assert lens == pb.lens, (where, lens, pb.lens)
@@ -46,6 +77,12 @@ def check_ring(cache, pb, where, live_only=False):
     for which, want in (("k", pb.K), ("v", pb.V)):
         ring = host_bits(cache.k if which == "k" else cache.v)
         win, rest = ring_to_logical(ring, base, L)
+        if tokens_only:
+            for b in live:
+                cols = np.flatnonzero(pb.M[b, :L])
+                if not np.array_equal(win[:, b][:, :, cols], want[:, b][:, :, cols]):
+                    raise AssertionError(f"{where}: {which} tokens of slot {b} differ")
+            continue
         if live_only:
             win, want = win[:, live], want[:, live]
         if not np.array_equal(win, want):
@@ -73,8 +110,15 @@ def padded_kv(n_layers, batch, n_kv_heads, capacity, head_dim, dtype, pad=4096 +
     return views[0], views[1], lambda: all(bool((b[:, per:] == 7.0).all()) for b in bufs)
 
 
-def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale=0.0, layout="by_layer"):
-    """Drive the whole schedule; returns the largest attention error seen."""
+def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale=0.0, layout="by_layer",
+        release_every=1, scrub=True):
+    """Drive the whole schedule; returns the largest attention error seen.
+
+    release_every: step s's evictions release (BATON_RELEASE) only when
+    s % release_every == release_every - 1, and a release of no slot closes
+    the run when release_every > 1.  scrub: evictions overwrite the finished
+    queries' tokens with placeholders (BATON_SCRUB); without it, once a query
+    has been evicted, only the live rows' tokens are compared."""
     cap = w.capacity() if capacity is None else capacity
     if layout == "padded":
         # two allocations whose layers are 4096 + 16 elements apart beyond their rows
@@ -106,19 +150,22 @@ def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale
     embed(list(range(w.batch)), w.init_lens, list(range(w.batch)))
     check_ring(cache, pb, "initial batch")
     sc = None if scale == 0.0 else scale
+    stale = False   # some eviction left its tokens in place
     for s, ev in enumerate(w.steps):
-        cache.evict(ev.evict, release=True)
-        pb.evict(ev.evict, release=True)
+        release = s % release_every == release_every - 1
+        cache.evict(ev.evict, release=release, scrub=scrub)
+        pb.evict(ev.evict, release=release)
+        stale |= bool(ev.evict) and not scrub
         if check_every_op:
-            check_ring(cache, pb, f"step {s} evict", live_only=True)
+            check_ring(cache, pb, f"step {s} evict", live_only=True, tokens_only=stale)
         if ev.insert:
             embed(ev.insert, ev.insert_lens, ev.insert_qids)
             if check_every_op:
-                check_ring(cache, pb, f"step {s} embed", live_only=True)
+                check_ring(cache, pb, f"step {s} embed", live_only=True, tokens_only=stale)
         if check_every_op and s % 2 == 1:
             cache.flush()
             torch.cuda.synchronize()
-            check_ring(cache, pb, f"step {s} flush")
+            check_ring(cache, pb, f"step {s} flush", tokens_only=stale)
         m = cache.build_mask()
         assert np.array_equal(m.cpu().numpy(), pb.mask()), f"step {s} mask"
         for layer in range(w.n_layers):
@@ -138,11 +185,17 @@ def run(w, capacity=None, split=None, fill_bits=None, check_every_op=True, scale
         cache.advance()
         pb.advance()
         if check_every_op or s == len(w.steps) - 1:
-            check_ring(cache, pb, f"step {s} advance")
+            check_ring(cache, pb, f"step {s} advance", tokens_only=stale)
+    if release_every > 1:
+        cache.evict([], release=True, scrub=scrub)
+        pb.evict([], release=True)
+        torch.cuda.synchronize()
+        check_ring(cache, pb, "closing release", tokens_only=stale)
     if layout == "padded":
         torch.cuda.synchronize()
         assert padding_intact(), "a write landed in the padding between layers"
     cache.close()
+    note_margin(worst, w.dtype, w.name)
     return worst
 
 
@@ -280,6 +333,7 @@ def run_sampled(w, sample_steps, sample_layers, n_slots=4, seed=0, split=None, c
     torch.cuda.synchronize()
     check_placeholders_outside_live(cache, cache.fill_bits)
     cache.close()
+    note_margin(worst, w.dtype, f"{w.name} sampled")
     return worst, checked
 
 
@@ -363,17 +417,19 @@ def run_sampled_no_pd(w, sample_steps, sample_layers=(0,), n_slots=4, n_pos=6, h
     cache.flush()
     check_placeholders_outside_live(cache, cache.fill_bits, mask=cache.build_mask())
     cache.close()
+    note_margin(worst, w.dtype, f"{w.name} sampled, no P&D")
     return worst, checked
 
 
 # ---------------------------------------------------------- scripted mode --
-def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", log=None):
+def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", log=None, scale=0.0):
     """A scripted sequence on a small batch, GPU and materialized oracle in
     lockstep, everything compared after every operation.
 
     shape: (dtype, n_layers, batch, n_q_heads, n_kv_heads, head_dim).  ops:
       ("embed", slots, lens, qids)   prefilled queries from the generator
-      ("evict", slots)               with release
+      ("evict", slots)               with release and scrub
+      ("evict", slots, release, scrub)  with the given flags
       ("extract", slots, tag)        store the slots' K/V aside (GPU and oracle)
       ("embed_saved", slots, tag)    re-insert stored queries into these slots
       ("shape", slots, lens, qids)   prefill new queries inside the batch in the next step
@@ -384,7 +440,9 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
                                      oracle repeats its parks and returns; `log` gets
                                      ("scale", parked slots, returned slots))
     After a step or a flush the whole ring is compared; after the other
-    operations the live rows (evicted rows may still hold old tokens).
+    operations the live rows (evicted rows may still hold old tokens); once an
+    eviction did not scrub, the live rows' tokens only.  scale: the attention
+    scale passed to every decode_attn (0: 1/sqrt(head_dim)).
     """
     dtype, NL, B, Hq, Hkv, D = shape
     from workload.configs import Workload
@@ -398,6 +456,8 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
     scaler, parked_cpu = None, []
     shaped = []
     worst = 0.0
+    stale = False
+    sc = None if scale == 0.0 else scale
     for op in ops:
         kind = op[0]
         if kind == "embed":
@@ -408,8 +468,10 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
                    gen.prefill_host(w.seed, "v", q, NL, Hkv, n, D, dtype)) for q, n in zip(qids, lens)]
             pb.embed(slots, lens, [h[0] for h in hs], [h[1] for h in hs])
         elif kind == "evict":
-            cache.evict(op[1], release=True)
-            pb.evict(op[1], release=True)
+            release, scrub = (op[2], op[3]) if len(op) > 2 else (True, True)
+            cache.evict(op[1], release=release, scrub=scrub)
+            pb.evict(op[1], release=release)
+            stale |= bool(op[1]) and not scrub
         elif kind == "extract":
             _, slots, tag = op
             ks, vs = cache.extract(slots)
@@ -441,21 +503,21 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
                     T = pb.step_width()
                     q, kn, vn = dev.prefill_step(s, layer, T, shaped)
                     out = torch.full_like(q, float("nan"))   # positions without a token stay NaN
-                    cache.decode_attn(layer, q, kn, vn, out=out)
+                    cache.decode_attn(layer, q, kn, vn, out=out, scale=scale)
                     hq = [gen.prefill_step_host(w.seed, which, s, layer, NL, B, T, h, D, dtype, shaped)
                           for which, h in (("q", Hq), ("k", Hkv), ("v", Hkv))]
                     assert np.array_equal(host_bits(kn), hq[1]), "device and host generators disagree"
-                    want = pb.decode_layer(layer, *hq)
+                    want = pb.decode_layer(layer, *hq, scale=sc)
                     got = O.widen(host_bits(out), dtype)
                     hole = np.isnan(want)
                     assert np.all(np.isnan(got[hole])), f"{op} layer {layer}: a position without a token was written"
                     err = float(np.max(np.abs(got[~hole] - want[~hole]))) if (~hole).any() else 0.0
                 else:
                     q, kn, vn = dev.decode(s, layer)
-                    out = cache.decode_attn(layer, q, kn, vn)
+                    out = cache.decode_attn(layer, q, kn, vn, scale=scale)
                     hq = [gen.decode_host(w.seed, sid, s, layer, NL, B, h, D, dtype)
                           for sid, h in ((gen.S_Q, Hq), (gen.S_KNEW, Hkv), (gen.S_VNEW, Hkv))]
-                    want = pb.decode_layer(layer, *hq)
+                    want = pb.decode_layer(layer, *hq, scale=sc)
                     err = max_err(out, want, dtype)
                 worst = max(worst, err)
                 assert err <= TOL[dtype], f"{op} layer {layer}: {err}"
@@ -483,8 +545,10 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
             raise ValueError(kind)
         torch.cuda.synchronize()
         check_ring(cache, pb, str(op),
-                   live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape", "move", "scale"))
+                   live_only=kind in ("evict", "embed", "embed_saved", "extract", "shape", "move", "scale"),
+                   tokens_only=stale)
         want_tok = [pb.hist_k[b].shape[2] if pb.lens[b] > 0 else 0 for b in range(B)]
         assert cache.tokens() == want_tok, (op, cache.tokens(), want_tok)
     cache.close()
+    note_margin(worst, dtype, f"script {dtype} {NL}x{B}x{Hq}/{Hkv}x{D}")
     return worst

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     for s in range(7):
-        assert B.baton_status_string(s)
+        assert B.baton_status_string(s) != "unknown status"
     assert B.baton_status_string(99) == "unknown status"
 
 
@@ -87,7 +87,10 @@ def test_host_checks_leave_state_unchanged():
         assert status(B.baton_kv_evict, h, [1]) == B.BATON_ESLOT          # free slot
         assert status(B.baton_kv_evict, h, [4]) == B.BATON_EINVAL         # out of range
         assert status(B.baton_kv_evict, h, [0, 0]) == B.BATON_EINVAL      # duplicate
-        assert status(B.baton_kv_evict, h, [], 2) == B.BATON_EINVAL       # unknown flag
+        assert status(B.baton_kv_evict, h, [], 4) == B.BATON_EINVAL       # unknown flag
+        assert status(B.baton_kv_evict, h, [1], B.BATON_SCRUB) == B.BATON_ESLOT
+        B.baton_kv_evict(h, [], B.BATON_RELEASE | B.BATON_SCRUB)          # both flags, no slot
+        B.baton_kv_evict(h, [], 0)                                         # neither
         assert status(B.baton_kv_embed, h, [0], [0], [FAKE_K], [FAKE_V]) == B.BATON_EINVAL   # empty query
         assert status(B.baton_kv_embed, h, [0], [300], [FAKE_K], [FAKE_V]) == B.BATON_ECAPACITY  # 300+1 > 300
         assert status(B.baton_kv_embed, h, [0, 0], [3, 3], [FAKE_K] * 2, [FAKE_V] * 2) == B.BATON_EINVAL

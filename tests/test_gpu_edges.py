@@ -71,6 +71,46 @@ def test_nan_placeholders_change_nothing(dtype, nan):
         assert np.all(np.isfinite(O.widen(a, dtype)))
 
 
+@pytest.mark.parametrize("dtype,nan", [("bf16", 0x7FC1), ("f32", 0x7FC00001)])
+def test_stale_nan_tokens_change_nothing(dtype, nan):
+    """Tokens left in place by evictions without BATON_SCRUB are never read
+    (sec. 4.1: the mask alone excludes them).  At every step the finished slots
+    first take queries as long as the batch whose keys and values are all NaN,
+    which leave again unscrubbed, so that the next queries sit over stale NaN
+    tokens: every output is bit for bit that of a twin batch that never held
+    them, and finite."""
+    w = configs.small(dtype, 2, 5, 4, 2, 64, L0=200, n_steps=4, n_evict=2, seed=13)
+    tdt, idt = (torch.bfloat16, torch.int16) if dtype == "bf16" else (torch.float32, torch.int32)
+    word = int(np.array(nan, np.uint16 if dtype == "bf16" else np.uint32).view(
+        np.int16 if dtype == "bf16" else np.int32))
+    outs = {}
+    for poison in (False, True):
+        cache, dev = driver.open_cache(w)
+        cache.set_split_tokens(64)
+        got = []
+        for s, ev in enumerate(w.steps):
+            if poison and ev.evict:
+                L = cache.query()[0]
+                cache.evict(ev.evict, release=False)
+                bad = [torch.full((w.n_layers, w.n_kv_heads, L, w.head_dim), word, dtype=idt,
+                                  device="cuda").view(tdt) for _ in ev.evict]
+                cache.embed(ev.evict, [L] * len(ev.evict), bad, bad)
+                cache.evict(ev.evict, release=True, scrub=False)
+            else:
+                cache.evict(ev.evict, release=True)
+            srcs = [dev.prefill(q, n) for q, n in zip(ev.insert_qids, ev.insert_lens)]
+            cache.embed(ev.insert, ev.insert_lens, [x[0] for x in srcs], [x[1] for x in srcs])
+            for layer in range(w.n_layers):
+                q, kn, vn = dev.decode(s, layer)
+                got.append(parity.host_bits(cache.decode_attn(layer, q, kn, vn)))
+            cache.advance()
+        outs[poison] = got
+        cache.close()
+    for a, b in zip(outs[False], outs[True]):
+        assert np.array_equal(a, b)
+        assert np.all(np.isfinite(O.widen(a, dtype)))
+
+
 def test_capacity_limits_leave_state():
     """ECAPACITY from embed and from decode, with the state (metadata and bytes) unchanged."""
     w = scripted("cap", "bf16", 1, 2, 2, 2, 64, [10, 6], [])

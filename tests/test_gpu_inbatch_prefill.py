@@ -105,3 +105,29 @@ def test_extract_with_holes():
     for shape in (("bf16", 2, 4, 8, 2, 128), ("f32", 1, 4, 4, 4, 64)):
         err = parity.run_script(shape, ops, capacity=256, split=64)
         print(f"[inbatch extract] {shape}: max abs error {err:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("scale", [1.0, -0.5])
+def test_peaked_and_negative_scale(scale):
+    """Prompts and decode rows with a peaked softmax (scale 1 at head_dim 128)
+    and with a negative scale, whose sign the prefill kernel folds into q."""
+    ops = [("embed", [0, 1, 2], [100, 40, 7], [0, 1, 2]), ("step", 0),
+           ("evict", [1]), ("shape", [1], [200], [3]), ("step", 1), ("step", 2),
+           ("evict", [0, 2]), ("shape", [2, 0], [129, 33], [4, 5]), ("step", 3), ("step", 4)]
+    for shape in (("bf16", 1, 3, 8, 8, 128), ("bf16", 1, 3, 16, 2, 64), ("f32", 1, 3, 4, 2, 128)):
+        err = parity.run_script(shape, ops, capacity=600, split=64, scale=scale)
+        print(f"[inbatch scale {scale}] {shape}: max abs error {err:.3g}", flush=True)
+
+
+def test_holes_with_unscrubbed_evictions():
+    """In-batch prefill and holes after evictions that leave stale tokens
+    (no BATON_SCRUB) and do not release: live tokens, mask and outputs as the
+    oracle says."""
+    ops = [("embed", [0, 1, 2], [30, 12, 50], [0, 1, 2]), ("step", 0),
+           ("evict", [1], False, False), ("shape", [1], [20], [3]), ("step", 1),
+           ("evict", [2], False, False), ("embed", [2], [9], [4]), ("step", 2),
+           ("evict", [0], True, False), ("shape", [0], [6], [5]), ("step", 3), ("step", 4),
+           ("evict", [], True, False), ("step", 5)]
+    for shape in (("bf16", 2, 3, 8, 2, 128), ("f32", 1, 3, 4, 4, 64)):
+        err = parity.run_script(shape, ops, capacity=256, split=64)
+        print(f"[inbatch stale] {shape}: max abs error {err:.3g}", flush=True)

@@ -68,3 +68,52 @@ def test_ring_wraparound_tight_capacity():
 def test_explicit_scale():
     w = configs.small("f32", 1, 3, 2, 2, 64, L0=70, n_steps=2, n_evict=1, seed=42)
     parity.run(w, scale=0.3)
+
+
+@pytest.mark.parametrize("name,release_every,scrub", [
+    ("mha-bf16-d128", 3, True),                # release only every third step, then a closing release
+    ("gqa8-bf16-d128-split64", 2, False),      # no placeholder bytes written at all
+    ("tiny-f32", 1, False),
+    ("gqa2-f32-d128-split64", 100, True),      # no release until the closing one
+    ("gqa2-bf16-d64-split64", 100, False),
+])
+def test_schedule_parity_release_and_scrub(name, release_every, scrub):
+    """Evictions without BATON_RELEASE (L keeps its leading placeholder columns
+    until a later release, sec. 4.1 "Resources releasing") and without
+    BATON_SCRUB (the finished queries' tokens stay as stale bytes that the mask
+    alone excludes, sec. 4.1 KV_Cache paragraph): the live tokens, the mask and
+    every output as the oracle says."""
+    w, kw = SMALL[name]
+    print(f"[parity] {name} release every {release_every}, scrub {scrub}", flush=True)
+    err = parity.run(w, release_every=release_every, scrub=scrub, **kw)
+    print(f"[parity] {name} release every {release_every}, scrub {scrub}: max abs error {err:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("scrub", [True, False])
+def test_ring_wraparound_rare_release(scrub):
+    """A tight ring with release every fourth step only: L grows past its
+    leading placeholders, growth on insertion follows each release, and the
+    window wraps around the end of the ring."""
+    w = configs.small("bf16", 1, 6, 4, 4, 64, L0=160, n_steps=12, n_evict=3, seed=43)
+    cap = w.L0 + w.n_steps + 1
+    print(f"[parity] wraparound, release every 4, scrub {scrub}, cap={cap}", flush=True)
+    parity.run(w, capacity=cap, split=64, release_every=4, scrub=scrub)
+
+
+@pytest.mark.parametrize("name,scale", [
+    ("mha-bf16-d128", 1.0),                    # the VALU kernel, bf16 (scores of spread ~11)
+    ("gqa8-bf16-d128-split64", 1.0),           # the matrix-core kernel, 8 q-heads per kv-head
+    ("gqa4-bf16-d128", 1.5),
+    ("gqa2-f32-d128-split64", 1.0),            # the VALU kernel, fp32
+    ("mha-bf16-d128", -1.0),                   # a negative scale
+    ("gqa8-bf16-d128-split64", -0.7),
+])
+def test_peaked_softmax(name, scale):
+    """A scale of 1 at head_dim 128 (about 11 times 1/sqrt(128)) makes each
+    softmax nearly one-hot: the largest weights dwarf the rest, many fall below
+    fp32's normal range and the bf16-rounded weights of the matrix-core kernel
+    matter most."""
+    w, kw = SMALL[name]
+    print(f"[parity] {name} scale {scale}", flush=True)
+    err = parity.run(w, scale=scale, **kw)
+    print(f"[parity] {name} scale {scale}: max abs error {err:.3g}", flush=True)
