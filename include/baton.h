@@ -69,7 +69,8 @@ typedef enum baton_status {
                           or a prefill step would leave more than BATON_MAX_HOLES holes */
   BATON_EDTYPE = 4,    /* unsupported element type, head_dim or head grouping */
   BATON_ESTATE = 5,    /* call out of order with the decode step in progress */
-  BATON_EHIP = 6       /* the HIP runtime refused a launch */
+  BATON_EHIP = 6,      /* the HIP runtime refused a launch */
+  BATON_ESCRATCH = 7   /* baton_decode_attn_noalloc: the step needs more than BATON_SCRATCH_BYTES */
 } baton_status;
 
 typedef enum baton_dtype { BATON_F32 = 0, BATON_BF16 = 1 } baton_dtype;
@@ -286,6 +287,34 @@ size_t baton_decode_attn_workspace_bytes(const baton_cache* cache);
 baton_status baton_decode_attn(baton_cache* cache, int32_t layer, const void* q, const void* k_new,
                                const void* v_new, void* out, float scale, void* ws, size_t ws_bytes,
                                hipStream_t stream);
+
+/*
+ * baton_decode_attn without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, results and errors as
+ * baton_decode_attn (bit for bit the same output), but the work list and the
+ * split-K partial sums live in a scratch array of BATON_SCRATCH_BYTES that the
+ * library keeps in the memory of each GPU it runs on until the process ends.
+ * The call itself allocates nothing.  A step needs 32 bytes per work item, 16
+ * per slot and 4 * (head_dim + 4) * n_q_heads bytes per work item of one
+ * kv-head's items, each region rounded up to 256 bytes (work items: a
+ * row's cached tokens plus one, cut every split tokens; about 550 items and
+ * 18 MB for 128 slots of 8192 tokens with 64 query heads over 8 kv-heads).
+ * Every call on one GPU shares that GPU's scratch and finds there what the
+ * last call left: a step's first call (or the first after another cache used
+ * the scratch) writes the work list again.  Calls whose work overlaps in time
+ * on one GPU (on different streams) race on the scratch and give undefined
+ * results; calls in one stream's order, for one cache or several, do not.
+ * Errors: those of baton_decode_attn without the workspace's (EINVAL for a
+ * null or misaligned pointer, a layer out of range or a scale not finite;
+ * ESTATE; ECAPACITY), ESCRATCH (the step needs more than BATON_SCRATCH_BYTES:
+ * nothing is enqueued; a larger split, baton_set_split_tokens, needs less),
+ * EHIP (the GPU holding the cache or the scratch's address could not be
+ * determined).
+ */
+#define BATON_SCRATCH_BYTES (64u << 20)
+baton_status baton_decode_attn_noalloc(baton_cache* cache, int32_t layer, const void* q, const void* k_new,
+                                       const void* v_new, void* out, float scale, hipStream_t stream);
 
 /*
  * Enqueue the placeholder writes evictions still owe (see baton_kv_evict), so

@@ -12,9 +12,11 @@ import os
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbaton.so")
 
-BATON_OK, BATON_EINVAL, BATON_ESLOT, BATON_ECAPACITY, BATON_EDTYPE, BATON_ESTATE, BATON_EHIP = range(7)
+BATON_OK, BATON_EINVAL, BATON_ESLOT, BATON_ECAPACITY, BATON_EDTYPE, BATON_ESTATE, BATON_EHIP, \
+    BATON_ESCRATCH = range(8)
 STATUS_NAMES = ["BATON_OK", "BATON_EINVAL", "BATON_ESLOT", "BATON_ECAPACITY", "BATON_EDTYPE",
-                "BATON_ESTATE", "BATON_EHIP"]
+                "BATON_ESTATE", "BATON_EHIP", "BATON_ESCRATCH"]
+BATON_SCRATCH_BYTES = 64 << 20
 BATON_F32, BATON_BF16 = 0, 1
 BATON_FILL_NEG_INF_F32 = 0xFF800000
 BATON_FILL_NEG_INF_BF16 = 0xFF80
@@ -66,6 +68,7 @@ def lib():
         L.baton_decode_attn_workspace_bytes.argtypes = [vp]
         L.baton_decode_attn_workspace_bytes.restype = ctypes.c_size_t
         L.baton_decode_attn.argtypes = [vp, i32, vp, vp, vp, vp, ctypes.c_float, vp, ctypes.c_size_t, vp]
+        L.baton_decode_attn_noalloc.argtypes = [vp, i32, vp, vp, vp, vp, ctypes.c_float, vp]
         L.baton_step_advance.argtypes = [vp]
         L.baton_cache_flush.argtypes = [vp, vp]
         L.baton_cache_query.argtypes = [vp, P(i64), P(i64), P(i32)]
@@ -87,7 +90,7 @@ def lib():
         L.baton_status_string.restype = ctypes.c_char_p
         for name in ("baton_cache_create", "baton_cache_destroy", "baton_kv_evict", "baton_kv_embed",
                      "baton_kv_extract",
-                     "baton_build_mask", "baton_decode_attn", "baton_step_advance",
+                     "baton_build_mask", "baton_decode_attn", "baton_decode_attn_noalloc", "baton_step_advance",
                      "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
                      "baton_shape_insert", "baton_cache_tokens", "baton_kv_move", "baton_gemm_create",
                      "baton_gemm_destroy", "baton_linear", "baton_linear_pack", "baton_linear_packed",
@@ -199,6 +202,12 @@ def baton_decode_attn(cache, layer, q, k_new, v_new, out, scale, ws, ws_bytes, s
     _check(lib().baton_decode_attn(cache, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
                                    float(scale), _ptr(ws), ws_bytes, _stream(stream)),
            "baton_decode_attn")
+
+
+def baton_decode_attn_noalloc(cache, layer, q, k_new, v_new, out, scale, stream=None):
+    _check(lib().baton_decode_attn_noalloc(cache, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
+                                           float(scale), _stream(stream)),
+           "baton_decode_attn_noalloc")
 
 
 def baton_cache_flush(cache, stream=None):

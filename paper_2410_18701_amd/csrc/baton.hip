@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -74,7 +75,14 @@ struct baton_cache {
   bool meta_valid = false;
   int32_t n_items = 0;
   int32_t n_multi = 0;     // rows with several items
+  int dev = -1;            // the GPU holding K and V (found by the first no-allocation call)
 };
+
+// The work list and split-K partials of baton_decode_attn_noalloc: one array
+// per GPU, held until the process ends.  Host code never passes `scratch`
+// itself to a kernel (in host code it names a host-side stand-in); it uses
+// the device address hipGetSymbolAddress gives for each device.
+static __device__ __align__(256) uint8_t scratch[BATON_SCRATCH_BYTES];
 
 namespace {
 
@@ -406,6 +414,19 @@ void plan_items(baton_cache* c, baton::MetaArgs& m, int64_t& items, int64_t& mul
   }
 }
 
+// The workspace laid out for exactly `items` work items.
+WsLayout ws_exact(const baton_cache* c, int64_t items) {
+  WsLayout w;
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  w.max_items = items;
+  w.items_off = 0;
+  w.multi_off = up(sizeof(baton::Item) * (size_t)items);
+  w.partial_off = up(w.multi_off + sizeof(int4) * (size_t)c->d.batch);
+  w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * items * c->group *
+                                   (c->d.head_dim + 4));
+  return w;
+}
+
 // One layer of the step, after the checks: the owed placeholder writes (first
 // layer), the work list when `m` is given (written into the workspace at wsb
 // with layout w), the attention launches, and the prefill of new queries.
@@ -491,6 +512,30 @@ baton_status attn_run(baton_cache* c, int32_t layer, const void* q, const void* 
   return BATON_OK;
 }
 
+// ------------------------------------------------------ static scratch --
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];               // device address of `scratch` on each GPU
+const baton_cache* g_scratch_owner[kMaxDevices]; // whose work list the scratch holds
+
+// The scratch address on device dev, looked up once with that device current.
+baton_status scratch_on(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return BATON_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return BATON_EHIP;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return BATON_EHIP;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev && hipSetDevice(cur) != hipSuccess) return BATON_EHIP;
+    if (e != hipSuccess || !p) return BATON_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return BATON_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -504,6 +549,7 @@ const char* baton_status_string(baton_status s) {
     case BATON_EDTYPE: return "unsupported element type, head_dim or head grouping";
     case BATON_ESTATE: return "call out of order with the decode step in progress";
     case BATON_EHIP: return "HIP runtime error";
+    case BATON_ESCRATCH: return "the step's work list and partial sums exceed the static scratch";
   }
   return "unknown status";
 }
@@ -577,6 +623,10 @@ baton_status baton_cache_create(const baton_cache_desc* desc, uint32_t flags, hi
 }
 
 baton_status baton_cache_destroy(baton_cache* c) {
+  if (c && c->dev >= 0 && c->dev < kMaxDevices) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_owner[c->dev] == c) g_scratch_owner[c->dev] = nullptr;
+  }
   delete c;
   return BATON_OK;
 }
@@ -802,6 +852,41 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
     return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, stream);
   }
   return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, nullptr, 0, 0, stream);
+}
+
+baton_status baton_decode_attn_noalloc(baton_cache* c, int32_t layer, const void* q, const void* k_new,
+                                       const void* v_new, void* out, float scale, hipStream_t stream) {
+  baton_status st = attn_check(c, layer, q, k_new, v_new, out, scale);
+  if (st != BATON_OK) return st;
+  if (c->dev < 0) {   // the GPU that holds the cache, found once
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, c->d.k) != hipSuccess) return BATON_EHIP;
+    c->dev = attr.device;
+  }
+  void* sp = nullptr;
+  st = scratch_on(c->dev, &sp);
+  if (st != BATON_OK) return st;
+  char* wsb = static_cast<char*>(sp);
+  bool mine;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    mine = g_scratch_owner[c->dev] == c;
+  }
+  if (!c->meta_valid || c->meta_ws != sp || !mine) {
+    // A new work list: this step's, or the scratch last held another cache's.
+    baton::MetaArgs m;
+    int64_t items, multi;
+    plan_items(c, m, items, multi);
+    const WsLayout w = ws_exact(c, items);
+    if (w.total > BATON_SCRATCH_BYTES) return BATON_ESCRATCH;
+    st = attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, stream);
+    if (st == BATON_OK) {
+      std::lock_guard<std::mutex> lock(g_scratch_mu);
+      g_scratch_owner[c->dev] = c;
+    }
+    return st;
+  }
+  return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, ws_exact(c, c->n_items), nullptr, 0, 0, stream);
 }
 
 baton_status baton_cache_flush(baton_cache* c, hipStream_t stream) {

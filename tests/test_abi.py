@@ -28,7 +28,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in range(7):
+    for s in range(8):
         assert B.baton_status_string(s) != "unknown status"
     assert B.baton_status_string(99) == "unknown status"
 
@@ -107,6 +107,11 @@ def test_host_checks_leave_state_unchanged():
         assert status(B.baton_decode_attn, h, 0, 0, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws) == B.BATON_EINVAL
         assert status(B.baton_decode_attn, h, 0, FAKE_K, FAKE_K, FAKE_K, FAKE_K, 0.0, FAKE_V, ws - 1) == B.BATON_EINVAL
         assert status(B.baton_decode_attn, h, 0, FAKE_K, FAKE_K, FAKE_K, FAKE_K, float("nan"), FAKE_V, ws) == B.BATON_EINVAL
+        nd = B.baton_decode_attn_noalloc
+        assert status(nd, h, 2, FAKE_K, FAKE_K, FAKE_K, FAKE_K, 0.0) == B.BATON_EINVAL          # layer
+        assert status(nd, h, 0, FAKE_K, 0, FAKE_K, FAKE_K, 0.0) == B.BATON_EINVAL               # null k_new
+        assert status(nd, h, 0, FAKE_K, FAKE_K, FAKE_K, FAKE_K + 2, 0.0) == B.BATON_EINVAL      # misaligned
+        assert status(nd, h, 0, FAKE_K, FAKE_K, FAKE_K, FAKE_K, float("inf"), 0) == B.BATON_EINVAL
         assert status(B.baton_build_mask, h, 0, 1) == B.BATON_EINVAL
         assert status(B.baton_build_mask, h, FAKE_K, 0) == B.BATON_EINVAL   # ld < L + 1
         assert status(B.baton_set_split_tokens, h, 100) == B.BATON_EINVAL
