@@ -367,37 +367,21 @@ baton_status baton_set_split_tokens(baton_cache* cache, int32_t tokens);
  * W^Q, W^K, W^V projections, attention, feed-forward networks between).
  * These calls are the rest of such a layer, so that a decode step runs end to
  * end: RMS normalisation, the projections (the library's weight-streaming
- * kernel on packed weights up to 64 rows, hipBLASLt GEMMs on stored weights),
- * rotary position embedding at each query's own position, the gated
- * feed-forward, and fused forms of the projections with the step that follows
- * them.  bf16 only; every output is rounded to nearest even.
+ * kernel on packed weights, up to BATON_GEMM_MAX_ROWS rows), rotary position
+ * embedding at each query's own position, the gated feed-forward, and fused
+ * forms of the projections with the step that follows them.  bf16 only;
+ * every output is rounded to nearest even.
  */
-typedef struct baton_gemm baton_gemm; /* opaque: a hipBLASLt handle and its cached algorithm choices */
-
-/* Create / free a GEMM handle (hipBLASLt keeps internal resources of its own).
-   Errors: EINVAL (null out), EHIP. */
-baton_status baton_gemm_create(baton_gemm** out);
-baton_status baton_gemm_destroy(baton_gemm* gemm);
+#define BATON_GEMM_MAX_ROWS 256
 
 /*
- * y[r] (+)= x[r] . W^T for r < rows: x device [rows][in_dim], W device
- * [out_dim][in_dim] (a linear layer's stored weight), y device [rows][out_dim];
- * accumulate = 1 adds to y (the residual stream), 0 overwrites it.  fp32
- * accumulation.  ws: device workspace the GEMM may use (ws_bytes, may be 0).
- * The algorithm is hipBLASLt's first choice for the shape, kept per handle.
- * Errors: EINVAL (null or misaligned pointer, sizes < 1 or not multiples of 8,
- * accumulate not 0/1), EDTYPE (dtype not bf16), EHIP (no algorithm fits).
- */
-baton_status baton_linear(baton_gemm* gemm, int32_t dtype, const void* x, const void* w, void* y,
-                          int32_t rows, int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws,
-                          size_t ws_bytes, hipStream_t stream);
-
-/*
- * The same product at a decode step's batch (rows <= 64) on the library's
- * weight-streaming kernel, which reads the weight in a packed form made once
- * per weight by baton_linear_pack.  The weight dominates the traffic of such
- * a product and is read exactly once; the packed form lets each wave stream it
- * in contiguous 1 KB blocks.
+ * y[r] (+)= x[r] . W^T for r < rows <= BATON_GEMM_MAX_ROWS (a linear layer at a
+ * decode step's batch) on the library's weight-streaming kernel, which reads
+ * the weight in a packed form made once per weight by baton_linear_pack.  The
+ * weight dominates the traffic of such a product and is read once from HBM
+ * (rows past 64 are taken in chunks of 64 by workgroups that run together,
+ * the later chunks finding the weight in the last-level cache); the packed
+ * form lets each wave stream it in contiguous 1 KB blocks.
  *
  * baton_linear_packed_bytes: bytes of the packed form of an [out_dim][in_dim]
  * weight: 2 * ceil(out_dim / 16) * 16 * ceil(in_dim / 32) * 32 (0 for sizes < 1).
@@ -410,14 +394,16 @@ baton_status baton_linear(baton_gemm* gemm, int32_t dtype, const void* x, const 
  * Errors: EINVAL (null or misaligned pointer, sizes < 1 or not multiples of
  * 8), EDTYPE (not bf16), EHIP.
  *
- * baton_linear_packed: y[r] (+)= x[r] . W^T for r < rows <= 64, W given by its
- * packed form wp; x, y, accumulate as in baton_linear.  fp32 accumulation;
+ * baton_linear_packed: y[r] (+)= x[r] . W^T for r < rows <= BATON_GEMM_MAX_ROWS,
+ * W given by its packed form wp; x device [rows][in_dim], y device
+ * [rows][out_dim], both 16-byte aligned; accumulate = 1 adds to y (the
+ * residual stream), 0 overwrites it.  fp32 accumulation;
  * when the output has few 16-row slices the sum is split along in_dim and the
  * fp32 partial sums, kept in ws (device, caller-owned; as many splits as
  * ws_bytes holds rows * out_dim floats for, none with ws_bytes = 0), are added
  * in a second launch in a fixed order.  Errors: EINVAL (null or misaligned
- * pointer, rows outside 1..64, sizes < 1 or not multiples of 8, accumulate not
- * 0/1), EDTYPE, EHIP.
+ * pointer, rows outside 1..BATON_GEMM_MAX_ROWS, sizes < 1 or not multiples of
+ * 8, accumulate not 0/1), EDTYPE, EHIP.
  */
 size_t baton_linear_packed_bytes(int32_t out_dim, int32_t in_dim);
 baton_status baton_linear_pack(int32_t dtype, const void* w, void* wp, int32_t out_dim, int32_t in_dim,
@@ -448,10 +434,11 @@ baton_status baton_linear_packed_rmsnorm(int32_t dtype, const void* x, const voi
  * j < F = out_dim / 2 -- bit for bit baton_linear_packed with ws_bytes = 0
  * (the k-sum unsplit) into a [rows][out_dim] buffer followed by
  * baton_silu_mul, without writing or reading that buffer or a second launch.  W is [gate; up] ([out_dim][in_dim],
- * gate rows first) in its packed form wp; x device [rows <= 64][in_dim], y
- * device [rows][F].  Never splits along in_dim (no workspace).
- * Errors: EINVAL (null or misaligned pointer, rows outside 1..64, out_dim not a
- * positive multiple of 32, in_dim < 8 or not a multiple of 8), EDTYPE, EHIP.
+ * gate rows first) in its packed form wp; x device [rows <= BATON_GEMM_MAX_ROWS]
+ * [in_dim], y device [rows][F].  Never splits along in_dim (no workspace).
+ * Errors: EINVAL (null or misaligned pointer, rows outside
+ * 1..BATON_GEMM_MAX_ROWS, out_dim not a positive multiple of 32, in_dim < 8 or
+ * not a multiple of 8), EDTYPE, EHIP.
  */
 baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
                                       int32_t out_dim, int32_t in_dim, hipStream_t stream);

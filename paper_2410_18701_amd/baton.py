@@ -17,6 +17,7 @@ BATON_OK, BATON_EINVAL, BATON_ESLOT, BATON_ECAPACITY, BATON_EDTYPE, BATON_ESTATE
 STATUS_NAMES = ["BATON_OK", "BATON_EINVAL", "BATON_ESLOT", "BATON_ECAPACITY", "BATON_EDTYPE",
                 "BATON_ESTATE", "BATON_EHIP", "BATON_ESCRATCH"]
 BATON_SCRATCH_BYTES = 64 << 20
+BATON_GEMM_MAX_ROWS = 256
 BATON_F32, BATON_BF16 = 0, 1
 BATON_FILL_NEG_INF_F32 = 0xFF800000
 BATON_FILL_NEG_INF_BF16 = 0xFF80
@@ -73,9 +74,6 @@ def lib():
         L.baton_cache_flush.argtypes = [vp, vp]
         L.baton_cache_query.argtypes = [vp, P(i64), P(i64), P(i32)]
         L.baton_set_split_tokens.argtypes = [vp, i32]
-        L.baton_gemm_create.argtypes = [P(vp)]
-        L.baton_gemm_destroy.argtypes = [vp]
-        L.baton_linear.argtypes = [vp, i32, vp, vp, vp, i32, i32, i32, i32, vp, ctypes.c_size_t, vp]
         L.baton_linear_packed_bytes.argtypes = [i32, i32]
         L.baton_linear_packed_bytes.restype = ctypes.c_size_t
         L.baton_linear_pack.argtypes = [i32, vp, vp, i32, i32, vp]
@@ -92,8 +90,7 @@ def lib():
                      "baton_kv_extract",
                      "baton_build_mask", "baton_decode_attn", "baton_decode_attn_noalloc", "baton_step_advance",
                      "baton_cache_query", "baton_set_split_tokens", "baton_cache_flush",
-                     "baton_shape_insert", "baton_cache_tokens", "baton_kv_move", "baton_gemm_create",
-                     "baton_gemm_destroy", "baton_linear", "baton_linear_pack", "baton_linear_packed",
+                     "baton_shape_insert", "baton_cache_tokens", "baton_kv_move", "baton_linear_pack", "baton_linear_packed",
                      "baton_linear_packed_rmsnorm", "baton_linear_packed_silu",
                      "baton_rmsnorm", "baton_rope_qkv", "baton_silu_mul"):
             getattr(L, name).restype = st
@@ -233,21 +230,6 @@ def baton_set_split_tokens(cache, tokens):
 
 
 # ---- decode layer around the attention ----
-def baton_gemm_create():
-    out = ctypes.c_void_p()
-    _check(lib().baton_gemm_create(ctypes.byref(out)), "baton_gemm_create")
-    return out.value
-
-
-def baton_gemm_destroy(gemm):
-    _check(lib().baton_gemm_destroy(gemm), "baton_gemm_destroy")
-
-
-def baton_linear(gemm, dtype, x, w, y, rows, out_dim, in_dim, accumulate, ws, ws_bytes, stream=None):
-    _check(lib().baton_linear(gemm, dtype, _ptr(x), _ptr(w), _ptr(y), rows, out_dim, in_dim,
-                              int(accumulate), _ptr(ws), ws_bytes, _stream(stream)), "baton_linear")
-
-
 def baton_linear_packed_bytes(out_dim, in_dim):
     return lib().baton_linear_packed_bytes(out_dim, in_dim)
 

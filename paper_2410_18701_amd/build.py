@@ -17,7 +17,7 @@ FLAGS = [
 
 
 def build(verbose=False, extra=()):
-    cmd = ["hipcc", *FLAGS, *extra, *SOURCES, "-lhipblaslt", "-o", LIB + ".tmp"]
+    cmd = ["hipcc", *FLAGS, *extra, *SOURCES, "-o", LIB + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True, cwd=HERE)

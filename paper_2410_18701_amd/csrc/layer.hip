@@ -1,53 +1,19 @@
 // Host side of the decode-layer operations around the attention: the
-// projections (hipBLASLt on stored weights; the weight-streaming GEMM on
-// packed weights up to 64 rows), launches of the row and elementwise kernels.
+// projections on the library's weight-streaming GEMM over packed weights (up
+// to 256 rows), launches of the row and elementwise kernels.
 // The C ABI is documented in include/baton.h.
 #include <hip/hip_runtime.h>
-#include <hipblaslt/hipblaslt.h>
 
 #include <algorithm>
 #include <cmath>
-#include <map>
 #include <new>
-#include <tuple>
 
 #include "baton.h"
 #include "layer_ops.hpp"
 
-struct baton_gemm {
-  hipblasLtHandle_t lt = nullptr;
-  // Algorithm choice per (rows, out_dim, in_dim, 0, workspace bytes).
-  std::map<std::tuple<int32_t, int32_t, int32_t, int32_t, size_t>, hipblasLtMatmulAlgo_t> algos;
-};
-
 namespace {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-struct LtDescs {
-  hipblasLtMatmulDesc_t op = nullptr;
-  hipblasLtMatrixLayout_t a = nullptr, b = nullptr, c = nullptr;
-  ~LtDescs() {
-    if (a) hipblasLtMatrixLayoutDestroy(a);
-    if (b) hipblasLtMatrixLayoutDestroy(b);
-    if (c) hipblasLtMatrixLayoutDestroy(c);
-    if (op) hipblasLtMatmulDescDestroy(op);
-  }
-};
-
-// y [rows][out] = x [rows][in] . w [out][in]^T in column-major terms:
-// y^T (out x rows) = op(A) . op(B) with A = w viewed as in x out (transposed)
-// and B = x viewed as in x rows.
-bool make_descs(LtDescs& d, int32_t rows, int32_t out, int32_t in) {
-  const hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
-  if (hipblasLtMatmulDescCreate(&d.op, HIPBLAS_COMPUTE_32F, HIP_R_32F) != HIPBLAS_STATUS_SUCCESS) return false;
-  if (hipblasLtMatmulDescSetAttribute(d.op, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof(ta)) != HIPBLAS_STATUS_SUCCESS ||
-      hipblasLtMatmulDescSetAttribute(d.op, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof(tb)) != HIPBLAS_STATUS_SUCCESS)
-    return false;
-  return hipblasLtMatrixLayoutCreate(&d.a, HIP_R_16BF, in, out, in) == HIPBLAS_STATUS_SUCCESS &&
-         hipblasLtMatrixLayoutCreate(&d.b, HIP_R_16BF, in, rows, in) == HIPBLAS_STATUS_SUCCESS &&
-         hipblasLtMatrixLayoutCreate(&d.c, HIP_R_16BF, out, rows, out) == HIPBLAS_STATUS_SUCCESS;
-}
 
 #ifndef BATON_GEMM_TARGET_WAVES
 #define BATON_GEMM_TARGET_WAVES 1024   // weight slices x splits when the slices alone are too few
@@ -68,58 +34,6 @@ void launch_skinny_mg(const baton::SkinnyArgs& a, dim3 grid, hipStream_t s) {
 }  // namespace
 
 extern "C" {
-
-baton_status baton_gemm_create(baton_gemm** out) {
-  if (!out) return BATON_EINVAL;
-  baton_gemm* g = new (std::nothrow) baton_gemm();
-  if (!g) return BATON_EINVAL;
-  if (hipblasLtCreate(&g->lt) != HIPBLAS_STATUS_SUCCESS) {
-    delete g;
-    return BATON_EHIP;
-  }
-  *out = g;
-  return BATON_OK;
-}
-
-baton_status baton_gemm_destroy(baton_gemm* g) {
-  if (g) {
-    if (g->lt) hipblasLtDestroy(g->lt);
-    delete g;
-  }
-  return BATON_OK;
-}
-
-baton_status baton_linear(baton_gemm* g, int32_t dtype, const void* x, const void* w, void* y,
-                          int32_t rows, int32_t out_dim, int32_t in_dim, int32_t accumulate, void* ws,
-                          size_t ws_bytes, hipStream_t stream) {
-  if (!g || !x || !w || !y || rows < 1 || out_dim < 1 || in_dim < 1 || (ws_bytes && !ws)) return BATON_EINVAL;
-  if (accumulate != 0 && accumulate != 1) return BATON_EINVAL;
-  if (dtype != BATON_BF16) return BATON_EDTYPE;
-  if (!aligned16(x) || !aligned16(w) || !aligned16(y) || in_dim % 8 || out_dim % 8) return BATON_EINVAL;
-  LtDescs d;
-  if (!make_descs(d, rows, out_dim, in_dim)) return BATON_EHIP;
-  const auto key = std::make_tuple(rows, out_dim, in_dim, 0, ws_bytes);
-  auto it = g->algos.find(key);
-  if (it == g->algos.end()) {
-    // hipBLASLt's first choice.  (Timing its candidates back to back was
-    // measured and misleads: the repeated weight matrix stays in the caches,
-    // while a decode step reads each weight once from HBM.)
-    hipblasLtMatmulPreference_t pref;
-    if (hipblasLtMatmulPreferenceCreate(&pref) != HIPBLAS_STATUS_SUCCESS) return BATON_EHIP;
-    const uint64_t max_ws = ws_bytes;
-    hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &max_ws, sizeof(max_ws));
-    hipblasLtMatmulHeuristicResult_t res[1];
-    int n = 0;
-    const hipblasStatus_t st = hipblasLtMatmulAlgoGetHeuristic(g->lt, d.op, d.a, d.b, d.c, d.c, pref, 1, res, &n);
-    hipblasLtMatmulPreferenceDestroy(pref);
-    if (st != HIPBLAS_STATUS_SUCCESS || n < 1 || res[0].workspaceSize > ws_bytes) return BATON_EHIP;
-    it = g->algos.emplace(key, res[0].algo).first;
-  }
-  const float alpha = 1.f, beta = accumulate ? 1.f : 0.f;
-  const hipblasStatus_t st = hipblasLtMatmul(g->lt, d.op, &alpha, w, d.a, x, d.b, &beta, y, d.c, y, d.c,
-                                             &it->second, ws, ws_bytes, stream);
-  return st == HIPBLAS_STATUS_SUCCESS ? BATON_OK : BATON_EHIP;
-}
 
 size_t baton_linear_packed_bytes(int32_t out_dim, int32_t in_dim) {
   if (out_dim < 1 || in_dim < 1) return 0;
@@ -149,7 +63,7 @@ namespace {
 baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows, int32_t out_dim,
                            int32_t in_dim, int32_t accumulate, const void* gain, float eps, void* y_norm, void* ws,
                            size_t ws_bytes, hipStream_t stream) {
-  if (!x || !wp || !y || rows < 1 || rows > 64 || out_dim < 1 || in_dim < 1 || (ws_bytes && !ws))
+  if (!x || !wp || !y || rows < 1 || rows > BATON_GEMM_MAX_ROWS || out_dim < 1 || in_dim < 1 || (ws_bytes && !ws))
     return BATON_EINVAL;
   if (gain && (!y_norm || !aligned16(gain) || !aligned16(y_norm) || !(eps >= 0.f) || !std::isfinite(eps)))
     return BATON_EINVAL;
@@ -157,16 +71,16 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   if (dtype != BATON_BF16) return BATON_EDTYPE;
   if (!aligned16(x) || !aligned16(wp) || !aligned16(y) || in_dim % 8 || out_dim % 8 || in_dim > (1 << 24))
     return BATON_EINVAL;
-  // 16-row weight slices; with fewer than BATON_GEMM_MIN_SLICES of them,
-  // split along k into about BATON_GEMM_TARGET_WAVES / slices ranges (at least
-  // 8 blocks of 32 each, and only as many as the workspace holds partial sums
-  // for).  Measured on the llama2-7b shapes at 64 rows: the split's partial
-  // sums and second launch cost more than they gain once the slices alone
-  // give two waves per SIMD.
-  const int32_t slices = (out_dim + 15) / 16, kt = (in_dim + 31) / 32;
+  // 16-row weight slices, each streamed by a wave per 64-row chunk of x;
+  // with fewer than BATON_GEMM_MIN_SLICES such waves, split along k into about
+  // BATON_GEMM_TARGET_WAVES / waves ranges (at least 8 blocks of 32 each, and
+  // only as many as the workspace holds partial sums for).  Measured on the
+  // llama2-7b shapes at 64 rows: the split's partial sums and second launch
+  // cost more than they gain once the slices alone give two waves per SIMD.
+  const int32_t slices = (out_dim + 15) / 16, kt = (in_dim + 31) / 32, chunks = (rows + 63) / 64;
   int32_t S = 1;
-  if (slices < BATON_GEMM_MIN_SLICES)
-    S = std::max(1, std::min((BATON_GEMM_TARGET_WAVES + slices - 1) / slices, kt / 8));
+  if (slices * chunks < BATON_GEMM_MIN_SLICES)
+    S = std::max(1, std::min((BATON_GEMM_TARGET_WAVES + slices * chunks - 1) / (slices * chunks), kt / 8));
   if (!ws || !aligned16(ws)) S = 1;
   while (S > 1 && (size_t)S * rows * out_dim * sizeof(float) > ws_bytes) --S;
   const int32_t tc = (kt + S - 1) / S;
@@ -183,8 +97,9 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   a.tc = tc;
   a.accumulate = accumulate;
   a.gated = 0;
-  const dim3 grid((unsigned)((slices + baton::kGemmWaves - 1) / baton::kGemmWaves), (unsigned)S);
-  switch ((rows + 15) / 16) {
+  a.chunks = chunks;
+  const dim3 grid((unsigned)((slices + baton::kGemmWaves - 1) / baton::kGemmWaves * chunks), (unsigned)S);
+  switch (std::min(4, (rows + 15) / 16)) {
     case 1: launch_skinny_mg<1>(a, grid, stream); break;
     case 2: launch_skinny_mg<2>(a, grid, stream); break;
     case 3: launch_skinny_mg<3>(a, grid, stream); break;
@@ -228,8 +143,8 @@ baton_status baton_linear_packed_rmsnorm(int32_t dtype, const void* x, const voi
 
 baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* wp, void* y, int32_t rows,
                                       int32_t out_dim, int32_t in_dim, hipStream_t stream) {
-  if (!x || !wp || !y || rows < 1 || rows > 64 || out_dim < 32 || out_dim % 32 || in_dim < 8 || in_dim % 8 ||
-      in_dim > (1 << 24))
+  if (!x || !wp || !y || rows < 1 || rows > BATON_GEMM_MAX_ROWS || out_dim < 32 || out_dim % 32 || in_dim < 8 ||
+      in_dim % 8 || in_dim > (1 << 24))
     return BATON_EINVAL;
   if (dtype != BATON_BF16) return BATON_EDTYPE;
   if (!aligned16(x) || !aligned16(wp) || !aligned16(y)) return BATON_EINVAL;
@@ -245,8 +160,9 @@ baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* 
   a.tc = a.kt;   // never split along k: the epilogue needs the whole sum
   a.accumulate = 0;
   a.gated = out_dim / 2;
-  const dim3 grid((unsigned)((out_dim / 32 + 1) / 2), 1);   // two gate slices per workgroup
-  switch ((rows + 15) / 16) {
+  a.chunks = (rows + 63) / 64;
+  const dim3 grid((unsigned)((out_dim / 32 + 1) / 2 * a.chunks), 1);   // two gate slices per workgroup
+  switch (std::min(4, (rows + 15) / 16)) {
     case 1: launch_skinny_mg<1>(a, grid, stream); break;
     case 2: launch_skinny_mg<2>(a, grid, stream); break;
     case 3: launch_skinny_mg<3>(a, grid, stream); break;

@@ -110,9 +110,13 @@ __global__ void __launch_bounds__(256) silu_mul_kernel(const u32x4* __restrict__
 }
 
 // ------------------------------------------------------------ skinny GEMM --
-// y[m][n] (+)= sum_k x[m][k] w[n][k] for m < rows <= 64: a linear layer at a
-// decode step's batch.  The weight matrix (megabytes) is read exactly once and
-// dominates the traffic; x (rows x K) is small and stays in the caches.
+// y[m][n] (+)= sum_k x[m][k] w[n][k] for m < rows <= 256: a linear layer at a
+// decode step's batch.  The weight matrix (megabytes) is read once from HBM
+// and dominates the traffic; x (rows x K) is small and stays in the caches.
+// A workgroup takes 64 of the rows (grid z: chunks of 64 rows); the chunks of
+// one weight slice group are consecutive workgroups, which run at the same
+// time, so the weight bytes a second chunk reads come from the last-level
+// cache rather than HBM.
 //
 // The weight is used in a packed form, made once per weight by
 // pack_weight_kernel: 16-row slices of w, each a run of 1 KB blocks, one per
@@ -137,7 +141,8 @@ struct SkinnyArgs {
   const uint16_t* wp;    // packed weight: [ceil(N / 16)][ceil(K / 32)] blocks of 512 elements
   uint16_t* y;           // [rows][N]
   float* part;           // [S][rows][N] fp32, when S > 1
-  int32_t rows, N, K;
+  int32_t rows, N, K;    // rows <= 256
+  int32_t chunks;        // ceil(rows / 64): grid x is slice groups x chunks, the chunk fastest
   int32_t kt;            // blocks per slice, ceil(K / 32)
   int32_t tc;            // blocks per split
   int32_t accumulate;    // 1: y += x . w^T
@@ -189,8 +194,8 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
   // Gated: waves 0 and 1 take gate slices 2 x and 2 x + 1, waves 2 and 3 the
   // up slices of the same output columns (F / 16 further).
   static_assert(kGemmWaves == 4, "the gated epilogue pairs two gate and two up slices");
-  const int32_t slice = a.gated ? (w < 2 ? 2 * (int32_t)blockIdx.x + w : a.gated / 16 + 2 * (int32_t)blockIdx.x + w - 2)
-                                : (int32_t)blockIdx.x * kGemmWaves + w;
+  const int32_t grp = (int32_t)blockIdx.x / a.chunks;   // slice group
+  const int32_t slice = a.gated ? (w < 2 ? 2 * grp + w : a.gated / 16 + 2 * grp + w - 2) : grp * kGemmWaves + w;
   const int32_t n0 = slice * 16;
   const int32_t n_rows = max(0, min(16, a.N - n0));   // 0: a wave past N (loads nothing, writes nothing)
   const int32_t t_begin = blockIdx.y * a.tc, t_end = min(a.kt, t_begin + a.tc);
@@ -198,8 +203,10 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.wp) + ((int64_t)min(slice, (a.N + 15) / 16) * a.kt + t_begin) * 512, 0,
       n_rows > 0 ? (t_end - t_begin) * 1024 : 0, kGemmBufWord3);
+  const int32_t chunk = (int32_t)blockIdx.x % a.chunks;   // 64-row chunk of x and y
+  const int32_t xrow0 = 64 * chunk, rows = min(64, a.rows - xrow0);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.x), 0, (int32_t)(a.rows * row_bytes), kGemmBufWord3);
+      const_cast<uint16_t*>(a.x) + (int64_t)xrow0 * a.K, 0, (int32_t)(rows * row_bytes), kGemmBufWord3);
 
   gemm_f32x4 acc[MG];
 #pragma unroll
@@ -216,7 +223,7 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
       const int32_t p = tid + kWave * kGemmWaves * i;
       const int32_t m = p / Lds::kPieces, c = p % Lds::kPieces;
       const int32_t k = 32 * tb + 8 * c;
-      xr[i] = gemm_load<0>(rx, (m < a.rows && k < a.K && tb + c / 4 < t_end)
+      xr[i] = gemm_load<0>(rx, (m < rows && k < a.K && tb + c / 4 < t_end)
                                    ? (uint32_t)m * row_bytes + (uint32_t)k * 2u : kGemmOob);
     }
 #pragma unroll
@@ -302,7 +309,7 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
 #pragma unroll
       for (int j = 0; j < MG; ++j) {
         const int32_t m = 16 * j + c16;
-        if (m >= a.rows) continue;
+        if (m >= rows) continue;
         const uint2 u = ex[(w * MG + j) * kWave + lane];
         const uint32_t gw[2] = {pack_bf16(acc[j][0], acc[j][1]), pack_bf16(acc[j][2], acc[j][3])};
         const uint32_t uw[2] = {u.x, u.y};
@@ -313,7 +320,7 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
           const float s0 = g0 / (1.f + expf(-g0)), s1 = g1 / (1.f + expf(-g1));
           o[q] = pack_bf16(s0 * bf16_lo(uw[q]), s1 * bf16_hi(uw[q]));
         }
-        *reinterpret_cast<uint2*>(a.y + (int64_t)m * a.gated + n) = make_uint2(o[0], o[1]);
+        *reinterpret_cast<uint2*>(a.y + (int64_t)(xrow0 + m) * a.gated + n) = make_uint2(o[0], o[1]);
       }
     }
     return;
@@ -322,12 +329,12 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
 #pragma unroll
   for (int j = 0; j < MG; ++j) {
     const int32_t m = 16 * j + c16;
-    if (m >= a.rows) continue;
+    if (m >= rows) continue;
     if (gridDim.y > 1) {
-      *reinterpret_cast<float4*>(a.part + ((int64_t)blockIdx.y * a.rows + m) * a.N + n) =
+      *reinterpret_cast<float4*>(a.part + ((int64_t)blockIdx.y * a.rows + xrow0 + m) * a.N + n) =
           make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
     } else {
-      uint2* yp = reinterpret_cast<uint2*>(a.y + (int64_t)m * a.N + n);
+      uint2* yp = reinterpret_cast<uint2*>(a.y + (int64_t)(xrow0 + m) * a.N + n);
       float v0 = acc[j][0], v1 = acc[j][1], v2 = acc[j][2], v3 = acc[j][3];
       if (a.accumulate) {
         const uint2 old = *yp;

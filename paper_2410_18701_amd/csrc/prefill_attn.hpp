@@ -180,6 +180,10 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 #ifndef BATON_PREFILL_KT
 #define BATON_PREFILL_KT 64
 #endif
+#ifndef BATON_PREFILL_LAZY
+#define BATON_PREFILL_LAZY 8.0f
+#endif
+constexpr float kPrefillLazy = BATON_PREFILL_LAZY;
 #ifndef BATON_PREFILL_QG
 #define BATON_PREFILL_QG 1
 #endif
@@ -329,13 +333,26 @@ prefill_fa_kernel(const PrefillArgs a) {
 #pragma unroll
         for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e]);
         mx = max_over_groups(mx) * qscale;             // qscale >= 0: the max of the scaled scores
-        const float mn = fmaxf(m[gq], mx);
-        const float ref = mn == -INFINITY ? 0.f : mn;
-        // exponents are <= 0 here: the hardware exp2 (results below the
-        // smallest normal flush to 0, which a softmax weight may); the scale
-        // is applied in the exponent's multiply-add, the sum taken before P is
-        // rounded to bf16 for the matrix operation
-        const float alpha = __builtin_amdgcn_exp2f(m[gq] - ref);
+        // The reference the weights are taken against moves only when the
+        // block's maximum passes it by more than kPrefillLazy (base 2):
+        // softmax does not depend on the reference, the weights stay below
+        // 2^kPrefillLazy (well inside bf16's and fp32's range, at bf16's
+        // relative precision), and the accumulators are rescaled -- this
+        // lane's position by its own factor -- only when some position's
+        // reference moved, which after the first keys is rare.
+        if (__ballot(mx > m[gq] + kPrefillLazy)) {     // wave-uniform
+          const float mn = mx > m[gq] + kPrefillLazy ? mx : m[gq];
+          const float alpha = m[gq] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[gq] - mn);
+          lsum[gq] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[gq][dt] *= alpha;
+          m[gq] = mn;
+        }
+        const float ref = m[gq] == -INFINITY ? 0.f : m[gq];
+        // exponents are <= kPrefillLazy here: the hardware exp2 (results below
+        // the smallest normal flush to 0, which a softmax weight may); the
+        // scale is applied in the exponent's multiply-add, the sum taken
+        // before P is rounded to bf16 for the matrix operation
         float psum = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -343,15 +360,7 @@ prefill_fa_kernel(const PrefillArgs a) {
           pa[gq][e] = (__bf16)pf;
           psum += pf;
         }
-        lsum[gq] = lsum[gq] * alpha + psum;
-        m[gq] = mn;
-        // Rescale the accumulators (this lane's position's own factor) only
-        // when some position's maximum moved (after the first keys it rarely
-        // does).
-        if (__ballot(alpha != 1.f)) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[gq][dt] *= alpha;
-        }
+        lsum[gq] += psum;
       }
       const uint8_t* vblk = ldsV + kb * ROW + tr_off;
 #pragma unroll
@@ -440,4 +449,5 @@ prefill_fa_kernel(const PrefillArgs a) {
 }
 
 }  // namespace baton
+
 

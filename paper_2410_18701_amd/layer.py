@@ -23,26 +23,13 @@ class PackedWeight:
 
 
 class Gemm:
-    """A hipBLASLt handle for baton_linear, with a device workspace (also the
-    partial sums of baton_linear_packed)."""
+    """The device workspace of the projections (the partial sums of
+    baton_linear_packed when it splits along in_dim), and the projection calls."""
 
     def __init__(self, ws_bytes=32 << 20):
         import torch
-        self.handle = B.baton_gemm_create()
-        self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
-
-    def linear(self, x, w, y, accumulate=False):
-        """y (+)= x . w^T; x [rows][in], w [out][in], y [rows][out] (bf16, contiguous)."""
-        rows, in_dim = x.shape
-        out_dim = w.shape[0]
-        if w.shape[1] != in_dim or tuple(y.shape) != (rows, out_dim):
-            raise ValueError("linear: shapes do not match")
-        for t in (x, w, y):
-            if not t.is_contiguous():
-                raise ValueError("linear: contiguous tensors only")
-        B.baton_linear(self.handle, B.BATON_BF16, x, w, y, rows, out_dim, in_dim, accumulate, self.ws,
-                       self.ws.numel(), _stream())
-        return y
+        self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda") if ws_bytes else None
+        self.ws_bytes = ws_bytes
 
     def pack(self, w):
         """The packed form of a weight w [out][in] for linear_packed (made once per weight)."""
@@ -55,7 +42,7 @@ class Gemm:
         return PackedWeight(wp, out_dim, in_dim)
 
     def linear_packed(self, x, wp, y, accumulate=False):
-        """y (+)= x . w^T with w packed by pack(); x [rows <= 64][in], y [rows][out]."""
+        """y (+)= x . w^T with w packed by pack(); x [rows <= 256][in], y [rows][out]."""
         rows, in_dim = x.shape
         if in_dim != wp.in_dim or tuple(y.shape) != (rows, wp.out_dim):
             raise ValueError("linear_packed: shapes do not match")
@@ -63,7 +50,7 @@ class Gemm:
             if not t.is_contiguous():
                 raise ValueError("linear_packed: contiguous tensors only")
         B.baton_linear_packed(B.BATON_BF16, x, wp.data, y, rows, wp.out_dim, in_dim, accumulate, self.ws,
-                              self.ws.numel(), _stream())
+                              self.ws_bytes, _stream())
         return y
 
     def linear_packed_silu(self, x, wp, out):
@@ -89,13 +76,11 @@ class Gemm:
             if not t.is_contiguous():
                 raise ValueError("linear_packed_rmsnorm: contiguous tensors only")
         B.baton_linear_packed_rmsnorm(B.BATON_BF16, x, wp.data, y, rows, wp.out_dim, in_dim, accumulate, gain,
-                                      eps, y_norm, self.ws, self.ws.numel(), _stream())
+                                      eps, y_norm, self.ws, self.ws_bytes, _stream())
         return y
 
     def close(self):
-        if self.handle:
-            B.baton_gemm_destroy(self.handle)
-            self.handle = None
+        self.ws = None
 
 
 def rmsnorm(x, gain, y, eps):
@@ -128,22 +113,22 @@ class DecodeLayers:
     """The layers of one model over one BatonCache, with preallocated activations.
 
     weights[layer]: dict of bf16 device tensors norm1 [hid], qkv [(Hq + 2 Hkv) D][hid],
-    o [hid][Hq D], norm2 [hid], gate_up [2 F][hid], down [hid][F].  Up to 64 slots
-    the projections run on the weight-streaming GEMM over packed copies of the
-    weights, made here once (packed=False keeps hipBLASLt on the stored weights).
-    On the packed path each residual add is fused with the normalisation that
-    follows it (the output projection with norm2, the down projection with the
-    next layer's norm1), so layer(l + 1) expects x as layer(l) returned it, and
-    the gate/up projection with the gated activation."""
+    o [hid][Hq D], norm2 [hid], gate_up [2 F][hid], down [hid][F].  The projections
+    run on the weight-streaming GEMM over packed copies of the weights, made here
+    once.  Each residual add is fused with the normalisation that follows it (the
+    output projection with norm2, the down projection with the next layer's
+    norm1), so layer(l + 1) expects x as layer(l) returned it, and the gate/up
+    projection with the gated activation."""
 
     PROJ = ("qkv", "o", "gate_up", "down")
 
-    def __init__(self, cache, weights, gemm, theta=10000.0, eps=1e-5, packed=None):
+    def __init__(self, cache, weights, gemm, theta=10000.0, eps=1e-5):
         import torch
         self.cache, self.w, self.gemm, self.theta, self.eps = cache, weights, gemm, theta, eps
         Bt, Hq, Hkv, D = cache.batch, cache.n_q_heads, cache.n_kv_heads, cache.head_dim
-        self.packed = (Bt <= 64) if packed is None else packed
-        self.wp = [{k: gemm.pack(w[k]) for k in self.PROJ} for w in weights] if self.packed else None
+        if Bt > B.BATON_GEMM_MAX_ROWS:
+            raise ValueError(f"at most {B.BATON_GEMM_MAX_ROWS} slots")
+        self.wp = [{k: gemm.pack(w[k]) for k in self.PROJ} for w in weights]
         hid = weights[0]["norm1"].numel()
         F = weights[0]["down"].shape[1]
         e = lambda *s: torch.empty(s, dtype=torch.bfloat16, device="cuda")
@@ -154,32 +139,24 @@ class DecodeLayers:
 
     def layer(self, layer, x):
         """One layer of the decode step on the residual stream x [batch][hid] (in place)."""
-        w = self.w[layer]
-        if self.packed:
-            wp, lin = self.wp[layer], self.gemm.linear_packed
-        else:
-            wp, lin = w, self.gemm.linear
+        w, wp, g = self.w[layer], self.wp[layer], self.gemm
         if self._normed != (layer, x.data_ptr()):   # h holds norm1(x) after the previous layer
             rmsnorm(x, w["norm1"], self.h, self.eps)
         self._normed = None
-        lin(self.h, wp["qkv"], self.qkv)
+        g.linear_packed(self.h, wp["qkv"], self.qkv)
         rope_qkv(self.cache, self.qkv, self.q, self.k, self.v, self.theta)
         self.cache.decode_attn(layer, self.q, self.k, self.v, out=self.att)
         att = self.att.view(self.att.shape[0], -1)
-        if self.packed:
-            self.gemm.linear_packed_rmsnorm(att, wp["o"], x, w["norm2"], self.eps, self.h, accumulate=True)
+        g.linear_packed_rmsnorm(att, wp["o"], x, w["norm2"], self.eps, self.h, accumulate=True)
+        if wp["gate_up"].out_dim % 32 == 0:
+            g.linear_packed_silu(self.h, wp["gate_up"], self.act)
         else:
-            lin(att, wp["o"], x, accumulate=True)
-            rmsnorm(x, w["norm2"], self.h, self.eps)
-        if self.packed and wp["gate_up"].out_dim % 32 == 0:
-            self.gemm.linear_packed_silu(self.h, wp["gate_up"], self.act)
-        else:
-            lin(self.h, wp["gate_up"], self.gu)
+            g.linear_packed(self.h, wp["gate_up"], self.gu)
             silu_mul(self.gu, self.act)
-        if self.packed and layer + 1 < len(self.w):
-            self.gemm.linear_packed_rmsnorm(self.act, wp["down"], x, self.w[layer + 1]["norm1"], self.eps, self.h,
-                                            accumulate=True)
+        if layer + 1 < len(self.w):
+            g.linear_packed_rmsnorm(self.act, wp["down"], x, self.w[layer + 1]["norm1"], self.eps, self.h,
+                                    accumulate=True)
             self._normed = (layer + 1, x.data_ptr())
         else:
-            lin(self.act, wp["down"], x, accumulate=True)
+            g.linear_packed(self.act, wp["down"], x, accumulate=True)
         return x

@@ -439,6 +439,8 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
       ("scale", max_cells)           BatchScaler.shrink then grow at this threshold (the
                                      oracle repeats its parks and returns; `log` gets
                                      ("scale", parked slots, returned slots))
+      ("scale", max_cells, True)     the same with the return prefetched to device memory
+                                     on the scaler's second stream first
     After a step or a flush the whole ring is compared; after the other
     operations the live rows (evicted rows may still hold old tokens); once an
     eviction did not scrub, the live rows' tokens only.  scale: the attention
@@ -535,6 +537,8 @@ def run_script(shape, ops, seed=3, capacity=64, split=None, layout="by_layer", l
             for b in parked:                     # the oracle, in the same order
                 parked_cpu.append(pb.extract([b])[0])
                 pb.evict([b], release=True)
+            if len(op) > 2 and op[2]:
+                scaler.prefetch()
             back = scaler.grow()
             for b in back:
                 kh, vh = parked_cpu.pop(0)

@@ -161,7 +161,7 @@ def test_packed_linear_host_checks():
     assert status(B.baton_linear_pack, B.BATON_BF16, X, W, 64, 60) == B.BATON_EINVAL            # in % 8
     assert status(B.baton_linear_pack, B.BATON_F32, X, W, 64, 64) == B.BATON_EDTYPE
     lp = B.baton_linear_packed
-    assert status(lp, B.BATON_BF16, X, W, Y, 65, 64, 64, 0, 0, 0) == B.BATON_EINVAL           # rows > 64
+    assert status(lp, B.BATON_BF16, X, W, Y, 257, 64, 64, 0, 0, 0) == B.BATON_EINVAL          # rows > 256
     assert status(lp, B.BATON_BF16, X, W, Y, 0, 64, 64, 0, 0, 0) == B.BATON_EINVAL            # rows < 1
     assert status(lp, B.BATON_BF16, X, W, 0, 8, 64, 64, 0, 0, 0) == B.BATON_EINVAL            # null y
     assert status(lp, B.BATON_BF16, X, W + 4, Y, 8, 64, 64, 0, 0, 0) == B.BATON_EINVAL        # misaligned
@@ -175,12 +175,12 @@ def test_packed_linear_host_checks():
     assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G, 1e-5, 0, 0, 0) == B.BATON_EINVAL      # null y_norm
     assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G + 8, 1e-5, N, 0, 0) == B.BATON_EINVAL  # misaligned
     assert status(lpn, B.BATON_BF16, X, W, Y, 8, 64, 64, 1, G, -1.0, N, 0, 0) == B.BATON_EINVAL      # eps < 0
-    assert status(lpn, B.BATON_BF16, X, W, Y, 65, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EINVAL     # rows > 64
+    assert status(lpn, B.BATON_BF16, X, W, Y, 257, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EINVAL    # rows > 256
     assert status(lpn, B.BATON_F32, X, W, Y, 8, 64, 64, 1, G, 1e-5, N, 0, 0) == B.BATON_EDTYPE
     lps = B.baton_linear_packed_silu
     assert status(lps, B.BATON_BF16, X, W, 0, 8, 64, 64) == B.BATON_EINVAL       # null y
     assert status(lps, B.BATON_BF16, X, W, Y, 8, 48, 64) == B.BATON_EINVAL       # out % 32
-    assert status(lps, B.BATON_BF16, X, W, Y, 65, 64, 64) == B.BATON_EINVAL      # rows > 64
+    assert status(lps, B.BATON_BF16, X, W, Y, 257, 64, 64) == B.BATON_EINVAL     # rows > 256
     assert status(lps, B.BATON_BF16, X, W + 8, Y, 8, 64, 64) == B.BATON_EINVAL   # misaligned
     assert status(lps, B.BATON_BF16, X, W, Y, 8, 64, 60) == B.BATON_EINVAL       # in % 8
     assert status(lps, B.BATON_F32, X, W, Y, 8, 64, 64) == B.BATON_EDTYPE

@@ -44,24 +44,6 @@ def _close(got, want, rel=2.0 ** -7, atol=1e-3, what=""):
     assert np.all(err <= 0), f"{what}: worst excess {err.max():.3g} at {np.unravel_index(err.argmax(), err.shape)}"
 
 
-@pytest.mark.parametrize("rows,out_dim,in_dim,ws", [(1, 64, 64, 32 << 20), (5, 520, 136, 32 << 20),
-                                                    (64, 4096, 4096, 32 << 20), (8, 4096, 11008, 32 << 20),
-                                                    (100, 256, 512, 32 << 20)])
-def test_linear(rows, out_dim, in_dim, ws):
-    rng = np.random.default_rng(rows + out_dim)
-    k = round(np.log2(in_dim) / 2)
-    xb, wb, yb = _bits(rng, (rows, in_dim)), _bits(rng, (out_dim, in_dim), k), _bits(rng, (rows, out_dim))
-    g = PL.Gemm(ws_bytes=ws)
-    y = torch.empty((rows, out_dim), dtype=torch.bfloat16, device="cuda")
-    g.linear(_dev(xb), _dev(wb), y)
-    want = LL.linear(O.widen(xb, O.BF16), O.widen(wb, O.BF16))
-    _close(_val(y), want, what="linear")
-    y2 = _dev(yb)
-    g.linear(_dev(xb), _dev(wb), y2, accumulate=True)
-    _close(_val(y2), O.widen(yb, O.BF16) + want, what="linear accumulate")
-    g.close()
-
-
 def _pack_reference(wb):
     """The packed weight layout written out from its definition (include/baton.h):
     16-row slices, 1 KB blocks per 32 columns, lane l's 8 elements at 16 l."""
@@ -80,10 +62,14 @@ def _pack_reference(wb):
 # (rows, out_dim, in_dim, workspace bytes): one split along in_dim (many
 # outputs, or no workspace), several splits and their reduction (64 x 4096 x
 # 4096, 8 x 4096 x 11008), a partial 16-row slice and a column tail shorter
-# than 32 (17 x 1000 x 1000), every group of 16 rows.
+# than 32 (17 x 1000 x 1000), every group of 16 rows; past 64 rows, chunks of
+# 64 (128 and 256 rows at llama2-7b's shapes, a partial last chunk at 100 and
+# 200 rows, with and without splits).
 @pytest.mark.parametrize("rows,out_dim,in_dim,ws", [
     (1, 64, 64, 32 << 20), (5, 520, 136, 32 << 20), (64, 4096, 4096, 32 << 20), (8, 4096, 11008, 32 << 20),
-    (17, 1000, 1000, 32 << 20), (33, 12288, 4096, 32 << 20), (64, 4096, 4096, 0), (48, 22016, 4096, 32 << 20)])
+    (17, 1000, 1000, 32 << 20), (33, 12288, 4096, 32 << 20), (64, 4096, 4096, 0), (48, 22016, 4096, 32 << 20),
+    (128, 4096, 4096, 64 << 20), (256, 12288, 4096, 64 << 20), (100, 256, 512, 32 << 20),
+    (200, 1000, 1000, 32 << 20), (256, 4096, 11008, 0), (129, 4096, 4096, 64 << 20)])
 def test_linear_packed(rows, out_dim, in_dim, ws):
     rng = np.random.default_rng(rows + out_dim + 7)
     k = round(np.log2(in_dim) / 2)
@@ -108,7 +94,8 @@ def test_linear_packed(rows, out_dim, in_dim, ws):
 # against the oracle's norm of the oracle's product.
 @pytest.mark.parametrize("rows,out_dim,in_dim,ws", [
     (64, 4096, 4096, 32 << 20), (8, 4096, 11008, 32 << 20), (17, 1024, 1000, 32 << 20),
-    (33, 12288, 4096, 32 << 20), (64, 4096, 4096, 0)])
+    (33, 12288, 4096, 32 << 20), (64, 4096, 4096, 0), (128, 4096, 11008, 64 << 20), (256, 4096, 4096, 64 << 20),
+    (200, 1024, 1000, 0)])
 def test_linear_packed_rmsnorm(rows, out_dim, in_dim, ws):
     rng = np.random.default_rng(rows + out_dim + 13)
     k = round(np.log2(in_dim) / 2)
@@ -139,7 +126,8 @@ def test_linear_packed_rmsnorm(rows, out_dim, in_dim, ws):
 # gate/up at 64 and 8 rows, an odd number of 16-column gate slices (48 columns:
 # the last workgroup's second gate wave has none), rows not a multiple of 16;
 # and against the oracle.
-@pytest.mark.parametrize("rows,F,in_dim", [(64, 11008, 4096), (8, 11008, 4096), (17, 48, 136), (33, 1024, 1000)])
+@pytest.mark.parametrize("rows,F,in_dim", [(64, 11008, 4096), (8, 11008, 4096), (17, 48, 136), (33, 1024, 1000),
+                                            (128, 11008, 4096), (256, 1024, 1000), (150, 48, 136)])
 def test_linear_packed_silu(rows, F, in_dim):
     rng = np.random.default_rng(rows + F + 17)
     k = round(np.log2(in_dim) / 2)
@@ -205,7 +193,7 @@ def test_rope_at_token_counts():
     cache.close()
 
 
-def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128, packed=None):
+def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128):
     """GPU layers and the oracle in lockstep; returns the worst relative excess."""
     w = Workload("layer", "bf16", NL, B, m.n_q_heads, m.n_kv_heads, m.head_dim, 1, 0, seed=seed)
     dev = driver.DeviceInputs(w)
@@ -214,7 +202,7 @@ def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128, packed=None):
     wd = [M.weights_device(seed, m, l) for l in range(NL)]
     wh = [M.weights_host(seed, m, l) for l in range(NL)]
     gemm = PL.Gemm()
-    layers = PL.DecodeLayers(cache, wd, gemm, m.theta, m.eps, packed=packed)
+    layers = PL.DecodeLayers(cache, wd, gemm, m.theta, m.eps)
     step = 0
     for op in steps_ops:
         if op[0] == "embed":
@@ -250,12 +238,20 @@ def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128, packed=None):
     cache.close()
 
 
-@pytest.mark.parametrize("packed", [True, False], ids=["packed", "hipblaslt"])
-def test_layers_small_model(packed):
+def test_layers_small_model():
     m = M.ModelShape(256, 4, 2, 64, 512)
     ops = [("embed", [0, 1, 2], [9, 30, 4], [0, 1, 2]), ("step",), ("step",),
            ("evict", [1]), ("embed", [3, 1], [12, 40], [3, 4]), ("step",), ("evict", [0]), ("step",)]
-    _run_layers(m, 2, 4, ops, packed=packed)
+    _run_layers(m, 2, 4, ops)
+
+
+def test_layers_small_model_128_slots():
+    """Past 64 slots every projection takes its rows in chunks of 64."""
+    m = M.ModelShape(256, 4, 2, 64, 512)
+    lens = [(7 * b) % 50 + 1 for b in range(128)]
+    ops = [("embed", list(range(128)), lens, list(range(128))), ("step",),
+           ("evict", [3, 70, 127]), ("embed", [70, 3], [60, 2], [128, 129]), ("step",)]
+    _run_layers(m, 1, 128, ops)
 
 
 def test_layers_llama2_7b_shape():

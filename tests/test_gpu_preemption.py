@@ -166,3 +166,79 @@ def test_move_and_compact(shape):
     ]
     err = parity.run_script(shape, ops, capacity=256, split=64)
     print(f"[move] {shape}: max abs error {err:.3g}", flush=True)
+
+
+def test_batch_scaler_threshold_prefetched():
+    """The same policy with the parked query's return prefetched to device
+    memory on the scaler's second stream: the same decisions and the same
+    bits as returning it straight from pinned host memory."""
+    ops = [("embed", [0, 1, 2], [30, 95, 20], [0, 1, 2])]
+    ops += [("step", s) for s in range(6)]
+    ops += [("scale", 300, True), ("step", 6), ("step", 7), ("scale", 300, True), ("evict", [0]),
+            ("scale", 300, True), ("step", 8), ("step", 9)]
+    log = []
+    err = parity.run_script(("bf16", 2, 4, 8, 2, 128), ops, capacity=256, split=64, log=log)
+    assert log == [("scale", [1], []), ("scale", [], []), ("scale", [], [0])], log
+    print(f"[scaler prefetched] {log}: max abs error {err:.3g}", flush=True)
+
+
+def test_prefetched_return_overlaps_the_step():
+    """A parked query's return over the host link: straight from pinned host
+    memory after a step (the embed reads over the link on the step's stream)
+    against prefetched to device memory on the second stream while the step's
+    attention runs.  Both return the query's tokens bit for bit; the timings
+    (HIP events on the step's stream) are printed."""
+    from paper_2410_18701_amd.scaling import BatchScaler
+    from workload import driver
+    from workload.configs import Workload
+    NL, Bt, Hq, Hkv, D, n = 8, 128, 64, 8, 128, 2000
+    w = Workload("overlap", "bf16", NL, Bt, Hq, Hkv, D, n, 0, seed=6)
+    w.init_lens = [n] * (Bt - 1) + [n // 2]
+    cache, dev = driver.open_cache(w, capacity=n + 64)
+    scaler = BatchScaler(cache, max_cells=10 ** 9)
+    ins = [dev.decode(s, layer) for s in range(6) for layer in range(NL)]
+    E = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(s):
+        for layer in range(NL):
+            q, kn, vn = ins[s * NL + layer]
+            cache.decode_attn(layer, q, kn, vn)
+        cache.advance()
+
+    step(0)
+    torch.cuda.synchronize()
+    a, b = E(), E()
+    a.record()
+    step(1)
+    b.record()
+    torch.cuda.synchronize()
+    t_step = a.elapsed_time(b)
+    times = {}
+    for s, mode in ((2, "direct"), (4, "prefetched")):
+        L, _, lens = cache.query()
+        victim = max((b for b in range(Bt) if lens[b] > 0), key=lambda b: (lens[b], -b))
+        ks, vs = cache.extract([victim])              # the query before it leaves, to compare
+        scaler.max_cells = (sum(1 for x in lens if x > 0) - 1) * L   # room for one row fewer
+        parked = scaler.shrink()
+        assert parked == [victim], (parked, victim)   # the longest rows tie; the lowest slot goes
+        scaler.max_cells = 10 ** 9
+        torch.cuda.synchronize()
+        a, b = E(), E()
+        a.record()
+        if mode == "prefetched":
+            scaler.prefetch()
+        step(s)
+        back = scaler.grow()
+        b.record()
+        torch.cuda.synchronize()
+        times[mode] = a.elapsed_time(b)
+        assert len(back) == len(parked)
+        slot = back[0]
+        k2, v2 = cache.extract([slot])
+        assert torch.equal(k2[0].view(torch.int16), ks[0].view(torch.int16))
+        assert torch.equal(v2[0].view(torch.int16), vs[0].view(torch.int16))
+        step(s + 1)
+    mb = 2 * NL * Hkv * n * D * 2 / 1e6
+    print(f"[overlap] step {t_step:.3f} ms; step + return of {mb:.0f} MB: straight from host memory "
+          f"{times['direct']:.3f} ms, prefetched during the step {times['prefetched']:.3f} ms", flush=True)
+    cache.close()

@@ -8,6 +8,18 @@ import torch
 from paper_2410_18701_amd.scaling import BatchScaler
 
 
+class Scaler(BatchScaler):
+    """The policy with the data movement replaced by the stand-in's calls."""
+
+    def _park(self, b):
+        ks, _ = self.cache.extract([b])
+        return {"n": ks[0].shape[2], "dk": None}
+
+    def _unpark(self, p, b):
+        t = torch.zeros((1, 1, p["n"], 8))
+        self.cache.embed([b], [p["n"]], [t], [t.clone()])
+
+
 class FakeCache:
     def __init__(self, batch, lens):
         self.lens = list(lens) + [0] * (batch - len(lens))
@@ -23,6 +35,9 @@ class FakeCache:
         self.calls.append(("extract", b))
         t = torch.zeros((1, 1, self.lens[b], 8))
         return [t], [t.clone()]
+
+    def tokens(self):
+        return list(self.lens)
 
     def evict(self, slots, release=True):
         (b,) = slots
@@ -44,7 +59,7 @@ class FakeCache:
 
 def test_longest_leaves_and_returns_when_it_fits():
     c = FakeCache(4, [36, 101, 26])
-    s = BatchScaler(c, max_cells=300)
+    s = Scaler(c, max_cells=300)
     assert s.footprint() == 303
     assert s.shrink() == [1]                       # 3 x 101 -> 2 x 36
     assert c.calls == [("extract", 1), ("evict", 1)] and s.footprint() == 72
@@ -57,7 +72,7 @@ def test_longest_leaves_and_returns_when_it_fits():
 
 def test_shrink_stops_at_one_query_and_parks_in_order():
     c = FakeCache(4, [50, 60, 70, 80])
-    s = BatchScaler(c, max_cells=40)
+    s = Scaler(c, max_cells=40)
     assert s.shrink() == [3, 2, 1]                 # longest first; one query stays
     assert [p["n"] for p in s.parked] == [80, 70, 60]
     assert s.footprint() == 50
@@ -71,6 +86,6 @@ def test_ties_go_to_the_longest_row():
     # two long rows: removing any one row leaves L at 100, so every removal
     # gives 2 x 100; the tie goes to the longest row (then the lowest slot)
     c = FakeCache(4, [100, 100, 10])
-    s = BatchScaler(c, max_cells=250)
+    s = Scaler(c, max_cells=250)
     assert s.shrink() == [0]                       # 3 x 100 -> 2 x 100 = 200
     assert s.footprint() == 200
