@@ -393,11 +393,11 @@ def cpu_baseline(w, max_workers):
 
 
 def kernel_sources_sha256():
-    """Hash of the decode-attention kernel sources: counters taken on other
-    sources do not describe this kernel."""
+    """Hash of the decode attention's kernel sources and launch configuration:
+    counters taken on other sources do not describe this kernel."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("common.hpp", "decode_attn.hpp", "decode_attn_mfma.hpp", "baton.hip"):
+    for f in ("common.hpp", "decode_attn.hpp", "decode_attn_mfma.hpp", "decode_launch.hpp"):
         with open(os.path.join(ROOT, "paper_2410_18701_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
