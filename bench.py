@@ -40,8 +40,7 @@ DEFAULT_WORKLOAD = GQA_WORKLOAD
 SECONDARY_WORKLOAD = "7b-b64-L4096"
 # rocprofv3 FETCH_SIZE / WRITE_SIZE records of decode attention, by workload:
 # traffic over algorithmic bytes, valid for the kernel sources they were taken on
-TRAFFIC = {GQA_WORKLOAD: "decode_attn_70b_gqa_b128_L8192_traffic.json",
-           "7b-b64-L4096": "decode_attn_7b_b64_L4096_traffic.json"}
+TRAFFIC = {GQA_WORKLOAD: "decode_attn_70b_gqa_b128_L8192_traffic.json"}
 
 
 def parse():
