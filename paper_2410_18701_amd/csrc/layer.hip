@@ -25,10 +25,31 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 #define BATON_GEMM_KU 4                // 1 KB weight blocks per load batch of a wave
 #endif
 
-template <int MG>
+#ifndef BATON_GEMM_WIDE
+#define BATON_GEMM_WIDE 0              // past 64 rows: 1: all rows per workgroup; 0: chunks of 64 rows
+#endif
+
+template <int MG, int KU>
 void launch_skinny_mg(const baton::SkinnyArgs& a, dim3 grid, hipStream_t s) {
-  hipLaunchKernelGGL((baton::skinny_gemm_kernel<MG, BATON_GEMM_KU>), grid, dim3(baton::kWave * baton::kGemmWaves), 0,
-                     s, a);
+  hipLaunchKernelGGL((baton::skinny_gemm_kernel<MG, KU>), grid, dim3(baton::kWave * baton::kGemmWaves), 0, s, a);
+}
+
+// Row tiles, batch depth and row chunks for `rows` rows: up to 64 rows, one
+// workgroup row set of ceil(rows / 16) tiles with four 1 KB blocks per batch;
+// past it, 8 or 16 tiles with two or one block per batch, or (without
+// BATON_GEMM_WIDE) chunks of 64 rows.
+int32_t row_chunks(int32_t rows) { return rows <= 64 || BATON_GEMM_WIDE ? 1 : (rows + 63) / 64; }
+
+void launch_skinny(const baton::SkinnyArgs& a, dim3 grid, hipStream_t s) {
+  const int32_t rows = a.rows;
+  if (rows > 128 && BATON_GEMM_WIDE) return launch_skinny_mg<16, 1>(a, grid, s);
+  if (rows > 64 && BATON_GEMM_WIDE) return launch_skinny_mg<8, 2>(a, grid, s);
+  switch (std::min(4, (rows + 15) / 16)) {
+    case 1: return launch_skinny_mg<1, BATON_GEMM_KU>(a, grid, s);
+    case 2: return launch_skinny_mg<2, BATON_GEMM_KU>(a, grid, s);
+    case 3: return launch_skinny_mg<3, BATON_GEMM_KU>(a, grid, s);
+    default: return launch_skinny_mg<4, BATON_GEMM_KU>(a, grid, s);
+  }
 }
 
 }  // namespace
@@ -77,7 +98,7 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   // only as many as the workspace holds partial sums for).  Measured on the
   // llama2-7b shapes at 64 rows: the split's partial sums and second launch
   // cost more than they gain once the slices alone give two waves per SIMD.
-  const int32_t slices = (out_dim + 15) / 16, kt = (in_dim + 31) / 32, chunks = (rows + 63) / 64;
+  const int32_t slices = (out_dim + 15) / 16, kt = (in_dim + 31) / 32, chunks = row_chunks(rows);
   int32_t S = 1;
   if (slices * chunks < BATON_GEMM_MIN_SLICES)
     S = std::max(1, std::min((BATON_GEMM_TARGET_WAVES + slices * chunks - 1) / (slices * chunks), kt / 8));
@@ -99,12 +120,7 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   a.gated = 0;
   a.chunks = chunks;
   const dim3 grid((unsigned)((slices + baton::kGemmWaves - 1) / baton::kGemmWaves * chunks), (unsigned)S);
-  switch (std::min(4, (rows + 15) / 16)) {
-    case 1: launch_skinny_mg<1>(a, grid, stream); break;
-    case 2: launch_skinny_mg<2>(a, grid, stream); break;
-    case 3: launch_skinny_mg<3>(a, grid, stream); break;
-    default: launch_skinny_mg<4>(a, grid, stream); break;
-  }
+  launch_skinny(a, grid, stream);
   const int64_t n_out = (int64_t)rows * out_dim;
   if (S > 1 && gain) {
     hipLaunchKernelGGL(baton::reduce_rmsnorm_kernel, dim3(rows), dim3(baton::kRowThreads), 0, stream, a.part, a.y, S,
@@ -160,14 +176,9 @@ baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* 
   a.tc = a.kt;   // never split along k: the epilogue needs the whole sum
   a.accumulate = 0;
   a.gated = out_dim / 2;
-  a.chunks = (rows + 63) / 64;
+  a.chunks = row_chunks(rows);
   const dim3 grid((unsigned)((out_dim / 32 + 1) / 2 * a.chunks), 1);   // two gate slices per workgroup
-  switch (std::min(4, (rows + 15) / 16)) {
-    case 1: launch_skinny_mg<1>(a, grid, stream); break;
-    case 2: launch_skinny_mg<2>(a, grid, stream); break;
-    case 3: launch_skinny_mg<3>(a, grid, stream); break;
-    default: launch_skinny_mg<4>(a, grid, stream); break;
-  }
+  launch_skinny(a, grid, stream);
   return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
 }
 

@@ -113,10 +113,13 @@ __global__ void __launch_bounds__(256) silu_mul_kernel(const u32x4* __restrict__
 // y[m][n] (+)= sum_k x[m][k] w[n][k] for m < rows <= 256: a linear layer at a
 // decode step's batch.  The weight matrix (megabytes) is read once from HBM
 // and dominates the traffic; x (rows x K) is small and stays in the caches.
-// A workgroup takes 64 of the rows (grid z: chunks of 64 rows); the chunks of
-// one weight slice group are consecutive workgroups, which run at the same
-// time, so the weight bytes a second chunk reads come from the last-level
-// cache rather than HBM.
+// A workgroup takes up to 64 rows (MG <= 4 tiles of 16 per wave); past 64,
+// the grid cuts the rows into chunks of 64, the chunks of one slice group
+// consecutive workgroups, each streaming the weight again.  (Built as an
+// alternative: all rows in one workgroup, MG = 8 or 16 with shorter batches,
+// KU = 2 or 1, so that the staged rows and their registers stay within
+// bounds -- every weight block streamed once, but each read from LDS 16
+// times as often per block.)
 //
 // The weight is used in a packed form, made once per weight by
 // pack_weight_kernel: 16-row slices of w, each a run of 1 KB blocks, one per
@@ -173,20 +176,22 @@ __global__ void __launch_bounds__(256) pack_weight_kernel(const u32x4* __restric
   wp[i] = (n < N && k < K) ? w[((int64_t)n * K + k) / 8] : u32x4{0, 0, 0, 0};
 }
 
-// Activation rows staged in LDS per batch of KU blocks: 64 rows of 64 KU
-// bytes, each padded by 16 bytes so that the 16 rows one B-operand read spans
-// fall in different banks.
-template <int KU>
+// Activation rows staged in LDS per batch of KU blocks: the workgroup's rows
+// (64, or 16 MG past 64) of 64 KU bytes, each padded by 16 bytes so that the
+// 16 rows one B-operand read spans fall in different banks.
+template <int KU, int MG>
 struct GemmLds {
+  static constexpr int kRows = 16 * MG > 64 ? 16 * MG : 64;   // rows of x per workgroup
   static constexpr int kRow = 64 * KU + 16;   // bytes per staged row
-  static constexpr int kBuf = 64 * kRow;      // one batch of 64 rows
+  static constexpr int kBuf = kRows * kRow;   // one batch of the rows
   static constexpr int kPieces = 4 * KU;      // 16-byte pieces per row and batch
 };
 
 template <int MG, int KU>
 __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const SkinnyArgs a) {
-  using Lds = GemmLds<KU>;
-  constexpr int kXPer = 64 * Lds::kPieces / (kWave * kGemmWaves);   // activation pieces per thread and batch
+  using Lds = GemmLds<KU, MG>;
+  constexpr int kXPer = Lds::kRows * Lds::kPieces / (kWave * kGemmWaves);   // activation pieces per thread and batch
+  static_assert(MG * 2 * kWave * 8 <= Lds::kBuf, "gated exchange area");
   __shared__ __attribute__((aligned(16))) uint8_t xs[2][Lds::kBuf];
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -203,8 +208,8 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.wp) + ((int64_t)min(slice, (a.N + 15) / 16) * a.kt + t_begin) * 512, 0,
       n_rows > 0 ? (t_end - t_begin) * 1024 : 0, kGemmBufWord3);
-  const int32_t chunk = (int32_t)blockIdx.x % a.chunks;   // 64-row chunk of x and y
-  const int32_t xrow0 = 64 * chunk, rows = min(64, a.rows - xrow0);
+  const int32_t chunk = (int32_t)blockIdx.x % a.chunks;   // the workgroup's rows of x and y
+  const int32_t xrow0 = Lds::kRows * chunk, rows = min(Lds::kRows, a.rows - xrow0);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.x) + (int64_t)xrow0 * a.K, 0, (int32_t)(rows * row_bytes), kGemmBufWord3);
 

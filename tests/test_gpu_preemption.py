@@ -196,7 +196,7 @@ def test_prefetched_return_overlaps_the_step():
     w.init_lens = [n] * (Bt - 1) + [n // 2]
     cache, dev = driver.open_cache(w, capacity=n + 64)
     scaler = BatchScaler(cache, max_cells=10 ** 9)
-    ins = [dev.decode(s, layer) for s in range(6) for layer in range(NL)]
+    ins = [dev.decode(s, layer) for s in range(8) for layer in range(NL)]
     E = lambda: torch.cuda.Event(enable_timing=True)
 
     def step(s):
@@ -214,7 +214,9 @@ def test_prefetched_return_overlaps_the_step():
     torch.cuda.synchronize()
     t_step = a.elapsed_time(b)
     times = {}
-    for s, mode in ((2, "direct"), (4, "prefetched")):
+    # The first transfer on a new stream pays a one-time start-up (several ms
+    # on a fresh process); the cycle "warmup" is not timed.
+    for s, mode in ((2, "warmup"), (4, "direct"), (6, "prefetched")):
         L, _, lens = cache.query()
         victim = max((b for b in range(Bt) if lens[b] > 0), key=lambda b: (lens[b], -b))
         ks, vs = cache.extract([victim])              # the query before it leaves, to compare
@@ -225,7 +227,7 @@ def test_prefetched_return_overlaps_the_step():
         torch.cuda.synchronize()
         a, b = E(), E()
         a.record()
-        if mode == "prefetched":
+        if mode in ("prefetched", "warmup"):
             scaler.prefetch()
         step(s)
         back = scaler.grow()
