@@ -48,7 +48,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=4)
-    p.add_argument("--config", default=DEFAULT_WORKLOAD,
+    p.add_argument("--config", default=None,
                    choices=["b32-L2048", "7b-b64-L4096", "70b-gqa-b128-L8192", "skew-b256-L32768",
                             "skew-growth-b256-L32768"])
     p.add_argument("--layers", type=int, default=None,
@@ -59,7 +59,8 @@ def parse():
                    help="prefill the new queries inside the batch (no prefill/decode separation) "
                         "instead of embedding prefilled ones")
     p.add_argument("--model", default=None, choices=["llama2-7b"],
-                   help="run whole decode layers of this model (synthetic weights) around the attention")
+                   help="run whole decode layers of this model (synthetic weights) around the attention "
+                        f"(default workload then {SECONDARY_WORKLOAD})")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-workers", type=int, default=16,
                    help="most worker processes of the CPU oracle's all-cores run (the host's cores, at most this)")
@@ -73,7 +74,10 @@ def parse():
                    help="where the rocprofv3-derived traffic records of decode attention are (FETCH_SIZE/"
                         "WRITE_SIZE scaled by a copy of known size, as a ratio to the algorithmic bytes); a "
                         "record is used only for its workload and while the kernel sources are unchanged")
-    return p.parse_args()
+    args = p.parse_args()
+    if args.config is None:
+        args.config = SECONDARY_WORKLOAD if args.model else DEFAULT_WORKLOAD
+    return args
 
 
 def log(msg):

@@ -24,31 +24,68 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 #ifndef BATON_GEMM_KU
 #define BATON_GEMM_KU 4                // 1 KB weight blocks per load batch of a wave
 #endif
+#ifndef BATON_GEMM_MIN_WAVES_WIDE
+#define BATON_GEMM_MIN_WAVES_WIDE 768  // past 64 rows: from this many waves on, no split along k
+#endif
+#ifndef BATON_GEMM_TARGET_WAVES_WIDE
+#define BATON_GEMM_TARGET_WAVES_WIDE 1024
+#endif
 
 #ifndef BATON_GEMM_WIDE
 #define BATON_GEMM_WIDE 0              // past 64 rows: 1: all rows per workgroup; 0: chunks of 64 rows
 #endif
 
-template <int MG, int KU>
+#ifndef BATON_GEMM_NS_WIDE
+#define BATON_GEMM_NS_WIDE 2           // past 64 rows: weight slices per wave
+#endif
+#ifndef BATON_GEMM_KU_WIDE
+#define BATON_GEMM_KU_WIDE 2           // past 64 rows: 1 KB weight blocks per slice and load batch
+#endif
+#ifndef BATON_GEMM_MG_WIDE
+#define BATON_GEMM_MG_WIDE 4           // past 64 rows: row tiles of 16 per chunk
+#endif
+
+#ifndef BATON_GEMM_DEPTH
+#define BATON_GEMM_DEPTH 4             // register sets of the load pipeline, up to 64 rows
+#endif
+#ifndef BATON_GEMM_DEPTH_WIDE
+#define BATON_GEMM_DEPTH_WIDE 4        // past 64 rows
+#endif
+
+template <int MG, int KU, int NS>
 void launch_skinny_mg(const baton::SkinnyArgs& a, dim3 grid, hipStream_t s) {
-  hipLaunchKernelGGL((baton::skinny_gemm_kernel<MG, KU>), grid, dim3(baton::kWave * baton::kGemmWaves), 0, s, a);
+  constexpr int P = NS > 1 ? BATON_GEMM_DEPTH_WIDE : BATON_GEMM_DEPTH;
+  const dim3 block(baton::kWave * baton::kGemmWaves);
+  if (a.chunks == 1) hipLaunchKernelGGL((baton::skinny_gemm_kernel<MG, KU, 2, NS, P>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((baton::skinny_gemm_kernel<MG, KU, 0, NS, P>), grid, block, 0, s, a);
 }
 
-// Row tiles, batch depth and row chunks for `rows` rows: up to 64 rows, one
-// workgroup row set of ceil(rows / 16) tiles with four 1 KB blocks per batch;
-// past it, 8 or 16 tiles with two or one block per batch, or (without
-// BATON_GEMM_WIDE) chunks of 64 rows.
-int32_t row_chunks(int32_t rows) { return rows <= 64 || BATON_GEMM_WIDE ? 1 : (rows + 63) / 64; }
+// Row tiles, batch depth, slices per wave and row chunks for `rows` rows: up
+// to 64 rows, one workgroup row set of ceil(rows / 16) tiles, one slice per
+// wave and four 1 KB blocks per batch; past it, chunks of 64 rows with
+// BATON_GEMM_NS_WIDE slices per wave (or, with BATON_GEMM_WIDE, all rows in
+// one workgroup: 8 or 16 tiles with two or one block per batch).
+int32_t row_chunks(int32_t rows) {
+  return rows <= 64 || BATON_GEMM_WIDE ? 1 : (rows + 16 * BATON_GEMM_MG_WIDE - 1) / (16 * BATON_GEMM_MG_WIDE);
+}
+int32_t wave_slices(int32_t rows) { return rows <= 64 || BATON_GEMM_WIDE ? 1 : BATON_GEMM_NS_WIDE; }
+
+// Workgroups of a grid of `groups` slice groups x `chunks` row chunks: with
+// several chunks, whole sets of 8 groups (the kernel's XCD-aware dealing).
+int64_t gemm_blocks(int32_t groups, int32_t chunks) {
+  return chunks == 1 ? groups : (int64_t)(groups + 7) / 8 * 8 * chunks;
+}
 
 void launch_skinny(const baton::SkinnyArgs& a, dim3 grid, hipStream_t s) {
   const int32_t rows = a.rows;
-  if (rows > 128 && BATON_GEMM_WIDE) return launch_skinny_mg<16, 1>(a, grid, s);
-  if (rows > 64 && BATON_GEMM_WIDE) return launch_skinny_mg<8, 2>(a, grid, s);
-  switch (std::min(4, (rows + 15) / 16)) {
-    case 1: return launch_skinny_mg<1, BATON_GEMM_KU>(a, grid, s);
-    case 2: return launch_skinny_mg<2, BATON_GEMM_KU>(a, grid, s);
-    case 3: return launch_skinny_mg<3, BATON_GEMM_KU>(a, grid, s);
-    default: return launch_skinny_mg<4, BATON_GEMM_KU>(a, grid, s);
+  if (rows > 128 && BATON_GEMM_WIDE) return launch_skinny_mg<16, 1, 1>(a, grid, s);
+  if (rows > 64 && BATON_GEMM_WIDE) return launch_skinny_mg<8, 2, 1>(a, grid, s);
+  if (rows > 64) return launch_skinny_mg<BATON_GEMM_MG_WIDE, BATON_GEMM_KU_WIDE, BATON_GEMM_NS_WIDE>(a, grid, s);
+  switch ((rows + 15) / 16) {
+    case 1: return launch_skinny_mg<1, BATON_GEMM_KU, 1>(a, grid, s);
+    case 2: return launch_skinny_mg<2, BATON_GEMM_KU, 1>(a, grid, s);
+    case 3: return launch_skinny_mg<3, BATON_GEMM_KU, 1>(a, grid, s);
+    default: return launch_skinny_mg<4, BATON_GEMM_KU, 1>(a, grid, s);
   }
 }
 
@@ -92,16 +129,22 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   if (dtype != BATON_BF16) return BATON_EDTYPE;
   if (!aligned16(x) || !aligned16(wp) || !aligned16(y) || in_dim % 8 || out_dim % 8 || in_dim > (1 << 24))
     return BATON_EINVAL;
-  // 16-row weight slices, each streamed by a wave per 64-row chunk of x;
-  // with fewer than BATON_GEMM_MIN_SLICES such waves, split along k into about
-  // BATON_GEMM_TARGET_WAVES / waves ranges (at least 8 blocks of 32 each, and
-  // only as many as the workspace holds partial sums for).  Measured on the
-  // llama2-7b shapes at 64 rows: the split's partial sums and second launch
-  // cost more than they gain once the slices alone give two waves per SIMD.
+  // 16-row weight slices, streamed by waves (one slice each up to 64 rows,
+  // two past it) per 64-row chunk of x; with fewer than BATON_GEMM_MIN_SLICES
+  // such waves (BATON_GEMM_MIN_WAVES_WIDE past 64 rows), split along k into
+  // about BATON_GEMM_TARGET_WAVES(_WIDE) / waves ranges (at least 8 blocks of
+  // 32 each, and only as many as the workspace holds partial sums for).
+  // Measured on the llama2-7b shapes: at 64 rows the split's partial sums and
+  // second launch cost more than they gain once the slices alone give two
+  // waves per SIMD; past 64 rows the output and down projections (one or two
+  // workgroups per CU unsplit) gain from it, the QKV projection at 128 rows
+  // (768 waves) does not.
   const int32_t slices = (out_dim + 15) / 16, kt = (in_dim + 31) / 32, chunks = row_chunks(rows);
+  const int32_t ns = wave_slices(rows), waves = (slices + ns - 1) / ns * chunks;
+  const int32_t min_waves = chunks > 1 ? BATON_GEMM_MIN_WAVES_WIDE : BATON_GEMM_MIN_SLICES;
+  const int32_t target = chunks > 1 ? BATON_GEMM_TARGET_WAVES_WIDE : BATON_GEMM_TARGET_WAVES;
   int32_t S = 1;
-  if (slices * chunks < BATON_GEMM_MIN_SLICES)
-    S = std::max(1, std::min((BATON_GEMM_TARGET_WAVES + slices * chunks - 1) / (slices * chunks), kt / 8));
+  if (waves < min_waves) S = std::max(1, std::min((target + waves - 1) / waves, kt / 8));
   if (!ws || !aligned16(ws)) S = 1;
   while (S > 1 && (size_t)S * rows * out_dim * sizeof(float) > ws_bytes) --S;
   const int32_t tc = (kt + S - 1) / S;
@@ -119,7 +162,8 @@ baton_status linear_packed(int32_t dtype, const void* x, const void* wp, void* y
   a.accumulate = accumulate;
   a.gated = 0;
   a.chunks = chunks;
-  const dim3 grid((unsigned)((slices + baton::kGemmWaves - 1) / baton::kGemmWaves * chunks), (unsigned)S);
+  a.groups = (slices + baton::kGemmWaves * ns - 1) / (baton::kGemmWaves * ns);
+  const dim3 grid((unsigned)gemm_blocks(a.groups, chunks), (unsigned)S);
   launch_skinny(a, grid, stream);
   const int64_t n_out = (int64_t)rows * out_dim;
   if (S > 1 && gain) {
@@ -177,7 +221,9 @@ baton_status baton_linear_packed_silu(int32_t dtype, const void* x, const void* 
   a.accumulate = 0;
   a.gated = out_dim / 2;
   a.chunks = row_chunks(rows);
-  const dim3 grid((unsigned)((out_dim / 32 + 1) / 2 * a.chunks), 1);   // two gate slices per workgroup
+  const int32_t ns = wave_slices(rows);
+  a.groups = (out_dim / 32 + 2 * ns - 1) / (2 * ns);   // 2 ns gate slices per workgroup
+  const dim3 grid((unsigned)gemm_blocks(a.groups, a.chunks), 1);
   launch_skinny(a, grid, stream);
   return hipGetLastError() == hipSuccess ? BATON_OK : BATON_EHIP;
 }

@@ -114,12 +114,13 @@ __global__ void __launch_bounds__(256) silu_mul_kernel(const u32x4* __restrict__
 // decode step's batch.  The weight matrix (megabytes) is read once from HBM
 // and dominates the traffic; x (rows x K) is small and stays in the caches.
 // A workgroup takes up to 64 rows (MG <= 4 tiles of 16 per wave); past 64,
-// the grid cuts the rows into chunks of 64, the chunks of one slice group
-// consecutive workgroups, each streaming the weight again.  (Built as an
-// alternative: all rows in one workgroup, MG = 8 or 16 with shorter batches,
-// KU = 2 or 1, so that the staged rows and their registers stay within
-// bounds -- every weight block streamed once, but each read from LDS 16
-// times as often per block.)
+// the grid cuts the rows into chunks of 64 whose workgroups for one slice
+// group run on the same XCD, so that the weight is read from HBM about once
+// and from that XCD's L2 by the other chunks, and each wave takes two weight
+// slices.  (Built as an alternative: all rows in one workgroup, MG = 8 or 16
+// with shorter batches, KU = 2 or 1, so that the staged rows and their
+// registers stay within bounds -- every weight block streamed once, but each
+// read from LDS 16 times as often per block.)
 //
 // The weight is used in a packed form, made once per weight by
 // pack_weight_kernel: 16-row slices of w, each a run of 1 KB blocks, one per
@@ -145,7 +146,8 @@ struct SkinnyArgs {
   uint16_t* y;           // [rows][N]
   float* part;           // [S][rows][N] fp32, when S > 1
   int32_t rows, N, K;    // rows <= 256
-  int32_t chunks;        // ceil(rows / 64): grid x is slice groups x chunks, the chunk fastest
+  int32_t chunks;        // row chunks: ceil(rows / 64), or 1
+  int32_t groups;        // slice groups (workgroups per chunk)
   int32_t kt;            // blocks per slice, ceil(K / 32)
   int32_t tc;            // blocks per split
   int32_t accumulate;    // 1: y += x . w^T
@@ -187,41 +189,72 @@ struct GemmLds {
   static constexpr int kPieces = 4 * KU;      // 16-byte pieces per row and batch
 };
 
-template <int MG, int KU>
+// The (slice group, row chunk) of a workgroup.  One chunk: the group is the
+// workgroup index.  Several: workgroups are dealt to the GPU's eight XCDs in
+// turn (index mod 8), so the chunks of one group go to indices 8 apart -- the
+// same XCD, dispatched one after the other -- and the weight blocks they all
+// read come from that XCD's L2 after the first read; the grid is padded to
+// whole sets of 8 groups, the padding workgroups doing nothing.
+__device__ __forceinline__ bool gemm_tile(const SkinnyArgs& a, int32_t& grp, int32_t& chunk) {
+  if (a.chunks == 1) {
+    grp = (int32_t)blockIdx.x;
+    chunk = 0;
+    return true;
+  }
+  const int32_t b = (int32_t)blockIdx.x, j = b / 8;
+  chunk = j % a.chunks;
+  grp = (j / a.chunks) * 8 + b % 8;
+  return grp < a.groups;
+}
+
+// WAUX: the weight loads' cache policy, 2 (non-temporal) when each weight
+// block is read once (one row chunk), 0 when the group's other chunks read it
+// again from L2.  P: register sets of the load pipeline.  NS: weight slices
+// per wave; with NS > 1 every activation
+// operand a wave reads from LDS feeds NS matrix operations instead of one,
+// which matters past 64 rows, where the workgroup's LDS reads would otherwise
+// take as long as its matrix operations.
+template <int MG, int KU, int WAUX, int NS, int P>
 __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const SkinnyArgs a) {
   using Lds = GemmLds<KU, MG>;
   constexpr int kXPer = Lds::kRows * Lds::kPieces / (kWave * kGemmWaves);   // activation pieces per thread and batch
-  static_assert(MG * 2 * kWave * 8 <= Lds::kBuf, "gated exchange area");
+  static_assert(NS * MG * 2 * kWave * 8 <= 2 * Lds::kBuf, "gated exchange area: both staging buffers");
   __shared__ __attribute__((aligned(16))) uint8_t xs[2][Lds::kBuf];
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave, c16 = lane % 16, g4 = lane / 16;
-  // Gated: waves 0 and 1 take gate slices 2 x and 2 x + 1, waves 2 and 3 the
+  // Gated: waves 0 and 1 take gate slices 2 NS x + NS w + i, waves 2 and 3 the
   // up slices of the same output columns (F / 16 further).
-  static_assert(kGemmWaves == 4, "the gated epilogue pairs two gate and two up slices");
-  const int32_t grp = (int32_t)blockIdx.x / a.chunks;   // slice group
-  const int32_t slice = a.gated ? (w < 2 ? 2 * grp + w : a.gated / 16 + 2 * grp + w - 2) : grp * kGemmWaves + w;
-  const int32_t n0 = slice * 16;
-  const int32_t n_rows = max(0, min(16, a.N - n0));   // 0: a wave past N (loads nothing, writes nothing)
+  static_assert(kGemmWaves == 4, "the gated epilogue pairs two gate and two up waves");
+  int32_t grp, chunk;   // slice group, and the workgroup's rows of x and y
+  if (!gemm_tile(a, grp, chunk)) return;   // the whole workgroup: padding
+  const int32_t slice0 = a.gated ? (w < 2 ? 2 * NS * grp + NS * w : a.gated / 16 + 2 * NS * grp + NS * (w - 2))
+                                 : (grp * kGemmWaves + w) * NS;
   const int32_t t_begin = blockIdx.y * a.tc, t_end = min(a.kt, t_begin + a.tc);
   const uint32_t row_bytes = (uint32_t)a.K * 2u;
-  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.wp) + ((int64_t)min(slice, (a.N + 15) / 16) * a.kt + t_begin) * 512, 0,
-      n_rows > 0 ? (t_end - t_begin) * 1024 : 0, kGemmBufWord3);
-  const int32_t chunk = (int32_t)blockIdx.x % a.chunks;   // the workgroup's rows of x and y
+  __amdgpu_buffer_rsrc_t rw[NS];   // slice i: empty past N (loads zeros, writes nothing)
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    const int32_t slice = slice0 + i;
+    rw[i] = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(a.wp) + ((int64_t)min(slice, (a.N + 15) / 16) * a.kt + t_begin) * 512, 0,
+        16 * slice < a.N ? (t_end - t_begin) * 1024 : 0, kGemmBufWord3);
+  }
   const int32_t xrow0 = Lds::kRows * chunk, rows = min(Lds::kRows, a.rows - xrow0);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.x) + (int64_t)xrow0 * a.K, 0, (int32_t)(rows * row_bytes), kGemmBufWord3);
 
-  gemm_f32x4 acc[MG];
+  gemm_f32x4 acc[NS][MG];
 #pragma unroll
-  for (int j = 0; j < MG; ++j) acc[j] = gemm_f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < NS; ++i)
+#pragma unroll
+    for (int j = 0; j < MG; ++j) acc[i][j] = gemm_f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Loads of batch b (blocks t_begin + KU b ...): the workgroup's activation
   // pieces (thread tid: pieces tid + 64 kGemmWaves i -- row p / (4 KU), 16 bytes at
   // 16 (p % (4 KU)) of the batch) and this wave's weight blocks, both issued
   // unconditionally (past the end they return zeros).
-  auto issue = [&](int32_t b, u32x4 (&xr)[kXPer], u32x4 (&wr)[KU]) {
+  auto issue = [&](int32_t b, u32x4 (&xr)[kXPer], u32x4 (&wr)[NS][KU]) {
     const int32_t tb = t_begin + KU * b;
 #pragma unroll
     for (int i = 0; i < kXPer; ++i) {
@@ -232,9 +265,11 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
                                    ? (uint32_t)m * row_bytes + (uint32_t)k * 2u : kGemmOob);
     }
 #pragma unroll
-    for (int u = 0; u < KU; ++u)
-      wr[u] = gemm_load<2>(rw, tb + u < t_end ? (uint32_t)(tb + u - t_begin) * 1024u + (uint32_t)lane * 16u
-                                              : kGemmOob);   // streamed once
+    for (int u = 0; u < KU; ++u) {
+      const uint32_t off = tb + u < t_end ? (uint32_t)(tb + u - t_begin) * 1024u + (uint32_t)lane * 16u : kGemmOob;
+#pragma unroll
+      for (int i = 0; i < NS; ++i) wr[i][u] = gemm_load<WAUX>(rw[i], off);
+    }
   };
   auto stage = [&](int buf, const u32x4 (&xr)[kXPer]) {
 #pragma unroll
@@ -243,7 +278,7 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
       *reinterpret_cast<u32x4*>(&xs[buf][(p / Lds::kPieces) * Lds::kRow + (p % Lds::kPieces) * 16]) = xr[i];
     }
   };
-  auto mult = [&](int buf, const u32x4 (&wr)[KU]) {
+  auto mult = [&](int buf, const u32x4 (&wr)[NS][KU]) {
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
       u32x4 xb[MG];
@@ -252,100 +287,111 @@ __global__ void __launch_bounds__(kWave * kGemmWaves) skinny_gemm_kernel(const S
         xb[j] = *reinterpret_cast<const u32x4*>(&xs[buf][(16 * j + c16) * Lds::kRow + (32 * u + 8 * g4) * 2]);
 #pragma unroll
       for (int j = 0; j < MG; ++j)
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(gemm_bf16x8, wr[u]),
-                                                         __builtin_bit_cast(gemm_bf16x8, xb[j]), acc[j], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < NS; ++i)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(gemm_bf16x8, wr[i][u]),
+                                                              __builtin_bit_cast(gemm_bf16x8, xb[j]), acc[i][j], 0,
+                                                              0, 0);
     }
   };
-  // Four register sets: while batch b is multiplied, batches b + 1 .. b + 3
+  // P register sets: while batch b is multiplied, batches b + 1 .. b + P - 1
   // are in flight (every batch's activation loads are issued ahead of its
   // weight loads, so waiting for activations never waits for weights), and
-  // batch b + 1's activations, issued two batches earlier, go to LDS at the
-  // end of the step.  Batch b's activations are in LDS buffer b & 1.
+  // batch b + 1's activations, issued P - 2 batches earlier, go to LDS at the
+  // end of the step.  Batch b's activations are in LDS buffer b & 1.  Sets are
+  // indexed by constants only (the steps are unrolled), so they stay in
+  // registers.
   const int32_t n_batch = (t_end - t_begin + KU - 1) / KU;   // the same for the whole workgroup
   if (n_batch > 0) {
-    u32x4 x0[kXPer], x1[kXPer], x2[kXPer], x3[kXPer], w0[KU], w1[KU], w2[KU], w3[KU];
-    issue(0, x0, w0);
-    issue(1, x1, w1);
-    issue(2, x2, w2);
-    stage(0, x0);
+    u32x4 xr[P][kXPer], wr[P][NS][KU];
+#pragma unroll
+    for (int q = 0; q < P - 1; ++q) issue(q, xr[q], wr[q]);
+    stage(0, xr[0]);
     __syncthreads();
-#define BATON_GEMM_STEP(S, XN, WN, WC, XS) \
-  issue(b + S + 3, XN, WN);                \
-  __builtin_amdgcn_sched_barrier(0);       \
-  mult((b + S) & 1, WC);                   \
-  stage((b + S + 1) & 1, XS);              \
+#define BATON_GEMM_STEP(S)                                               \
+  issue(b + (S) + P - 1, xr[((S) + P - 1) % P], wr[((S) + P - 1) % P]); \
+  __builtin_amdgcn_sched_barrier(0);                                     \
+  mult((b + (S)) & 1, wr[(S) % P]);                                      \
+  stage((b + (S) + 1) & 1, xr[((S) + 1) % P]);                           \
   __syncthreads();
     // A counted loop with no exit inside its body (an exit between the steps
     // makes the compiler drain every load in flight at the loop head), then
-    // the last n_batch % 4 steps.
+    // the last n_batch % P steps.
     int32_t b = 0;
-    for (; b + 4 <= n_batch; b += 4) {
-      BATON_GEMM_STEP(0, x3, w3, w0, x1)
-      BATON_GEMM_STEP(1, x0, w0, w1, x2)
-      BATON_GEMM_STEP(2, x1, w1, w2, x3)
-      BATON_GEMM_STEP(3, x2, w2, w3, x0)
-    }
-    if (b < n_batch) {
-      BATON_GEMM_STEP(0, x3, w3, w0, x1)
-      if (b + 1 < n_batch) {
-        BATON_GEMM_STEP(1, x0, w0, w1, x2)
-        if (b + 2 < n_batch) {
-          BATON_GEMM_STEP(2, x1, w1, w2, x3)
-        }
+    for (; b + P <= n_batch; b += P) {
+#pragma unroll
+      for (int q = 0; q < P; ++q) {
+        BATON_GEMM_STEP(q)
       }
+    }
+#pragma unroll
+    for (int q = 0; q < P - 1; ++q) {
+      if (b + q >= n_batch) break;
+      BATON_GEMM_STEP(q)
     }
 #undef BATON_GEMM_STEP
   }
-  const int32_t n = n0 + 4 * g4;
   if (a.gated) {
     // The up waves hand their outputs, rounded to bf16 as the product's output
     // would be, to the gate waves through LDS (free: the loop ended on a
-    // barrier); lane l of both holds the same (row, column).  The activation
+    // barrier, after which neither staging buffer is read again); lane l of
+    // both holds the same (row, column).  The activation
     // is then silu_mul_kernel's arithmetic on the rounded values.
-    uint2* ex = reinterpret_cast<uint2*>(&xs[0][0]);   // [2 waves][MG][64 lanes]
+    uint2* ex = reinterpret_cast<uint2*>(&xs[0][0]);   // [2 waves][NS][MG][64 lanes]
     if (w >= 2) {
 #pragma unroll
-      for (int j = 0; j < MG; ++j)
-        ex[((w - 2) * MG + j) * kWave + lane] =
-            make_uint2(pack_bf16(acc[j][0], acc[j][1]), pack_bf16(acc[j][2], acc[j][3]));
+      for (int i = 0; i < NS; ++i)
+#pragma unroll
+        for (int j = 0; j < MG; ++j)
+          ex[(((w - 2) * NS + i) * MG + j) * kWave + lane] =
+              make_uint2(pack_bf16(acc[i][j][0], acc[i][j][1]), pack_bf16(acc[i][j][2], acc[i][j][3]));
     }
     __syncthreads();
-    if (w < 2 && n < a.gated) {
+    if (w < 2) {
 #pragma unroll
-      for (int j = 0; j < MG; ++j) {
-        const int32_t m = 16 * j + c16;
-        if (m >= rows) continue;
-        const uint2 u = ex[(w * MG + j) * kWave + lane];
-        const uint32_t gw[2] = {pack_bf16(acc[j][0], acc[j][1]), pack_bf16(acc[j][2], acc[j][3])};
-        const uint32_t uw[2] = {u.x, u.y};
-        uint32_t o[2];
+      for (int i = 0; i < NS; ++i) {
+        const int32_t n = 16 * (slice0 + i) + 4 * g4;
+        if (n >= a.gated) continue;
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const float g0 = bf16_lo(gw[q]), g1 = bf16_hi(gw[q]);
-          const float s0 = g0 / (1.f + expf(-g0)), s1 = g1 / (1.f + expf(-g1));
-          o[q] = pack_bf16(s0 * bf16_lo(uw[q]), s1 * bf16_hi(uw[q]));
+        for (int j = 0; j < MG; ++j) {
+          const int32_t m = 16 * j + c16;
+          if (m >= rows) continue;
+          const uint2 u = ex[((w * NS + i) * MG + j) * kWave + lane];
+          const uint32_t gw[2] = {pack_bf16(acc[i][j][0], acc[i][j][1]), pack_bf16(acc[i][j][2], acc[i][j][3])};
+          const uint32_t uw[2] = {u.x, u.y};
+          uint32_t o[2];
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const float g0 = bf16_lo(gw[q]), g1 = bf16_hi(gw[q]);
+            const float s0 = g0 / (1.f + expf(-g0)), s1 = g1 / (1.f + expf(-g1));
+            o[q] = pack_bf16(s0 * bf16_lo(uw[q]), s1 * bf16_hi(uw[q]));
+          }
+          *reinterpret_cast<uint2*>(a.y + (int64_t)(xrow0 + m) * a.gated + n) = make_uint2(o[0], o[1]);
         }
-        *reinterpret_cast<uint2*>(a.y + (int64_t)(xrow0 + m) * a.gated + n) = make_uint2(o[0], o[1]);
       }
     }
     return;
   }
-  if (n >= a.N) return;
 #pragma unroll
-  for (int j = 0; j < MG; ++j) {
-    const int32_t m = 16 * j + c16;
-    if (m >= rows) continue;
-    if (gridDim.y > 1) {
-      *reinterpret_cast<float4*>(a.part + ((int64_t)blockIdx.y * a.rows + xrow0 + m) * a.N + n) =
-          make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
-    } else {
-      uint2* yp = reinterpret_cast<uint2*>(a.y + (int64_t)(xrow0 + m) * a.N + n);
-      float v0 = acc[j][0], v1 = acc[j][1], v2 = acc[j][2], v3 = acc[j][3];
-      if (a.accumulate) {
-        const uint2 old = *yp;
-        v0 += bf16_lo(old.x); v1 += bf16_hi(old.x); v2 += bf16_lo(old.y); v3 += bf16_hi(old.y);
+  for (int i = 0; i < NS; ++i) {
+    const int32_t n = 16 * (slice0 + i) + 4 * g4;
+    if (n >= a.N) continue;
+#pragma unroll
+    for (int j = 0; j < MG; ++j) {
+      const int32_t m = 16 * j + c16;
+      if (m >= rows) continue;
+      if (gridDim.y > 1) {
+        *reinterpret_cast<float4*>(a.part + ((int64_t)blockIdx.y * a.rows + xrow0 + m) * a.N + n) =
+            make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      } else {
+        uint2* yp = reinterpret_cast<uint2*>(a.y + (int64_t)(xrow0 + m) * a.N + n);
+        float v0 = acc[i][j][0], v1 = acc[i][j][1], v2 = acc[i][j][2], v3 = acc[i][j][3];
+        if (a.accumulate) {
+          const uint2 old = *yp;
+          v0 += bf16_lo(old.x); v1 += bf16_hi(old.x); v2 += bf16_lo(old.y); v3 += bf16_hi(old.y);
+        }
+        *yp = make_uint2(pack_bf16(v0, v1), pack_bf16(v2, v3));
       }
-      *yp = make_uint2(pack_bf16(v0, v1), pack_bf16(v2, v3));
     }
   }
 }
