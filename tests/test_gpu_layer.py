@@ -10,6 +10,8 @@ last place, 2^-9 relative, plus the fp32 accumulation of a GEMM; bound used:
 intermediate in bf16 where the GPU does; a bf16 tie that the two round apart
 propagates, so the bound there is 2^-5 |ref| + 2e-2, checked at the end of
 every layer."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -37,6 +39,28 @@ def _dev(bits):
 
 def _val(t):
     return O.widen(parity.host_bits(t), O.BF16)
+
+
+# Whole-layer bound: the residual stream after a layer against the oracle's
+# layer with the same bf16 roundings, each side going on from the GPU's stream.
+LAYER_REL, LAYER_ATOL = 2.0 ** -5, 2e-2
+_LAYER_WORST = {}
+
+
+def _note_layer_margin(got, want, what):
+    """Keeps the worst whole-layer error of the test (written with the other margins)."""
+    err = np.abs(got - want)
+    frac = float((err / (LAYER_REL * np.abs(want) + LAYER_ATOL)).max())
+    rel = float((err / np.maximum(np.abs(want), 1e-3)).max())
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" (")[0]
+    old = _LAYER_WORST.get(test)
+    if old is None or frac > old["frac_of_tol"]:
+        rec = {"test": test, "what": "whole layer " + what, "dtype": "bf16", "max_abs_err": float(err.max()),
+               "max_rel_err": rel, "tol": f"2^-5 |ref| + 2e-2", "frac_of_tol": round(frac, 4)}
+        if old is not None:
+            parity.MARGINS.remove(old)
+        parity.MARGINS.append(rec)
+        _LAYER_WORST[test] = rec
 
 
 def _close(got, want, rel=2.0 ** -7, atol=1e-3, what=""):
@@ -226,7 +250,8 @@ def _run_layers(m, NL, B, steps_ops, seed=21, capacity=128):
                 layers.layer(layer, x)
                 xh = LL.decode_layer(pb, layer, xh, wh[layer], pos, m.theta, m.eps, stored=O.BF16)
                 got = _val(x)
-                _close(got[live], xh[live], rel=2.0 ** -5, atol=2e-2, what=f"step {step} layer {layer}")
+                _close(got[live], xh[live], rel=LAYER_REL, atol=LAYER_ATOL, what=f"step {step} layer {layer}")
+                _note_layer_margin(got[live], xh[live], f"{m.name if hasattr(m, 'name') else 'layer'} B={B}")
                 xh = got   # both sides go on from the GPU's stream
             cache.advance()
             pb.advance()
