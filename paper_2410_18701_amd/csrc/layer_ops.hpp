@@ -1,5 +1,5 @@
 // Kernels of a decode layer around the attention: the weight-streaming GEMM
-// of the projections at decode batch sizes (larger batches use hipBLASLt), RMS
+// of the projections at decode batch sizes (up to 256 rows), RMS
 // normalisation, the fused projection's split with rotary embedding of
 // queries and keys, and the gated activation.  bf16 storage, fp32
 // arithmetic, outputs rounded to nearest even.
