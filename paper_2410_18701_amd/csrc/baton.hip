@@ -226,16 +226,18 @@ void launch_prefill_g(const baton_cache* c, baton::PrefillArgs& a, hipStream_t s
   }
   const int32_t hq = c->d.n_kv_heads * G;
   a.n_tiles = tiles;
+  a.n_attn = tiles * hq;
   // one XCD per kv-head's readers when the kv-heads (else the query heads) split evenly
   a.unit_heads = c->d.n_kv_heads % 8 == 0 ? G : 1;
   a.xcd_map = (hq / a.unit_heads) % 8 == 0 ? 1 : 0;
   const dim3 grid((unsigned)((int64_t)tiles * hq));
+  const dim3 grid_fa((unsigned)((int64_t)tiles * (hq + c->d.n_kv_heads)));   // and the append workgroups
   int32_t longest = 0;
   for (int32_t i = 0; i < a.n_ins; ++i) longest = std::max(longest, a.plen[i]);
   if (fa && longest > BATON_PREFILL_SPLIT_LEN)
-    hipLaunchKernelGGL((baton::prefill_fa_kernel<D, G, 2>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((baton::prefill_fa_kernel<D, G, 2>), grid_fa, dim3(512), 0, s, a);
   else if (fa)
-    hipLaunchKernelGGL((baton::prefill_fa_kernel<D, G, 1>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((baton::prefill_fa_kernel<D, G, 1>), grid_fa, dim3(256), 0, s, a);
   else if (c->d.dtype == BATON_BF16)
     hipLaunchKernelGGL((baton::prefill_valu_kernel<baton::BF16Tag, D, G>), grid, dim3(baton::kWave), 0, s, a);
   else

@@ -10,9 +10,12 @@
 // of the prefilled queries are numbered consecutively, a query's longest
 // tiles (the last positions, which see the most keys) first.  Keys and values
 // come straight from k_new / v_new (the prompt is read by every tile of a
-// head, through the caches).  The first query head of each kv-head appends
-// its tile's positions.  bf16 runs on the matrix cores (prefill_fa_kernel),
-// fp32 on the vector ALUs (prefill_valu_kernel).
+// head, through the caches).  The appends to the cache run in workgroups of
+// their own, one per (tile, kv-head), after all the attention workgroups in
+// the grid of prefill_fa_kernel (bf16, on the matrix cores): short ones, they
+// fill the end of the launch instead of lengthening every attention
+// workgroup by a load and a store of its tile; in prefill_valu_kernel (fp32,
+// the vector ALUs) the first query head of each kv-head appends its tile.
 #pragma once
 
 #include "common.hpp"
@@ -35,6 +38,8 @@ struct PrefillArgs {
   int32_t n_tiles;          // tiles over all prefilled queries (per query head)
   int32_t unit_heads;       // query heads that read the same keys (G), or 1
   int32_t xcd_map;          // 1: keep each unit's workgroups on one XCD (units % 8 == 0)
+  int32_t n_attn;           // attention workgroups (n_tiles x query heads); the matrix-core
+                            // kernel's grid then has n_tiles x n_kv_heads append workgroups
   float qscale;             // scale * log2(e)
   int32_t slot[kMaxPrefill];
   int32_t plen[kMaxPrefill];
@@ -52,7 +57,7 @@ struct PrefillArgs {
 // G query heads) run on the same XCD.
 __device__ __forceinline__ void prefill_work(const PrefillArgs& a, int& hq, int32_t& ins,
                                              int32_t& tile) {
-  const int32_t nq = (int32_t)(gridDim.x / a.n_tiles);   // query heads
+  const int32_t nq = a.n_attn / a.n_tiles;   // query heads
   const int32_t g = blockIdx.x / nq, j = blockIdx.x % nq;
   if (a.xcd_map) {
     const int32_t xcd = j % 8, k = j / 8;
@@ -216,6 +221,19 @@ prefill_fa_kernel(const PrefillArgs a) {
   uint8_t* const ldsK = lds;
   uint8_t* const ldsV = lds + S * KT * ROW;
   const int tid = threadIdx.x;
+  if ((int32_t)blockIdx.x >= a.n_attn) {
+    // An append workgroup (after every attention workgroup in the grid, so
+    // that these short ones fill the end of the launch): tile g of the
+    // prefilled queries' prompt positions, kv-head h, into the ring.
+    const int32_t j = (int32_t)blockIdx.x - a.n_attn;
+    const int32_t g = j / a.n_kv_heads, h = j % a.n_kv_heads;
+    int32_t ins = 0;
+    while (ins < a.n_ins - 1 && g >= a.tile_end[ins]) ++ins;
+    const int32_t tile = a.tile_end[ins] - 1 - g, p = a.plen[ins], b = a.slot[ins];
+    const int64_t row0 = (int64_t)b * a.T + (a.T - p);
+    prefill_append<VPT>(a, b, h, p, row0, tile * TILE, min(TILE, p - tile * TILE), tid, NT);
+    return;
+  }
   const int wave = tid / kWave, lane = tid % kWave;
   const int ks = wave / 4;                             // key stream of this wave
   const int g4 = lane / 16, c16 = lane % 16;
@@ -445,7 +463,6 @@ prefill_fa_kernel(const PrefillArgs a) {
       }
     }
   }
-  if (hq % G == 0) prefill_append<VPT>(a, b, h, p, row0, wg0, min(TILE, p - wg0), tid, NT);
 }
 
 }  // namespace baton
