@@ -378,10 +378,10 @@ baton_status baton_set_split_tokens(baton_cache* cache, int32_t tokens);
  * y[r] (+)= x[r] . W^T for r < rows <= BATON_GEMM_MAX_ROWS (a linear layer at a
  * decode step's batch) on the library's weight-streaming kernel, which reads
  * the weight in a packed form made once per weight by baton_linear_pack.  The
- * weight dominates the traffic of such a product and is read once from HBM
- * (rows past 64 are taken in chunks of 64 by workgroups that run together,
- * the later chunks finding the weight in the last-level cache); the packed
- * form lets each wave stream it in contiguous 1 KB blocks.
+ * weight dominates the traffic of such a product and is read about once from
+ * HBM (rows past 64 are taken in chunks of 64 by workgroups dealt to the same
+ * XCD one after the other, the later chunks finding the weight in that XCD's
+ * L2); the packed form lets each wave stream it in contiguous 1 KB blocks.
  *
  * baton_linear_packed_bytes: bytes of the packed form of an [out_dim][in_dim]
  * weight: 2 * ceil(out_dim / 16) * 16 * ceil(in_dim / 32) * 32 (0 for sizes < 1).
