@@ -182,8 +182,11 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 //    the max and sum over the four lane groups use the gfx950 row swaps.
 // Rows are padded to 8 dwords past a multiple of 32, so that the 16 rows of a
 // transpose load spread over all banks.
+// Keys per LDS tile and key stream: 32 (a stage of 64 keys with two streams,
+// 37 KB of LDS) rather than 64, so that a workgroup's first stage arrives
+// sooner and its last stage carries fewer keys past its diagonal.
 #ifndef BATON_PREFILL_KT
-#define BATON_PREFILL_KT 64
+#define BATON_PREFILL_KT 32
 #endif
 #ifndef BATON_PREFILL_LAZY
 #define BATON_PREFILL_LAZY 8.0f
