@@ -75,6 +75,7 @@ struct baton_cache {
   bool meta_valid = false;
   int32_t n_items = 0;
   int32_t n_multi = 0;     // rows with several items
+  int32_t n_listed = 0;    // tokens in the gather list
   int dev = -1;            // the GPU holding K and V (found by the first no-allocation call)
 };
 
@@ -308,31 +309,34 @@ baton_status attn_check(const baton_cache* c, int32_t layer, const void* q, cons
 }
 
 // The step's work list: meta_kernel's arguments and the counts it will produce.
-void plan_items(baton_cache* c, baton::MetaArgs& m, int64_t& items, int64_t& multi) {
+void plan_items(baton_cache* c, baton::MetaArgs& m, int64_t& items, int64_t& multi, int64_t& listed) {
   std::memset(&m, 0, sizeof(m));
   m.L = c->L;
   m.batch = c->d.batch;
   c->step_split = c->split > 0 ? c->split : auto_split(c);
   m.split = c->step_split;
+  m.gather_max = gather_max(c);
   m.holes = hole_list(c);
-  items = multi = 0;   // as meta_kernel counts them
+  items = multi = listed = 0;   // as meta_kernel counts them
   for (int32_t b = 0; b < c->d.batch; ++b) {
     m.lens[b] = c->plen[b] > 0 ? -1 : c->lens[b];   // a row prefilled this step has no item
     m.first[b] = (uint8_t)first_hole(c, b);
-    const int64_t cnt = baton::row_items(m, b);
-    items += cnt;
-    multi += cnt > 1;
+    const baton::RowPlan p = baton::row_plan(m.holes, m.first[b], m.L, m.lens[b], m.split, m.gather_max);
+    items += p.items;
+    multi += p.items > 1;
+    listed += p.listed;
   }
 }
 
-// The workspace laid out for exactly `items` work items.
-WsLayout ws_exact(const baton_cache* c, int64_t items) {
+// The workspace laid out for exactly `items` work items and `listed` gathered tokens.
+WsLayout ws_exact(const baton_cache* c, int64_t items, int64_t listed) {
   WsLayout w;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   w.max_items = items;
   w.items_off = 0;
   w.multi_off = up(sizeof(baton::Item) * (size_t)items);
-  w.partial_off = up(w.multi_off + sizeof(int4) * (size_t)c->d.batch);
+  w.gather_off = up(w.multi_off + sizeof(int4) * (size_t)c->d.batch);
+  w.partial_off = up(w.gather_off + sizeof(int32_t) * (size_t)listed);
   w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * items * c->group *
                                    (c->d.head_dim + 4));
   return w;
@@ -343,7 +347,7 @@ WsLayout ws_exact(const baton_cache* c, int64_t items) {
 // with layout w), the attention launches, and the prefill of new queries.
 baton_status attn_run(baton_cache* c, int32_t layer, const void* q, const void* k_new, const void* v_new,
                       void* out, float scale, char* wsb, const WsLayout& w, const baton::MetaArgs* m,
-                      int64_t items, int64_t multi, hipStream_t stream) {
+                      int64_t items, int64_t multi, int64_t listed, hipStream_t stream) {
   if (c->n_done == 0) {
     const baton_status st = flush_pending(c, stream);
     if (st != BATON_OK) return st;
@@ -351,11 +355,13 @@ baton_status attn_run(baton_cache* c, int32_t layer, const void* q, const void* 
   if (m) {
     hipLaunchKernelGGL(baton::meta_kernel, dim3(1), dim3(baton::kMetaThreads), 0, stream, *m,
                        reinterpret_cast<baton::Item*>(wsb + w.items_off),
-                       reinterpret_cast<int4*>(wsb + w.multi_off));
+                       reinterpret_cast<int4*>(wsb + w.multi_off),
+                       reinterpret_cast<int32_t*>(wsb + w.gather_off));
     const baton_status st = hip_status(hipGetLastError());
     if (st != BATON_OK) return st;
     c->n_items = (int32_t)items;
     c->n_multi = (int32_t)multi;
+    c->n_listed = (int32_t)listed;
     c->meta_ws = wsb;
     c->meta_valid = true;
   }
@@ -372,6 +378,7 @@ baton_status attn_run(baton_cache* c, int32_t layer, const void* q, const void* 
   a.out = static_cast<uint32_t*>(out);
   a.items = reinterpret_cast<const baton::Item*>(wsb + w.items_off);
   a.multi = reinterpret_cast<const int4*>(wsb + w.multi_off);
+  a.gather = reinterpret_cast<const int32_t*>(wsb + w.gather_off);
   a.partial = reinterpret_cast<float*>(wsb + w.partial_off);
   a.cap = c->d.capacity;
   a.base = c->base;
@@ -757,12 +764,14 @@ baton_status baton_decode_attn(baton_cache* c, int32_t layer, const void* q, con
   char* wsb = static_cast<char*>(ws);
   if (!c->meta_valid || c->meta_ws != ws) {
     baton::MetaArgs m;
-    int64_t items, multi;
-    plan_items(c, m, items, multi);
-    if (items > w.max_items) return BATON_EINVAL;   // cannot happen: the layout bounds every row
-    return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, stream);
+    int64_t items, multi, listed;
+    plan_items(c, m, items, multi, listed);
+    // cannot happen: the layout bounds every row
+    if (items > w.max_items || (int64_t)(w.gather_off + sizeof(int32_t) * listed) > (int64_t)w.partial_off)
+      return BATON_EINVAL;
+    return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, listed, stream);
   }
-  return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, nullptr, 0, 0, stream);
+  return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, nullptr, 0, 0, 0, stream);
 }
 
 baton_status baton_decode_attn_noalloc(baton_cache* c, int32_t layer, const void* q, const void* k_new,
@@ -786,18 +795,19 @@ baton_status baton_decode_attn_noalloc(baton_cache* c, int32_t layer, const void
   if (!c->meta_valid || c->meta_ws != sp || !mine) {
     // A new work list: this step's, or the scratch last held another cache's.
     baton::MetaArgs m;
-    int64_t items, multi;
-    plan_items(c, m, items, multi);
-    const WsLayout w = ws_exact(c, items);
+    int64_t items, multi, listed;
+    plan_items(c, m, items, multi, listed);
+    const WsLayout w = ws_exact(c, items, listed);
     if (w.total > BATON_SCRATCH_BYTES) return BATON_ESCRATCH;
-    st = attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, stream);
+    st = attn_run(c, layer, q, k_new, v_new, out, scale, wsb, w, &m, items, multi, listed, stream);
     if (st == BATON_OK) {
       std::lock_guard<std::mutex> lock(g_scratch_mu);
       g_scratch_owner[c->dev] = c;
     }
     return st;
   }
-  return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, ws_exact(c, c->n_items), nullptr, 0, 0, stream);
+  return attn_run(c, layer, q, k_new, v_new, out, scale, wsb, ws_exact(c, c->n_items, c->n_listed), nullptr, 0,
+                  0, 0, stream);
 }
 
 baton_status baton_cache_flush(baton_cache* c, hipStream_t stream) {

@@ -150,10 +150,17 @@ struct HoleList {
 template <typename F>
 __host__ __device__ __forceinline__ void row_runs(const HoleList& hl, int32_t first, int64_t L,
                                                   int32_t n, F&& f) {
-  const int64_t c0 = L - n;
+  const int32_t c0 = (int32_t)(L - n);   // logical columns fit int32 (the hole list holds them so)
   int32_t t = 0;
-  for (int k = first; k < hl.n; ++k) {
-    const int32_t h0 = (int32_t)(hl.col[k][0] - c0), h1 = (int32_t)(hl.col[k][1] - c0);
+  const int kn = hl.n;
+  // the next hole is read while the current one is handled
+  int32_t a0 = first < kn ? hl.col[first][0] : 0, a1 = first < kn ? hl.col[first][1] : 0;
+  for (int k = first; k < kn; ++k) {
+    const int32_t h0 = a0 - c0, h1 = a1 - c0;
+    if (k + 1 < kn) {
+      a0 = hl.col[k + 1][0];
+      a1 = hl.col[k + 1][1];
+    }
     if (h1 <= 0 || h0 > n) continue;   // outside the row (never for a row's own holes)
     if (h0 > t) f(t, h0);
     t = h1 > t ? h1 : t;

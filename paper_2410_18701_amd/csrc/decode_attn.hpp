@@ -36,6 +36,7 @@ struct MetaArgs {
   int64_t L;
   int32_t batch;
   int32_t split;                    // tokens per item
+  int32_t gather_max;               // tokens per gathered item; 0: no gathered items
   int32_t lens[kMetaThreads];       // cached tokens (span); 0 free; -1 prefilled this step (no item)
   uint8_t first[kMetaThreads];      // index of the row's first hole
   HoleList holes;
@@ -43,98 +44,236 @@ struct MetaArgs {
 
 // One work item: the tokens [t_begin, t_end) of slot b's row (n = len_b
 // cached tokens, -1 for a free slot), and where the row's items start and how
-// many there are.
+// many there are.  A gathered item (kGathered) instead lists its tokens: the
+// token indices at [t_begin, t_end) of the workspace's gather list; with
+// kCurrent it also takes the row's current token n.
 struct Item {
   int4 span;     // (b, t_begin, t_end, n)
-  int4 row;      // (first item of the row, items of the row, this item's index, 0)
+  int4 row;      // (first item of the row, items of the row, this item's index, flags)
 };
+constexpr int32_t kGathered = 1, kCurrent = 2;
 
-// Items of a live row: each run of tokens cut into pieces of at most `split`.
-__host__ __device__ __forceinline__ int32_t row_items(const MetaArgs& a, int b) {
-  const int32_t n = a.lens[b];
-  if (n < 0) return 0;
-  if (n == 0) return 1;
-  int32_t cnt = 0;
-  row_runs(a.holes, a.first[b], a.L, n,
-           [&](int32_t t0, int32_t t1) { cnt += (t1 - t0 + a.split - 1) / a.split; });
-  return cnt;
+// floor(x / d) for 0 <= x and 64 <= d (so that x * inv stays far inside
+// int32): a float estimate from inv ~ 1/d, corrected to the exact quotient.
+// The work list divides every run by the split; an integer division by a
+// runtime value costs some 30 instructions.
+__host__ __device__ __forceinline__ int32_t div_floor(int32_t x, int32_t d, float inv) {
+  int32_t q = (int32_t)((float)x * inv);
+  int32_t r = x - q * d;
+  while (r < 0) {
+    --q;
+    r += d;
+  }
+  while (r >= d) {
+    ++q;
+    r -= d;
+  }
+  return q;
 }
 
-// Size classes of the dispatch order: an item of t tokens (split S) is in
-// class t * kSizeClasses / (S + 1); the order runs from the largest class down.
+// The split and the reciprocals its divisions use.
+struct Split {
+  int32_t s;
+  float inv, inv1;   // ~1 / s, ~1 / (s + 1)
+};
+__host__ __device__ __forceinline__ Split make_split(int32_t s) {
+  return Split{s, 1.0f / (float)s, 1.0f / (float)(s + 1)};
+}
+
+// A row's share of the work list.  Each run of consecutive tokens is cut
+// into pieces of at most `split` tokens -- unless gather_max > 0 and the run
+// is shorter than gather_max: such short runs (what a row keeps between the
+// holes of in-batch prefill steps, often a single token) are listed token by
+// token and the list is cut into gathered items of at most gather_max tokens,
+// so that a workgroup is not spent on each of them.  The current token of a
+// short last run goes with the row's last gathered item, not into the list.
+// short_piece(r) is called for each piece of r < split tokens.
+struct RowPlan {
+  int32_t items;       // work items of the row
+  int32_t full;        // pieces of exactly `split` tokens
+  int32_t listed;      // tokens in the gather list
+  int32_t gathered;    // gathered items
+  bool cur_gathered;   // the current token goes with the last gathered item
+};
+
+template <typename F>
+__host__ __device__ __forceinline__ RowPlan row_plan(const HoleList& hl, int32_t first, int64_t L, int32_t n,
+                                                     const Split& sp, int32_t gather_max, F&& short_piece) {
+  RowPlan p{0, 0, 0, 0, false};
+  if (n < 0) return p;
+  if (n == 0) {
+    p.items = 1;
+    return p;
+  }
+  row_runs(hl, first, L, n, [&](int32_t t0, int32_t t1) {
+    const int32_t len = t1 - t0;
+    if (len < gather_max) {
+      const bool last = t1 == n + 1;
+      p.listed += len - (last ? 1 : 0);
+      p.cur_gathered = p.cur_gathered || last;
+    } else {
+      const int32_t q = div_floor(len, sp.s, sp.inv), r = len - q * sp.s;
+      p.full += q;
+      p.items += q + (r > 0 ? 1 : 0);
+      if (r > 0) short_piece(r);
+    }
+  });
+  p.gathered = gather_max > 0 ? (p.listed + gather_max - 1) / gather_max : 0;
+  if (p.cur_gathered && p.gathered == 0) p.gathered = 1;
+  p.items += p.gathered;
+  return p;
+}
+
+__host__ __device__ __forceinline__ RowPlan row_plan(const HoleList& hl, int32_t first, int64_t L, int32_t n,
+                                                     int32_t split, int32_t gather_max) {
+  return row_plan(hl, first, L, n, make_split(split), gather_max, [](int32_t) {});
+}
+
+__host__ __device__ __forceinline__ int32_t row_items(const MetaArgs& a, int b) {
+  return row_plan(a.holes, a.first[b], a.L, a.lens[b], a.split, a.gather_max).items;
+}
+
+// Size classes of the dispatch order: an item of t <= split tokens is in
+// class t * kSizeClasses / (split + 1); the order runs from the largest class
+// down.
 constexpr int kSizeClasses = 64;
 
-__device__ __forceinline__ int32_t size_class(int32_t t, int32_t split) {
-  return (int32_t)((int64_t)t * kSizeClasses / (split + 1));
+__device__ __forceinline__ int32_t size_class(int32_t t, const Split& sp) {
+  return div_floor(t * kSizeClasses, sp.s + 1, sp.inv1);
+}
+
+// Class of a gathered item of t tokens (it may hold one more than `split`:
+// a full list and the current token).
+__device__ __forceinline__ int32_t gathered_class(int32_t t, const Split& sp) {
+  return size_class(min(t, sp.s), sp);
+}
+
+// Sum of x over this lane and the lanes below it in the wave.
+__device__ __forceinline__ int32_t wave_prefix_sum(int32_t x, int lane) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, kWave);
+    if (lane >= off) x += y;
+  }
+  return x;
 }
 
 // Builds the per-step work list in the workspace: one descriptor per item,
 // stored in the dispatch order -- the items from the most tokens to the fewest
 // (a counting sort over size classes; the order within a class is arbitrary
 // and affects no result) -- so that a workgroup needs a single load to start;
-// and the list of rows with several items (first item, item count, slot) for
-// combine_kernel.
+// the list of rows with several items (first item, item count, slot) for
+// combine_kernel; and the gather list of the gathered items' tokens.
 // The attention workgroups are then dealt largest first, so that the ones that
 // start last are short and the launch ends with little of the GPU idle.
+// One thread per slot.  The full pieces (`split` tokens), all of the top
+// class, take the first places of the list from one counter in LDS, one
+// atomic per wave and loop trip (a full piece of every slot, then the next
+// one of every slot: workgroups that run at the same time read many rows --
+// measured faster than each slot's pieces side by side); the shorter pieces,
+// the gathered items and a free slot's item take places through per-class
+// counters after them.  Row offsets come from wave prefix sums, and the hole
+// list is staged in LDS once, so the launch costs little more than its start.
 __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, Item* ws_items,
-                                                            int4* ws_multi) {
-  __shared__ int32_t scan[kMetaThreads];
-  __shared__ int32_t scan_multi[kMetaThreads];
-  __shared__ int32_t cursor[kSizeClasses];
-  const int b = threadIdx.x;
-  const int32_t n = b < a.batch ? a.lens[b] : 0;
-  const int32_t cnt = b < a.batch ? row_items(a, b) : 0;
+                                                            int4* ws_multi, int32_t* ws_gather) {
+  static_assert(kSizeClasses == kWave, "one lane per size class");
+  constexpr int kWaves = kMetaThreads / kWave;
+  __shared__ int32_t cursor[kSizeClasses];     // short items per class, then the class's next place
+  __shared__ int32_t full_items, full_next;
+  __shared__ int32_t wave_sum[3][kWaves];
+  __shared__ HoleList holes;   // staged once: each row walks it twice
+  const int b = threadIdx.x, lane = b % kWave, wv = b / kWave;
+  const int32_t n = b < a.batch ? a.lens[b] : -1;
+  const int32_t fh = b < a.batch ? a.first[b] : 0;
+  const int32_t gmax = a.gather_max;
+  const Split sp = make_split(a.split);
+  static_assert(2 * kMaxHoles <= kMetaThreads, "one thread per hole bound");
+  if (b < 2 * kMaxHoles) (&holes.col[0][0])[b] = (&a.holes.col[0][0])[b];
   if (b < kSizeClasses) cursor[b] = 0;
-  scan[b] = cnt;
-  scan_multi[b] = cnt > 1 ? 1 : 0;
-  __syncthreads();
-  for (int off = 1; off < kMetaThreads; off <<= 1) {
-    const int32_t add = b >= off ? scan[b - off] : 0;
-    const int32_t add_m = b >= off ? scan_multi[b - off] : 0;
-    __syncthreads();
-    scan[b] += add;
-    scan_multi[b] += add_m;
-    __syncthreads();
-  }
-  const int32_t first = scan[b] - cnt;
-  if (b < a.batch && cnt > 0) {
-    if (n == 0) {
-      atomicAdd(&cursor[0], 1);
-    } else {
-      row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
-        for (int32_t t = t0; t < t1; t += a.split)
-          atomicAdd(&cursor[size_class(min(t + a.split, t1) - t, a.split)], 1);
-      });
-    }
-    if (cnt > 1) ws_multi[scan_multi[b] - 1] = make_int4(first, cnt, b, 0);
+  if (b == 0) {
+    holes.n = a.holes.n;
+    full_items = full_next = 0;
   }
   __syncthreads();
-  if (b == 0) {   // start of each class in the order, largest class first
-    int32_t pos = 0;
-    for (int k = kSizeClasses - 1; k >= 0; --k) {
-      const int32_t c = cursor[k];
-      cursor[k] = pos;
-      pos += c;
+  // the row's plan; its short pieces counted per class on the way
+  const RowPlan p = row_plan(holes, fh, a.L, n, sp, gmax,
+                             [&](int32_t r) { atomicAdd(&cursor[size_class(r, sp)], 1); });
+  auto gathered_tokens = [&](int32_t j) {   // tokens of the row's gathered item j
+    return min(gmax, p.listed - j * gmax) + (p.cur_gathered && j == p.gathered - 1 ? 1 : 0);
+  };
+  if (n == 0) {
+    atomicAdd(&cursor[0], 1);
+  } else if (n > 0) {
+    for (int32_t j = 0; j < p.gathered; ++j) atomicAdd(&cursor[gathered_class(gathered_tokens(j), sp)], 1);
+    atomicAdd(&full_items, p.full);
+  }
+  const int32_t multi = p.items > 1 ? 1 : 0;
+  int32_t s_cnt = wave_prefix_sum(p.items, lane);
+  int32_t s_multi = wave_prefix_sum(multi, lane);
+  int32_t s_list = wave_prefix_sum(p.listed, lane);
+  if (lane == kWave - 1) {
+    wave_sum[0][wv] = s_cnt;
+    wave_sum[1][wv] = s_multi;
+    wave_sum[2][wv] = s_list;
+  }
+  __syncthreads();   // wave totals, full items and the class counts complete
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int32_t c0 = wave_sum[0][w], c1 = wave_sum[1][w], c2 = wave_sum[2][w];
+    if (w < wv) {
+      s_cnt += c0;
+      s_multi += c1;
+      s_list += c2;
     }
+  }
+  const int32_t first = s_cnt - p.items;   // the row's first item: its partial records start here
+  const int32_t list0 = s_list - p.listed;  // the row's tokens in the gather list start here
+  // Start of each class's places: after every full piece and every larger
+  // class (no other item is in a class above the full pieces').
+  if (wv == 0) {
+    const int k = kSizeClasses - 1 - lane;
+    const int32_t c = cursor[k];
+    cursor[k] = full_items + wave_prefix_sum(c, lane) - c;
   }
   __syncthreads();
   // The descriptors, each at its place in the dispatch order; an item's own
   // index (its row's first item + its rank in the row) numbers its partial
   // record.
-  if (b < a.batch && cnt > 0) {
-    if (n == 0) {
-      ws_items[atomicAdd(&cursor[0], 1)] = Item{make_int4(b, 0, 0, -1), make_int4(first, cnt, first, 0)};
-    } else {
-      int32_t c = first;
-      row_runs(a.holes, a.first[b], a.L, n, [&](int32_t t0, int32_t t1) {
-        for (int32_t t = t0; t < t1; t += a.split, ++c) {
-          const int32_t te = min(t + a.split, t1);
-          ws_items[atomicAdd(&cursor[size_class(te - t, a.split)], 1)] =
-              Item{make_int4(b, t, te, n), make_int4(first, cnt, c, 0)};
+  if (n == 0) {
+    ws_items[atomicAdd(&cursor[0], 1)] = Item{make_int4(b, 0, 0, -1), make_int4(first, 1, first, 0)};
+  } else if (n > 0) {
+    int32_t c = first, li = list0;
+    row_runs(holes, fh, a.L, n, [&](int32_t t0, int32_t t1) {
+      if (t1 - t0 < gmax) {   // a short run: listed, its current token excepted
+        const int32_t te = t1 == n + 1 ? n : t1;
+        for (int32_t t = t0; t < te; ++t) ws_gather[li++] = t;
+        return;
+      }
+      for (int32_t t = t0; t < t1; t += sp.s, ++c) {
+        const int32_t te = min(t + sp.s, t1);
+        int32_t pos;
+        if (te - t == sp.s) {
+          // the wave's lanes with a full piece take consecutive places, in lane order
+          const uint64_t act = __ballot(1);
+          const int32_t rank =
+              (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)act, 0u));
+          int32_t at = 0;
+          if (rank == 0) at = atomicAdd(&full_next, (int32_t)__popcll(act));
+          pos = __builtin_amdgcn_readfirstlane(at) + rank;
+        } else {
+          pos = atomicAdd(&cursor[size_class(te - t, sp)], 1);
         }
-      });
+        ws_items[pos] = Item{make_int4(b, t, te, n), make_int4(first, p.items, c, 0)};
+      }
+    });
+    for (int32_t j = 0; j < p.gathered; ++j, ++c) {
+      const int32_t g0 = list0 + j * gmax, g1 = min(g0 + gmax, list0 + p.listed);
+      const int32_t flags = kGathered | (p.cur_gathered && j == p.gathered - 1 ? kCurrent : 0);
+      const int32_t pos = atomicAdd(&cursor[gathered_class(gathered_tokens(j), sp)], 1);
+      ws_items[pos] = Item{make_int4(b, g0, g1, n), make_int4(first, p.items, c, flags)};
     }
   }
+  if (multi) ws_multi[s_multi - 1] = make_int4(first, p.items, b, 0);
 }
 
 struct AttnArgs {
@@ -147,6 +286,7 @@ struct AttnArgs {
   uint32_t* out;             // [batch][tw][n_q_heads][D]
   const Item* items;         // workspace: the work list in dispatch order
   const int4* multi;         // rows with several items: (first item, count, slot)
+  const int32_t* gather;     // tokens of the gathered items
   float* partial;            // [n_kv_heads][n_items][G][D + 4]
   int64_t cap, base, L;
   int32_t batch, n_kv_heads, split, n_items;
@@ -432,7 +572,31 @@ attn_kernel(const AttnArgs a) {
       vw[u] = load16(rv, off);
     }
   };
-  if (t_begin < c_end) {
+  const bool gathered = (rw.w & kGathered) != 0;
+  if (gathered) {
+    // A gathered item: its share of the listed tokens (short runs of a
+    // holey row), usually a single pass; the token index first, then the rows.
+    for (int32_t i0 = t_begin; i0 < t_end; i0 += STEP) {
+      int32_t tok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int32_t i = i0 + u * TPI + r;
+        tok[u] = i < t_end ? a.gather[i] : -1;
+      }
+      u32x4 kw[U], vw[U];
+      bool valid[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        valid[u] = tok[u] >= 0;
+        uint32_t col = start + (uint32_t)max(tok[u], 0);
+        col = col >= cap ? col - cap : col;
+        const uint32_t off = valid[u] ? col * ROWB + cl * 16u : 0x80000000u;
+        kw[u] = load16(rk, off);
+        vw[u] = load16(rv, off);
+      }
+      online_update<T, G, U, EPL, LPT>(kw, vw, valid, qf, m, l, acc);
+    }
+  } else if (t_begin < c_end) {
     u32x4 ka[U], va[U], kb[U], vb[U];
     bool la[U], lb[U];
     const int32_t n_iter = (c_end - t_begin + STEP - 1) / STEP;
@@ -451,8 +615,9 @@ attn_kernel(const AttnArgs a) {
   }
 
   // The current token: read from k_new / v_new by lane group 0, appended to
-  // the cache as column L by the wave that holds it (once per row).
-  if (n >= t_begin && n < t_end) {
+  // the cache as column L by the wave that holds it (once per row; of a
+  // gathered item, by its first wave).
+  if (gathered ? (rw.w & kCurrent) != 0 && w == 0 : n >= t_begin && n < t_end) {
     u32x4 kw[1] = {knew[cl]}, vw[1] = {vnew[cl]};
     bool valid[1] = {r == 0};
     online_update<T, G, 1, EPL, LPT>(kw, vw, valid, qf, m, l, acc);

@@ -7,7 +7,7 @@
 #pragma once
 
 // Automatic split: about kAutoItems work items (workgroups of
-// BATON_ATTN_WAVES waves) over the step's live tokens, which fills the GPU
+// BATON_ATTN_WAVES waves) over the step's cached tokens, which fills the GPU
 // several times over at the occupancy of these kernels, never fewer than 256
 // tokens per item (per-item set-up) nor more than 4096 (the tail).
 #ifndef BATON_AUTO_ITEMS
@@ -19,12 +19,14 @@
 constexpr int64_t kAutoSplitMin = BATON_AUTO_SPLIT_MIN, kAutoSplitMax = 4096, kAutoItems = BATON_AUTO_ITEMS;
 
 // Workspace layout: [items: max_items] [rows with several items: batch]
-// [dispatch order: max_items int32]
+// [gather list: max_listed int32]
 // [partials: n_kv_heads][max_items][group][head_dim + 4] fp32.
 struct WsLayout {
-  size_t items_off, multi_off, partial_off, total;
+  size_t items_off, multi_off, gather_off, partial_off, total;
   int64_t max_items;
 };
+
+int32_t gather_max(const baton_cache* c);
 
 WsLayout ws_layout(const baton_cache* c) {
   WsLayout w;
@@ -32,19 +34,25 @@ WsLayout ws_layout(const baton_cache* c) {
   // Most items a row can have: its tokens cut at every split and every hole.
   const int64_t smin = c->split > 0 ? c->split : kAutoSplitMin;
   w.max_items = B * ((c->d.capacity + smin - 1) / smin + (int64_t)c->holes.size() + 1);
+  // Most listed tokens: every run of every row short (below gather_max tokens).
+  const int64_t max_listed = B * ((int64_t)c->holes.size() + 1) * std::max(gather_max(c) - 1, 0);
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   w.items_off = 0;
   w.multi_off = up(w.items_off + sizeof(baton::Item) * w.max_items);
-  w.partial_off = up(w.multi_off + sizeof(int4) * B);
+  w.gather_off = up(w.multi_off + sizeof(int4) * B);
+  w.partial_off = up(w.gather_off + sizeof(int32_t) * max_listed);
   w.total = up(w.partial_off + sizeof(float) * (size_t)c->d.n_kv_heads * w.max_items * c->group *
                                    (c->d.head_dim + 4));
   return w;
 }
 
 int32_t auto_split(const baton_cache* c) {
+  // the tokens the step's items read: a row's span without its holes (after
+  // in-batch prefill steps mostly holes), and no row prefilled in the step
+  const baton::HoleList hl = hole_list(c);
   int64_t rows_tokens = 0;
   for (int32_t b = 0; b < c->d.batch; ++b)
-    if (c->lens[b] > 0) rows_tokens += c->lens[b] + 1;
+    if (c->lens[b] > 0 && c->plen[b] == 0) rows_tokens += row_tokens(c, b, hl) + 1;
   rows_tokens *= c->d.n_kv_heads;
   int64_t s = (rows_tokens + kAutoItems - 1) / kAutoItems;
   s = (s + 63) / 64 * 64;
@@ -87,6 +95,35 @@ bool launch_attn_d(int g, const baton::AttnArgs& a, int n_items, int n_multi, in
     case 8: launch_attn_t<T, D, 8>(a, n_items, n_multi, hkv, s); return true;
     default: return false;
   }
+}
+
+// Tokens per gathered work item: one pass of every wave of the VALU kernel's
+// workgroup; 0 where the matrix-core kernel runs (it takes no gathered items).
+template <typename T, int D, int G>
+constexpr int32_t gather_max_t() {
+  if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= BATON_MFMA_MIN_GROUP) {
+    return 0;
+  } else {
+    constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
+    return BATON_ATTN_WAVES * baton::Geometry<T, D>::kTpi * U;
+  }
+}
+
+template <typename T, int D>
+int32_t gather_max_d(int g) {
+  switch (g) {
+    case 1: return gather_max_t<T, D, 1>();
+    case 2: return gather_max_t<T, D, 2>();
+    case 4: return gather_max_t<T, D, 4>();
+    case 8: return gather_max_t<T, D, 8>();
+    default: return 0;
+  }
+}
+
+int32_t gather_max(const baton_cache* c) {
+  if (c->d.dtype == BATON_F32)
+    return c->d.head_dim == 64 ? gather_max_d<baton::F32Tag, 64>(c->group) : gather_max_d<baton::F32Tag, 128>(c->group);
+  return c->d.head_dim == 64 ? gather_max_d<baton::BF16Tag, 64>(c->group) : gather_max_d<baton::BF16Tag, 128>(c->group);
 }
 
 bool launch_attn(const baton_cache* c, const baton::AttnArgs& a, hipStream_t s) {

@@ -131,3 +131,29 @@ def test_holes_with_unscrubbed_evictions():
     for shape in (("bf16", 2, 3, 8, 2, 128), ("f32", 1, 3, 4, 4, 64)):
         err = parity.run_script(shape, ops, capacity=256, split=64)
         print(f"[inbatch stale] {shape}: max abs error {err:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("shape", [("f32", 1, 3, 4, 4, 128), ("bf16", 1, 3, 8, 8, 128), ("bf16", 1, 3, 4, 4, 64)],
+                         ids=_sid)
+def test_gathered_items(shape):
+    """A row that lives through many prefill steps keeps a short run (the
+    tokens it decoded since the last one) behind each hole; the VALU kernel
+    reads such runs as gathered items of at most one pass of a workgroup (32,
+    64 and 128 tokens for these shapes, more than the split at head_dim 64):
+    slot 0 ends with some 70 tokens in short runs behind 19 holes (several
+    gathered items, the last with the current token), slot 1 (a 10-token
+    prompt) is short runs only, slot 2 is prefilled again and again with
+    prompts of 3-40 tokens."""
+    prompts = [5, 23, 40, 7, 31, 12, 3, 37]
+    ops = [("embed", [0], [100], [0]), ("shape", [1], [10], [1]), ("step", 0)]
+    s, qid = 1, 2
+    for c in range(18):
+        if c:
+            ops.append(("evict", [2]))
+        ops += [("shape", [2], [prompts[c % len(prompts)]], [qid]), ("step", s)]
+        qid, s = qid + 1, s + 1
+        for _ in range(c % 5 + 1):
+            ops.append(("step", s))
+            s += 1
+    err = parity.run_script(shape, ops, capacity=1024, split=64)
+    print(f"[inbatch gathered] {shape}: {s} steps, max abs error {err:.3g}", flush=True)
