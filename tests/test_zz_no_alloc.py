@@ -97,6 +97,39 @@ def test_noalloc_against_oracle():
     parity.note_margin(worst, w.dtype, "no-allocation entry point")
 
 
+def test_noalloc_holey_rows():
+    """In-batch prefill steps (no prefill/decode separation) through the
+    no-allocation entry point: holey rows whose one-token runs are read as
+    gathered items (MHA bf16, the VALU kernel), and the prompts' prefill --
+    bit for bit the workspace entry point's outputs and caches."""
+    w = configs.small("bf16", 1, 6, 8, 8, 128, L0=150, n_steps=14, n_evict=1, new_hi=60, seed=64)
+    print("[noalloc] holey rows: bf16 1 layer, 6 slots, MHA 8, L0 150, a prefill every step", flush=True)
+    a, dev = driver.open_cache(w, no_pd=True)
+    b, _ = driver.open_cache(w, no_pd=True)
+    st = torch.cuda.current_stream().cuda_stream
+    for s, ev in enumerate(w.steps):
+        ins = list(zip(ev.insert, ev.insert_qids, ev.insert_lens))
+        for c in (a, b):
+            c.evict(ev.evict, release=True)
+            if ins:
+                c.shape_insert(ev.insert, ev.insert_lens)
+        T = a.step_width
+        for layer in range(w.n_layers):
+            q, kn, vn = dev.prefill_step(s, layer, T, ins) if ins else dev.decode(s, layer)
+            want = torch.zeros_like(q)
+            a.decode_attn(layer, q, kn, vn, out=want)
+            got = torch.zeros_like(q)
+            B.baton_decode_attn_noalloc(b.handle, layer, q, kn, vn, got, 0.0, st)
+            assert np.array_equal(parity.host_bits(got), parity.host_bits(want)), f"step {s} layer {layer}"
+        for c in (a, b):
+            c.advance()
+    torch.cuda.synchronize()
+    for x, y in ((a.k, b.k), (a.v, b.v)):
+        assert torch.equal(x.view(torch.int16), y.view(torch.int16)), "caches differ"
+    a.close()
+    b.close()
+
+
 def test_noalloc_refuses_a_step_beyond_the_scratch():
     """512 slots of 3000 tokens, 8 kv-heads of 8 q-heads, 64-token splits:
     about 24,000 items per kv-head, far beyond the scratch.  ESCRATCH, nothing
