@@ -185,26 +185,53 @@ attn_mfma_kernel(const AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int32_t c_end = min(t_end, n);
-  for (int32_t tt = t_begin; tt < c_end; tt += 32) {
-    u32x4 kw[Geo::kVLoads], vw[Geo::kVLoads];
+  const bool gathered = (rw.w & kGathered) != 0;
+  if (gathered) {
+    // A gathered item: its share of the listed tokens (short runs of a
+    // holey row), 32 per block; the token indices first, then the rows.
+    for (int32_t i0 = t_begin; i0 < t_end; i0 += 32) {
+      int32_t tok[Geo::kVLoads];
 #pragma unroll
-    for (int u = 0; u < Geo::kVLoads; ++u) {
-      const int32_t t = tt + u * Geo::kTpiV + lane / VPT;
-      uint32_t col = start + (uint32_t)t;
-      col = col >= cap ? col - cap : col;
-      // past the end: an offset beyond the buffer, which loads zeros
-      const uint32_t off = t < c_end ? col * ROWB + (lane % VPT) * 16u : 0x80000000u;
-      kw[u] = load16(rk, off);
-      vw[u] = load16(rv, off);
+      for (int u = 0; u < Geo::kVLoads; ++u) {
+        const int32_t i = i0 + u * Geo::kTpiV + lane / VPT;
+        tok[u] = i < t_end ? a.gather[i] : -1;
+      }
+      u32x4 kw[Geo::kVLoads], vw[Geo::kVLoads];
+#pragma unroll
+      for (int u = 0; u < Geo::kVLoads; ++u) {
+        uint32_t col = start + (uint32_t)max(tok[u], 0);
+        col = col >= cap ? col - cap : col;
+        const uint32_t off = tok[u] >= 0 ? col * ROWB + (lane % VPT) * 16u : 0x80000000u;
+        kw[u] = load16(rk, off);
+        vw[u] = load16(rv, off);
+      }
+      const int32_t nvalid = min(32, t_end - i0);
+      const uint32_t mask = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+      mfma_block<D, G>(kw, vw, qb, mask, a.qscale, ldk, lds, m, lsum, o, lane);
     }
-    const int32_t nvalid = min(32, c_end - tt);
-    const uint32_t mask = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
-    mfma_block<D, G>(kw, vw, qb, mask, a.qscale, ldk, lds, m, lsum, o, lane);
+  } else {
+    const int32_t c_end = min(t_end, n);
+    for (int32_t tt = t_begin; tt < c_end; tt += 32) {
+      u32x4 kw[Geo::kVLoads], vw[Geo::kVLoads];
+#pragma unroll
+      for (int u = 0; u < Geo::kVLoads; ++u) {
+        const int32_t t = tt + u * Geo::kTpiV + lane / VPT;
+        uint32_t col = start + (uint32_t)t;
+        col = col >= cap ? col - cap : col;
+        // past the end: an offset beyond the buffer, which loads zeros
+        const uint32_t off = t < c_end ? col * ROWB + (lane % VPT) * 16u : 0x80000000u;
+        kw[u] = load16(rk, off);
+        vw[u] = load16(rv, off);
+      }
+      const int32_t nvalid = min(32, c_end - tt);
+      const uint32_t mask = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+      mfma_block<D, G>(kw, vw, qb, mask, a.qscale, ldk, lds, m, lsum, o, lane);
+    }
   }
 
-  // The current token, a one-token tile read from k_new / v_new, and its append.
-  if (n >= t_begin && n < t_end) {
+  // The current token, a one-token tile read from k_new / v_new, and its
+  // append (of a gathered item, by its first wave).
+  if (gathered ? (rw.w & kCurrent) != 0 && w == 0 : n >= t_begin && n < t_end) {
     const u32x4* knew = reinterpret_cast<const u32x4*>(a.knew) + (bt * a.n_kv_heads + h) * VPT;
     const u32x4* vnew = reinterpret_cast<const u32x4*>(a.vnew) + (bt * a.n_kv_heads + h) * VPT;
     u32x4 kw[Geo::kVLoads], vw[Geo::kVLoads];   // token 0 of the block; the other rows zero

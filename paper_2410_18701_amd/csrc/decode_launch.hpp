@@ -97,12 +97,12 @@ bool launch_attn_d(int g, const baton::AttnArgs& a, int n_items, int n_multi, in
   }
 }
 
-// Tokens per gathered work item: one pass of every wave of the VALU kernel's
-// workgroup; 0 where the matrix-core kernel runs (it takes no gathered items).
+// Tokens per gathered work item: one pass of every wave of the workgroup
+// (32-token blocks on the matrix-core kernel).
 template <typename T, int D, int G>
 constexpr int32_t gather_max_t() {
   if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= BATON_MFMA_MIN_GROUP) {
-    return 0;
+    return BATON_ATTN_WAVES * 32;
   } else {
     constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
     return BATON_ATTN_WAVES * baton::Geometry<T, D>::kTpi * U;

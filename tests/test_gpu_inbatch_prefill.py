@@ -133,13 +133,14 @@ def test_holes_with_unscrubbed_evictions():
         print(f"[inbatch stale] {shape}: max abs error {err:.3g}", flush=True)
 
 
-@pytest.mark.parametrize("shape", [("f32", 1, 3, 4, 4, 128), ("bf16", 1, 3, 8, 8, 128), ("bf16", 1, 3, 4, 4, 64)],
-                         ids=_sid)
+@pytest.mark.parametrize("shape", [("f32", 1, 3, 4, 4, 128), ("bf16", 1, 3, 8, 8, 128), ("bf16", 1, 3, 4, 4, 64),
+                                   ("bf16", 1, 3, 16, 2, 128), ("bf16", 1, 3, 8, 4, 64)], ids=_sid)
 def test_gathered_items(shape):
     """A row that lives through many prefill steps keeps a short run (the
-    tokens it decoded since the last one) behind each hole; the VALU kernel
-    reads such runs as gathered items of at most one pass of a workgroup (32,
-    64 and 128 tokens for these shapes, more than the split at head_dim 64):
+    tokens it decoded since the last one) behind each hole; the attention
+    kernels read such runs as gathered items of at most one pass of a
+    workgroup (VALU: 32, 64 and 128 tokens for the first three shapes, more
+    than the split at head_dim 64; matrix cores, grouped heads: 64):
     slot 0 ends with some 70 tokens in short runs behind 19 holes (several
     gathered items, the last with the current token), slot 1 (a 10-token
     prompt) is short runs only, slot 2 is prefilled again and again with
