@@ -38,6 +38,7 @@ GQA_WORKLOAD = "70b-gqa-b128-L8192"   # 80 layers' padded cache exceed HBM: a re
 GQA_LAYERS, GQA_RESIDENT = 80, 24
 DEFAULT_WORKLOAD = GQA_WORKLOAD
 SECONDARY_WORKLOAD = "7b-b64-L4096"
+NO_PD_WORKLOAD = "b32-L2048"   # without P&D separation every step widens the ring by its longest prompt
 # rocprofv3 FETCH_SIZE / WRITE_SIZE records of decode attention, by workload:
 # traffic over algorithmic bytes, valid for the kernel sources they were taken on
 TRAFFIC = {GQA_WORKLOAD: "decode_attn_70b_gqa_b128_L8192_traffic.json"}
@@ -57,7 +58,7 @@ def parse():
     p.add_argument("--split", type=int, default=None, help="tokens per attention work item")
     p.add_argument("--no-pd", action="store_true",
                    help="prefill the new queries inside the batch (no prefill/decode separation) "
-                        "instead of embedding prefilled ones")
+                        f"instead of embedding prefilled ones (default workload then {NO_PD_WORKLOAD})")
     p.add_argument("--model", default=None, choices=["llama2-7b"],
                    help="run whole decode layers of this model (synthetic weights) around the attention "
                         f"(default workload then {SECONDARY_WORKLOAD})")
@@ -79,7 +80,7 @@ def parse():
                         "record is used only for its workload and while the kernel sources are unchanged")
     args = p.parse_args()
     if args.config is None:
-        args.config = SECONDARY_WORKLOAD if args.model else DEFAULT_WORKLOAD
+        args.config = SECONDARY_WORKLOAD if args.model else NO_PD_WORKLOAD if args.no_pd else DEFAULT_WORKLOAD
     return args
 
 
