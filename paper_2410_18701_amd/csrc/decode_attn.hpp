@@ -129,10 +129,6 @@ __host__ __device__ __forceinline__ RowPlan row_plan(const HoleList& hl, int32_t
   return row_plan(hl, first, L, n, make_split(split), gather_max, [](int32_t) {});
 }
 
-__host__ __device__ __forceinline__ int32_t row_items(const MetaArgs& a, int b) {
-  return row_plan(a.holes, a.first[b], a.L, a.lens[b], a.split, a.gather_max).items;
-}
-
 // Size classes of the dispatch order: an item of t <= split tokens is in
 // class t * kSizeClasses / (split + 1); the order runs from the largest class
 // down.
