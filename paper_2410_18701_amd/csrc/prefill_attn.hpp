@@ -179,7 +179,10 @@ __global__ void __launch_bounds__(kWave) prefill_valu_kernel(const PrefillArgs a
 //    columns 16*dt + 4*(m % 4), so lane i gets V[4g + e][16*dt + i].  Lane l
 //    then holds output columns 16*dt + 4*(l/16) + r of position l % 16 of the
 //    group: a position's rescale and normalisation stay in its own lanes, and
-//    the max and sum over the four lane groups use the gfx950 row swaps.
+//    the max over the four lane groups uses the gfx950 row swaps.
+//  * The weights' sum: one more operation per block, a column of ones as A
+//    and the same P^T as B, so the sum is of the bf16 weights P·V was made
+//    of, and every lane of a position holds it whole.
 // Rows are padded to 8 dwords past a multiple of 32, so that the 16 rows of a
 // transpose load spread over all banks.
 // Keys per LDS tile and key stream: 32 (a stage of 64 keys with two streams,
@@ -270,12 +273,18 @@ prefill_fa_kernel(const PrefillArgs a) {
       qb[gq][kk] = as_bf16x8(qi < p ? qin[((row0 + qi) * nq + hq) * VPT + kk * 4 + g4] ^ qsign : zero);
   }
 
+  // Running max, the sums of the weights (ol: the weights as rounded to bf16
+  // for the matrix operation, times a column of ones, on the matrix cores --
+  // the output is then normalized by exactly the weights it was made of) and
+  // the output accumulators.
   float m[QG], lsum[QG];
+  f32x4 ol[QG];
   f32x4 o[QG][DT];
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
 #pragma unroll
   for (int gq = 0; gq < QG; ++gq) {
     m[gq] = -INFINITY;
-    lsum[gq] = 0.f;
+    ol[gq] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[gq][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -364,7 +373,7 @@ prefill_fa_kernel(const PrefillArgs a) {
         if (__ballot(mx > m[gq] + kPrefillLazy)) {     // wave-uniform
           const float mn = mx > m[gq] + kPrefillLazy ? mx : m[gq];
           const float alpha = m[gq] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[gq] - mn);
-          lsum[gq] *= alpha;
+          ol[gq] *= alpha;
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) o[gq][dt] *= alpha;
           m[gq] = mn;
@@ -372,16 +381,9 @@ prefill_fa_kernel(const PrefillArgs a) {
         const float ref = m[gq] == -INFINITY ? 0.f : m[gq];
         // exponents are <= kPrefillLazy here: the hardware exp2 (results below
         // the smallest normal flush to 0, which a softmax weight may); the
-        // scale is applied in the exponent's multiply-add, the sum taken
-        // before P is rounded to bf16 for the matrix operation
-        float psum = 0.f;
+        // scale is applied in the exponent's multiply-add
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pf = __builtin_amdgcn_exp2f(fmaf(s[e], qscale, -ref));
-          pa[gq][e] = (__bf16)pf;
-          psum += pf;
-        }
-        lsum[gq] += psum;
+        for (int e = 0; e < 8; ++e) pa[gq][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[e], qscale, -ref));
       }
       const uint8_t* vblk = ldsV + kb * ROW + tr_off;
 #pragma unroll
@@ -394,6 +396,8 @@ prefill_fa_kernel(const PrefillArgs a) {
         for (int gq = 0; gq < QG; ++gq)
           o[gq][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pa[gq], o[gq][dt], 0, 0, 0);
       }
+#pragma unroll
+      for (int gq = 0; gq < QG; ++gq) ol[gq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pa[gq], ol[gq], 0, 0, 0);
     }
   };
   // The next stage's loads are in flight while the current one is computed.
@@ -412,6 +416,10 @@ prefill_fa_kernel(const PrefillArgs a) {
     compute(k0);
   }
 
+  // Every lane of a position holds its whole sum (the operation summed over
+  // the 32 keys of each block).
+#pragma unroll
+  for (int gq = 0; gq < QG; ++gq) lsum[gq] = ol[gq][0];
   if constexpr (S > 1) {
     // Key streams 1.. hand their states to stream 0 (same positions, same lane).
     __syncthreads();                                   // the stage buffers are free
@@ -454,7 +462,7 @@ prefill_fa_kernel(const PrefillArgs a) {
 #pragma unroll
     for (int gq = 0; gq < QG; ++gq) {
       const int32_t qi = i0 + 16 * gq + c16;
-      const float ls = sum_over_groups(lsum[gq]);
+      const float ls = lsum[gq];
       if (qi < p) {
         const float inv = 1.f / ls;
         uint16_t* o16 = reinterpret_cast<uint16_t*>(a.out) + ((row0 + qi) * nq + hq) * D + 4 * g4;
