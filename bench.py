@@ -693,6 +693,9 @@ def bench_decode(args, w, probes=True, no_scrub_steps=0):
         },
         "per_step_ms": quantiles([x.elapsed_time(y) for x, y in main["step"]]),
         "decode_attn_call_us": quantiles([x.elapsed_time(y) * 1e3 for x, y in main["attn"]]),
+        "timing": (f"HIP events on the launch stream; a {args.lead_bytes >> 20} MiB device copy queued just before "
+                   "the timed region, outside it, keeps the host loop ahead of the GPU" if args.lead_bytes > 0
+                   else "HIP events on the launch stream"),
     }
     if rec:
         result["roofline"]["traffic_over_algorithmic"] = rec["traffic_over_algorithmic"]
