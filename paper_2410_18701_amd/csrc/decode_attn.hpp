@@ -154,79 +154,180 @@ __device__ __forceinline__ int32_t wave_prefix_sum(int32_t x, int lane) {
   return x;
 }
 
+// Most tokens of a gathered item (the largest gather_max of the attention
+// kernels: bf16 at head_dim 64).
+constexpr int32_t kMaxGatherTokens = 128;
+
 // Builds the per-step work list in the workspace: one descriptor per item,
 // stored in the dispatch order -- the items from the most tokens to the fewest
 // (a counting sort over size classes; the order within a class is arbitrary
 // and affects no result) -- so that a workgroup needs a single load to start;
 // the list of rows with several items (first item, item count, slot) for
-// combine_kernel; and the gather list of the gathered items' tokens.
+// combine_kernel; and the gather list of the gathered items' tokens.  The
+// items are those of row_plan.
 // The attention workgroups are then dealt largest first, so that the ones that
 // start last are short and the launch ends with little of the GPU idle.
-// One thread per slot.  The full pieces (`split` tokens), all of the top
-// class, take the first places of the list from one counter in LDS, one
-// atomic per wave and loop trip (a full piece of every slot, then the next
-// one of every slot: workgroups that run at the same time read many rows --
-// measured faster than each slot's pieces side by side); the shorter pieces,
-// the gathered items and a free slot's item take places through per-class
-// counters after them.  Row offsets come from wave prefix sums, and the hole
-// list is staged in LDS once, so the launch costs little more than its start.
+// One thread per slot, and no row walks the hole list: a row's holes are a
+// suffix of the list, so the run after hole k -- from its end to the next
+// hole's start, the last one to the current column L -- is the same columns
+// for every row that holds hole k.  The first wave plans these shared runs
+// once (pieces, listed tokens, suffix sums over k, the listed columns of the
+// short ones in LDS); a row's plan is then its own first run (to its first
+// hole, or to its current token) plus the suffix sums at its first hole.  The
+// full pieces (`split` tokens, all of the top class) take the first places of
+// the list from one counter in LDS, one atomic per wave and loop trip (a full
+// piece of every slot, then the next piece of every slot: workgroups that run
+// at the same time read many rows -- measured faster than each slot's pieces
+// side by side); the shorter pieces, the gathered items and a free slot's item
+// take places through per-class counters after them.  Row offsets come from
+// wave prefix sums, and a wave per row copies the row's listed tokens of the
+// shared runs into its gather list.
 __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, Item* ws_items,
                                                             int4* ws_multi, int32_t* ws_gather) {
   static_assert(kSizeClasses == kWave, "one lane per size class");
+  static_assert(kMaxHoles == kWave, "one lane per hole");
   constexpr int kWaves = kMetaThreads / kWave;
   __shared__ int32_t cursor[kSizeClasses];     // short items per class, then the class's next place
-  __shared__ int32_t full_items, full_next;
+  __shared__ int32_t full_items, full_next, n_long, last_short;
   __shared__ int32_t wave_sum[3][kWaves];
-  __shared__ HoleList holes;   // staged once: each row walks it twice
+  __shared__ int32_t first_col[kMaxHoles + 1];    // start column of hole k (the end of a row's first run)
+  __shared__ int32_t run_lo[kMaxHoles], run_hi[kMaxHoles];    // run k: columns [lo, hi)
+  __shared__ int32_t long_run[kMaxHoles];         // the runs cut into pieces, in column order
+  __shared__ int32_t suf_pieces[kMaxHoles + 1], suf_full[kMaxHoles + 1], suf_listed[kMaxHoles + 1];
+  __shared__ int32_t sl_pos[kMaxHoles + 1];       // where run k's listed columns start in `sl`
+  __shared__ int32_t holders[kMaxHoles + 1];      // rows by first hole, then rows that hold run k
+  __shared__ int32_t sl[kMaxHoles * (kMaxGatherTokens - 1)];   // the short runs' listed columns
+  __shared__ int32_t row_dst[kMetaThreads], row_c0[kMetaThreads], row_sl0[kMetaThreads],
+      row_shared[kMetaThreads];
   const int b = threadIdx.x, lane = b % kWave, wv = b / kWave;
   const int32_t n = b < a.batch ? a.lens[b] : -1;
-  const int32_t fh = b < a.batch ? a.first[b] : 0;
+  const int32_t nh = a.holes.n;
+  const int32_t fh = b < a.batch ? min((int32_t)a.first[b], nh) : nh;
   const int32_t gmax = a.gather_max;
+  const int32_t L = (int32_t)a.L;   // logical columns fit int32 (the hole list holds them so)
   const Split sp = make_split(a.split);
-  static_assert(2 * kMaxHoles <= kMetaThreads, "one thread per hole bound");
-  if (b < 2 * kMaxHoles) (&holes.col[0][0])[b] = (&a.holes.col[0][0])[b];
   if (b < kSizeClasses) cursor[b] = 0;
-  if (b == 0) {
-    holes.n = a.holes.n;
-    full_items = full_next = 0;
+  if (b <= kMaxHoles) holders[b] = 0;
+  if (b == 0) full_items = full_next = 0;
+
+  // The shared runs, planned by the first wave: lane k for hole k.
+  if (wv == 0) {
+    const int k = lane;
+    int32_t lo = 0, hi = 0, pieces = 0, full = 0, listed = 0;
+    bool is_long = false;
+    if (k < nh) {
+      lo = a.holes.col[k][1];
+      hi = k + 1 < nh ? a.holes.col[k + 1][0] : L + 1;
+      const int32_t len = hi - lo;
+      if (len < gmax) {
+        listed = k == nh - 1 ? len - 1 : len;   // the last run holds the current token, never listed
+      } else {
+        full = div_floor(len, sp.s, sp.inv);
+        pieces = full + (len - full * sp.s > 0 ? 1 : 0);
+        is_long = true;
+      }
+      first_col[k] = a.holes.col[k][0];
+    }
+    run_lo[k] = lo;
+    run_hi[k] = hi;
+    // suffix sums over k: the total less the sum below k
+    const int32_t p_pieces = wave_prefix_sum(pieces, lane), p_full = wave_prefix_sum(full, lane),
+                  p_listed = wave_prefix_sum(listed, lane);
+    const int32_t t_pieces = __shfl(p_pieces, kWave - 1, kWave), t_full = __shfl(p_full, kWave - 1, kWave),
+                  t_listed = __shfl(p_listed, kWave - 1, kWave);
+    suf_pieces[k] = t_pieces - (p_pieces - pieces);
+    suf_full[k] = t_full - (p_full - full);
+    suf_listed[k] = t_listed - (p_listed - listed);
+    sl_pos[k] = p_listed - listed;
+    const uint64_t longs = __ballot(is_long);
+    if (is_long)
+      long_run[__builtin_amdgcn_mbcnt_hi((uint32_t)(longs >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)longs, 0u))] = k;
+    if (k == 0) {
+      suf_pieces[kMaxHoles] = suf_full[kMaxHoles] = suf_listed[kMaxHoles] = 0;
+      sl_pos[kMaxHoles] = t_listed;
+      n_long = (int32_t)__popcll(longs);
+      last_short = nh > 0 && !((longs >> (nh - 1)) & 1u);
+    }
   }
   __syncthreads();
-  // the row's plan; its short pieces counted per class on the way
-  const RowPlan p = row_plan(holes, fh, a.L, n, sp, gmax,
-                             [&](int32_t r) { atomicAdd(&cursor[size_class(r, sp)], 1); });
-  auto gathered_tokens = [&](int32_t j) {   // tokens of the row's gathered item j
-    return min(gmax, p.listed - j * gmax) + (p.cur_gathered && j == p.gathered - 1 ? 1 : 0);
-  };
+  // The short runs' listed columns, a wave per run.
+  for (int k = wv; k < nh; k += kWaves) {
+    const int32_t at = sl_pos[k], cnt = sl_pos[k + 1] - at, lo = run_lo[k];
+    for (int32_t i = lane; i < cnt; i += kWave) sl[at + i] = lo + i;
+  }
+
+  // This row's plan: its first run, then the shared runs from its first hole.
+  int32_t items = 0, full = 0, listed = 0, first_listed = 0, gathered = 0;
+  bool cur = false;
+  const int32_t c0 = L - n;
+  const int32_t f_end = fh < nh ? first_col[fh] - c0 : n + 1;   // the first run: tokens [0, f_end)
   if (n == 0) {
+    items = 1;
     atomicAdd(&cursor[0], 1);
   } else if (n > 0) {
-    for (int32_t j = 0; j < p.gathered; ++j) atomicAdd(&cursor[gathered_class(gathered_tokens(j), sp)], 1);
-    atomicAdd(&full_items, p.full);
+    if (f_end > 0) {
+      if (f_end < gmax) {
+        first_listed = fh < nh ? f_end : f_end - 1;
+        cur = fh == nh;
+      } else {
+        const int32_t q = div_floor(f_end, sp.s, sp.inv), r = f_end - q * sp.s;
+        full = q;
+        items = q + (r > 0 ? 1 : 0);
+        if (r > 0) atomicAdd(&cursor[size_class(r, sp)], 1);
+      }
+    }
+    if (fh < nh) cur = last_short != 0;
+    listed = first_listed + suf_listed[fh];
+    full += suf_full[fh];
+    items += suf_pieces[fh];
+    gathered = gmax > 0 ? (listed + gmax - 1) / gmax : 0;
+    if (cur && gathered == 0) gathered = 1;
+    items += gathered;
+    atomicAdd(&holders[fh], 1);
+    for (int32_t j = 0; j < gathered; ++j) {
+      const int32_t t = min(gmax, listed - j * gmax) + (cur && j == gathered - 1 ? 1 : 0);
+      atomicAdd(&cursor[gathered_class(t, sp)], 1);
+    }
+    atomicAdd(&full_items, full);
   }
-  const int32_t multi = p.items > 1 ? 1 : 0;
-  int32_t s_cnt = wave_prefix_sum(p.items, lane);
+  const int32_t multi = items > 1 ? 1 : 0;
+  int32_t s_cnt = wave_prefix_sum(items, lane);
   int32_t s_multi = wave_prefix_sum(multi, lane);
-  int32_t s_list = wave_prefix_sum(p.listed, lane);
+  int32_t s_list = wave_prefix_sum(listed, lane);
   if (lane == kWave - 1) {
     wave_sum[0][wv] = s_cnt;
     wave_sum[1][wv] = s_multi;
     wave_sum[2][wv] = s_list;
   }
-  __syncthreads();   // wave totals, full items and the class counts complete
+  __syncthreads();   // wave totals, row counts by first hole and the class counts complete
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
-    const int32_t c0 = wave_sum[0][w], c1 = wave_sum[1][w], c2 = wave_sum[2][w];
+    const int32_t c0w = wave_sum[0][w], c1 = wave_sum[1][w], c2 = wave_sum[2][w];
     if (w < wv) {
-      s_cnt += c0;
+      s_cnt += c0w;
       s_multi += c1;
       s_list += c2;
     }
   }
-  const int32_t first = s_cnt - p.items;   // the row's first item: its partial records start here
-  const int32_t list0 = s_list - p.listed;  // the row's tokens in the gather list start here
-  // Start of each class's places: after every full piece and every larger
-  // class (no other item is in a class above the full pieces').
+  const int32_t first = s_cnt - items;     // the row's first item: its partial records start here
+  const int32_t list0 = s_list - listed;   // the row's tokens in the gather list start here
+  row_dst[b] = list0 + first_listed;       // and those of its shared runs here
+  row_c0[b] = c0;
+  row_sl0[b] = sl_pos[fh];
+  row_shared[b] = n > 0 ? suf_listed[fh] : 0;
   if (wv == 0) {
+    // The shorter pieces of the long shared runs: one per row that holds the
+    // run.  Then the start of each class's places: after every full piece and
+    // every larger class (no other item is in a class above the full pieces').
+    const int32_t hold = wave_prefix_sum(holders[lane], lane);   // rows whose first hole is <= lane
+    if (lane < nh) {
+      const int32_t len = run_hi[lane] - run_lo[lane];
+      if (len >= gmax) {
+        const int32_t r = len - div_floor(len, sp.s, sp.inv) * sp.s;
+        if (r > 0 && hold > 0) atomicAdd(&cursor[size_class(r, sp)], hold);
+      }
+    }
+    __threadfence_block();   // the wave's adds land before its lanes read the counts
     const int k = kSizeClasses - 1 - lane;
     const int32_t c = cursor[k];
     cursor[k] = full_items + wave_prefix_sum(c, lane) - c;
@@ -238,13 +339,8 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   if (n == 0) {
     ws_items[atomicAdd(&cursor[0], 1)] = Item{make_int4(b, 0, 0, -1), make_int4(first, 1, first, 0)};
   } else if (n > 0) {
-    int32_t c = first, li = list0;
-    row_runs(holes, fh, a.L, n, [&](int32_t t0, int32_t t1) {
-      if (t1 - t0 < gmax) {   // a short run: listed, its current token excepted
-        const int32_t te = t1 == n + 1 ? n : t1;
-        for (int32_t t = t0; t < te; ++t) ws_gather[li++] = t;
-        return;
-      }
+    int32_t c = first;
+    auto pieces_of = [&](int32_t t0, int32_t t1) {   // a long run, cut at every `split` tokens
       for (int32_t t = t0; t < t1; t += sp.s, ++c) {
         const int32_t te = min(t + sp.s, t1);
         int32_t pos;
@@ -259,17 +355,42 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
         } else {
           pos = atomicAdd(&cursor[size_class(te - t, sp)], 1);
         }
-        ws_items[pos] = Item{make_int4(b, t, te, n), make_int4(first, p.items, c, 0)};
+        ws_items[pos] = Item{make_int4(b, t, te, n), make_int4(first, items, c, 0)};
       }
-    });
-    for (int32_t j = 0; j < p.gathered; ++j, ++c) {
-      const int32_t g0 = list0 + j * gmax, g1 = min(g0 + gmax, list0 + p.listed);
-      const int32_t flags = kGathered | (p.cur_gathered && j == p.gathered - 1 ? kCurrent : 0);
-      const int32_t pos = atomicAdd(&cursor[gathered_class(gathered_tokens(j), sp)], 1);
-      ws_items[pos] = Item{make_int4(b, g0, g1, n), make_int4(first, p.items, c, flags)};
+    };
+    if (f_end > 0) {
+      if (f_end < gmax) {
+        for (int32_t t = 0; t < first_listed; ++t) ws_gather[list0 + t] = t;
+      } else {
+        pieces_of(0, f_end);
+      }
+    }
+    const int32_t nl = n_long;
+    for (int32_t i = 0; i < nl; ++i) {
+      const int32_t k = long_run[i];
+      if (k >= fh) pieces_of(run_lo[k] - c0, run_hi[k] - c0);
+    }
+    for (int32_t j = 0; j < gathered; ++j, ++c) {
+      const int32_t g0 = list0 + j * gmax, g1 = min(g0 + gmax, list0 + listed);
+      const int32_t flags = kGathered | (cur && j == gathered - 1 ? kCurrent : 0);
+      const int32_t t = min(gmax, listed - j * gmax) + (cur && j == gathered - 1 ? 1 : 0);
+      const int32_t pos = atomicAdd(&cursor[gathered_class(t, sp)], 1);
+      ws_items[pos] = Item{make_int4(b, g0, g1, n), make_int4(first, items, c, flags)};
     }
   }
-  if (multi) ws_multi[s_multi - 1] = make_int4(first, p.items, b, 0);
+  if (multi) ws_multi[s_multi - 1] = make_int4(first, items, b, 0);
+  // Every row's listed tokens of the shared runs, a wave per row: wave w
+  // takes rows w, w + kWaves, ..., read one per lane, and copies those with any.
+  static_assert(kWaves * kWave == kMetaThreads, "a lane per row");
+  const int r = wv + kWaves * lane;
+  const int32_t cnt = r < a.batch ? row_shared[r] : 0;
+  const int32_t dst = row_dst[r], src = row_sl0[r], rc0 = row_c0[r];
+  for (uint64_t m = __ballot(cnt > 0); m != 0; m &= m - 1) {
+    const int j = (int)__builtin_ctzll(m);
+    const int32_t cj = __shfl(cnt, j, kWave), dj = __shfl(dst, j, kWave), sj = __shfl(src, j, kWave),
+                  oj = __shfl(rc0, j, kWave);
+    for (int32_t i = lane; i < cj; i += kWave) ws_gather[dj + i] = sl[sj + i] - oj;
+  }
 }
 
 struct AttnArgs {

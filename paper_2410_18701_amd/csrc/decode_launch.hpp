@@ -101,12 +101,12 @@ bool launch_attn_d(int g, const baton::AttnArgs& a, int n_items, int n_multi, in
 // (32-token blocks on the matrix-core kernel).
 template <typename T, int D, int G>
 constexpr int32_t gather_max_t() {
-  if constexpr (BATON_GQA_MFMA && T::kBytes == 2 && G >= BATON_MFMA_MIN_GROUP) {
-    return BATON_ATTN_WAVES * 32;
-  } else {
-    constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
-    return BATON_ATTN_WAVES * baton::Geometry<T, D>::kTpi * U;
-  }
+  constexpr int U = G <= 2 ? BATON_ATTN_U_SMALL_G : BATON_ATTN_U_LARGE_G;
+  constexpr int32_t g = BATON_GQA_MFMA && T::kBytes == 2 && G >= BATON_MFMA_MIN_GROUP
+                            ? BATON_ATTN_WAVES * 32
+                            : BATON_ATTN_WAVES * baton::Geometry<T, D>::kTpi * U;
+  static_assert(g <= baton::kMaxGatherTokens, "meta_kernel stages at most kMaxGatherTokens - 1 listed tokens a run");
+  return g;
 }
 
 template <typename T, int D>
