@@ -211,7 +211,13 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   if (b == 0) full_items = full_next = 0;
 
   // The shared runs, planned by the first wave: lane k for hole k.
-  if (wv == 0) {
+  if (wv == 0 && nh == 0) {   // none: every row's plan is its own single run
+    suf_pieces[lane] = suf_full[lane] = suf_listed[lane] = sl_pos[lane] = 0;
+    if (lane == 0) {
+      suf_pieces[kMaxHoles] = suf_full[kMaxHoles] = suf_listed[kMaxHoles] = sl_pos[kMaxHoles] = 0;
+      n_long = last_short = 0;
+    }
+  } else if (wv == 0) {
     const int k = lane;
     int32_t lo = 0, hi = 0, pieces = 0, full = 0, listed = 0;
     bool is_long = false;
@@ -246,7 +252,7 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
       suf_pieces[kMaxHoles] = suf_full[kMaxHoles] = suf_listed[kMaxHoles] = 0;
       sl_pos[kMaxHoles] = t_listed;
       n_long = (int32_t)__popcll(longs);
-      last_short = nh > 0 && !((longs >> (nh - 1)) & 1u);
+      last_short = !((longs >> (nh - 1)) & 1u);
     }
   }
   __syncthreads();
@@ -283,7 +289,7 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
     gathered = gmax > 0 ? (listed + gmax - 1) / gmax : 0;
     if (cur && gathered == 0) gathered = 1;
     items += gathered;
-    atomicAdd(&holders[fh], 1);
+    if (fh < nh) atomicAdd(&holders[fh], 1);   // a row past the last hole holds no shared run
     for (int32_t j = 0; j < gathered; ++j) {
       const int32_t t = min(gmax, listed - j * gmax) + (cur && j == gathered - 1 ? 1 : 0);
       atomicAdd(&cursor[gathered_class(t, sp)], 1);
@@ -311,23 +317,28 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   }
   const int32_t first = s_cnt - items;     // the row's first item: its partial records start here
   const int32_t list0 = s_list - listed;   // the row's tokens in the gather list start here
-  row_dst[b] = list0 + first_listed;       // and those of its shared runs here
-  row_c0[b] = c0;
-  row_sl0[b] = sl_pos[fh];
-  row_shared[b] = n > 0 ? suf_listed[fh] : 0;
+  const bool any_shared = sl_pos[kMaxHoles] > 0;   // listed tokens in the shared runs
+  if (any_shared) {
+    row_dst[b] = list0 + first_listed;       // and those of its shared runs here
+    row_c0[b] = c0;
+    row_sl0[b] = sl_pos[fh];
+    row_shared[b] = n > 0 ? suf_listed[fh] : 0;
+  }
   if (wv == 0) {
     // The shorter pieces of the long shared runs: one per row that holds the
     // run.  Then the start of each class's places: after every full piece and
     // every larger class (no other item is in a class above the full pieces').
-    const int32_t hold = wave_prefix_sum(holders[lane], lane);   // rows whose first hole is <= lane
-    if (lane < nh) {
-      const int32_t len = run_hi[lane] - run_lo[lane];
-      if (len >= gmax) {
-        const int32_t r = len - div_floor(len, sp.s, sp.inv) * sp.s;
-        if (r > 0 && hold > 0) atomicAdd(&cursor[size_class(r, sp)], hold);
+    if (nh > 0) {
+      const int32_t hold = wave_prefix_sum(holders[lane], lane);   // rows whose first hole is <= lane
+      if (lane < nh) {
+        const int32_t len = run_hi[lane] - run_lo[lane];
+        if (len >= gmax) {
+          const int32_t r = len - div_floor(len, sp.s, sp.inv) * sp.s;
+          if (r > 0 && hold > 0) atomicAdd(&cursor[size_class(r, sp)], hold);
+        }
       }
+      __threadfence_block();   // the wave's adds land before its lanes read the counts
     }
-    __threadfence_block();   // the wave's adds land before its lanes read the counts
     const int k = kSizeClasses - 1 - lane;
     const int32_t c = cursor[k];
     cursor[k] = full_items + wave_prefix_sum(c, lane) - c;
@@ -382,6 +393,7 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   // Every row's listed tokens of the shared runs, a wave per row: wave w
   // takes rows w, w + kWaves, ..., read one per lane, and copies those with any.
   static_assert(kWaves * kWave == kMetaThreads, "a lane per row");
+  if (!any_shared) return;
   const int r = wv + kWaves * lane;
   const int32_t cnt = r < a.batch ? row_shared[r] : 0;
   const int32_t dst = row_dst[r], src = row_sl0[r], rc0 = row_c0[r];
