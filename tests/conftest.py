@@ -12,7 +12,8 @@ def pytest_configure(config):
 
 def pytest_sessionfinish(session, exitstatus):
     """Keep the parity runs' largest attention errors (and their fraction of
-    the tolerance) in gpurun_out/parity_margins.json when any ran."""
+    the tolerance) as JSON when any ran: at BATON_MARGINS_OUT, else as
+    parity_margins.json in the results folder the GPU runs hand back."""
     parity = sys.modules.get("tests.parity")
     if parity is not None:
         parity.write_margins(os.environ.get("BATON_MARGINS_OUT",
