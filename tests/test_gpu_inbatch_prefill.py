@@ -158,3 +158,35 @@ def test_gathered_items(shape):
             s += 1
     err = parity.run_script(shape, ops, capacity=1024, split=64)
     print(f"[inbatch gathered] {shape}: {s} steps, max abs error {err:.3g}", flush=True)
+
+
+@pytest.mark.parametrize("shape", [("bf16", 1, 4, 8, 2, 128), ("bf16", 1, 4, 4, 4, 64), ("f32", 1, 4, 4, 4, 128)],
+                         ids=_sid)
+def test_many_holes_rows_of_different_ages(shape):
+    """Sixty holes held by rows of different ages: slot 0 lives through every
+    prefill step, slot 1 is prefilled again and again, slot 2 is embedded
+    (prefilled elsewhere) after 20 of them and slot 3 prefilled in the batch
+    after 40, so each row holds its own suffix of the hole list.  The run
+    behind a hole is the prefill step's one token and up to two decode steps,
+    or (twice) 66 decode steps: listed runs, runs cut into a piece of the
+    split (64) and a remainder, and back-to-back short runs in one work list
+    (66 tokens are listed at head_dim 64, whose gathered items hold 128)."""
+    prompts = [5, 23, 40, 7, 31, 12, 3, 37, 2, 18]
+    ops = [("embed", [0], [150], [0]), ("step", 0)]
+    s, qid = 1, 1
+    for c in range(60):
+        if c:
+            ops.append(("evict", [1]))
+        if c == 20:
+            ops.append(("embed", [2], [90], [qid]))
+            qid += 1
+        slots, lens = [1], [prompts[c % len(prompts)]]
+        if c == 40:
+            slots, lens = [1, 3], [lens[0], 25]
+        ops += [("shape", slots, lens, list(range(qid, qid + len(slots)))), ("step", s)]
+        qid, s = qid + len(slots), s + 1
+        for _ in range(66 if c in (10, 35) else c % 3):
+            ops.append(("step", s))
+            s += 1
+    err = parity.run_script(shape, ops, capacity=2048, split=64)
+    print(f"[inbatch many holes] {shape}: {s} steps, max abs error {err:.3g}", flush=True)
