@@ -167,10 +167,11 @@ constexpr int32_t kMaxGatherTokens = 128;
 // items are those of row_plan.
 // The attention workgroups are then dealt largest first, so that the ones that
 // start last are short and the launch ends with little of the GPU idle.
-// One thread per slot, and no row walks the hole list: a row's holes are a
-// suffix of the list, so the run after hole k -- from its end to the next
-// hole's start, the last one to the current column L -- is the same columns
-// for every row that holds hole k.  The first wave plans these shared runs
+// One thread per slot, and no row walks the hole list: the holes a row holds
+// are the list from its first hole on (the host gives each row a first hole
+// that ends after the row's first column), so the run after hole k -- from
+// its end to the next hole's start, the last one to the current column L --
+// is the same columns for every row that holds hole k.  The first wave plans these shared runs
 // once (pieces, listed tokens, suffix sums over k, the listed columns of the
 // short ones in LDS); a row's plan is then its own first run (to its first
 // hole, or to its current token) plus the suffix sums at its first hole.  The
@@ -190,12 +191,12 @@ __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, It
   __shared__ int32_t cursor[kSizeClasses];     // short items per class, then the class's next place
   __shared__ int32_t full_items, full_next, n_long, last_short;
   __shared__ int32_t wave_sum[3][kWaves];
-  __shared__ int32_t first_col[kMaxHoles + 1];    // start column of hole k (the end of a row's first run)
+  __shared__ int32_t first_col[kMaxHoles];        // start column of hole k (the end of a row's first run)
   __shared__ int32_t run_lo[kMaxHoles], run_hi[kMaxHoles];    // run k: columns [lo, hi)
   __shared__ int32_t long_run[kMaxHoles];         // the runs cut into pieces, in column order
   __shared__ int32_t suf_pieces[kMaxHoles + 1], suf_full[kMaxHoles + 1], suf_listed[kMaxHoles + 1];
   __shared__ int32_t sl_pos[kMaxHoles + 1];       // where run k's listed columns start in `sl`
-  __shared__ int32_t holders[kMaxHoles + 1];      // rows by first hole, then rows that hold run k
+  __shared__ int32_t holders[kMaxHoles + 1];      // live rows by first hole (run k's: those up to k)
   __shared__ int32_t sl[kMaxHoles * (kMaxGatherTokens - 1)];   // the short runs' listed columns
   __shared__ int32_t row_dst[kMetaThreads], row_c0[kMetaThreads], row_sl0[kMetaThreads],
       row_shared[kMetaThreads];
