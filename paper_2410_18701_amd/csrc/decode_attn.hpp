@@ -22,6 +22,8 @@
 // zeros.  Exponentials are base 2 with scale*log2(e) folded into q.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 #ifndef BATON_ATTN_NT
@@ -171,18 +173,18 @@ constexpr int32_t kMaxGatherTokens = 128;
 // are the list from its first hole on (the host gives each row a first hole
 // that ends after the row's first column), so the run after hole k -- from
 // its end to the next hole's start, the last one to the current column L --
-// is the same columns for every row that holds hole k.  The first wave plans these shared runs
-// once (pieces, listed tokens, suffix sums over k, the listed columns of the
-// short ones in LDS); a row's plan is then its own first run (to its first
-// hole, or to its current token) plus the suffix sums at its first hole.  The
-// full pieces (`split` tokens, all of the top class) take the first places of
-// the list from one counter in LDS, one atomic per wave and loop trip (a full
-// piece of every slot, then the next piece of every slot: workgroups that run
-// at the same time read many rows -- measured faster than each slot's pieces
-// side by side); the shorter pieces, the gathered items and a free slot's item
-// take places through per-class counters after them.  Row offsets come from
-// wave prefix sums, and a wave per row copies the row's listed tokens of the
-// shared runs into its gather list.
+// is the same columns for every row that holds hole k.  The first wave plans
+// these shared runs once (pieces, listed tokens, suffix sums over k, the
+// listed columns of the short ones in LDS); a row's plan is then its own first
+// run (to its first hole, or to its current token) plus the suffix sums at its
+// first hole.  The full pieces (`split` tokens, all of the top class) take
+// the first places of the list from one counter in LDS, one atomic per wave
+// and loop trip (a full piece of every slot, then the next piece of every
+// slot: workgroups that run at the same time read many rows -- measured faster
+// than each slot's pieces side by side); the shorter pieces, the gathered
+// items and a free slot's item take places through per-class counters after
+// them.  Row offsets come from wave prefix sums, and a wave per row copies the
+// row's listed tokens of the shared runs into its gather list.
 __global__ void __launch_bounds__(kMetaThreads) meta_kernel(const MetaArgs a, Item* ws_items,
                                                             int4* ws_multi, int32_t* ws_gather) {
   static_assert(kSizeClasses == kWave, "one lane per size class");
@@ -486,16 +488,59 @@ __device__ __forceinline__ void online_update(const u32x4 (&kw)[U], const u32x4 
 }
 
 // Log-sum-exp merge of a row's partial records (m, l, acc[D]) for one query
-// head: lane i reads record i's m (64 at a time) and the wave reduces the max;
-// then every lane accumulates its D/64 elements over the records, eight
-// records' loads in flight at a time, with the weights broadcast from the
-// lanes that computed them.
+// head.  Up to eight records (most rows): every lane loads all of them at
+// once (two, four or eight records' worth) -- each record's m and l, and its
+// own D/64 elements -- and merges them in record order after that one round
+// trip.  More: lane i reads record i's m
+// (64 at a time) and the wave reduces the max; then every lane accumulates its
+// elements over the records, eight records' loads in flight at a time, with
+// the weights broadcast from the lanes that computed them.
 template <typename T, int D, int G>
 __device__ __forceinline__ void merge_row(const float* base, int32_t count, uint32_t* outw,
                                           int lane) {
   constexpr int REC = D + 4;
   constexpr int PER = D / kWave;   // elements per lane (1 or 2)
   constexpr int64_t STRIDE = (int64_t)G * REC;
+  auto store = [&](const float (&o)[PER], float inv) {
+    if constexpr (T::kBytes == 4) {
+#pragma unroll
+      for (int e = 0; e < PER; ++e) outw[lane * PER + e] = __float_as_uint(o[e] * inv);
+    } else {
+      uint16_t* out16 = reinterpret_cast<uint16_t*>(outw);
+#pragma unroll
+      for (int e = 0; e < PER; ++e) out16[lane * PER + e] = (uint16_t)f32_to_bf16_rne(o[e] * inv);
+    }
+  };
+  // count <= N records, all loaded at once (past the last: the last again, weighted 0)
+  auto few = [&](auto n_tag) {
+    constexpr int N = decltype(n_tag)::value;
+    float mv[N], lv[N], v[N][PER];
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const float* rec = base + (int64_t)min(j, count - 1) * STRIDE;
+      mv[j] = rec[D];
+      lv[j] = rec[D + 1];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) v[j][e] = rec[lane * PER + e];
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < N; ++j) mx = j < count ? fmaxf(mx, mv[j]) : mx;
+    float l = 0.f, o[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) o[e] = 0.f;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const float w = j < count && mv[j] != -INFINITY ? exp2f(mv[j] - mx) : 0.f;
+      l += w * lv[j];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) o[e] = fmaf(w, v[j][e], o[e]);
+    }
+    store(o, 1.f / l);
+  };
+  if (count <= 2) return few(std::integral_constant<int, 2>{});
+  if (count <= 4) return few(std::integral_constant<int, 4>{});
+  if (count <= 8) return few(std::integral_constant<int, 8>{});
   float mm = -INFINITY;
   for (int32_t i0 = 0; i0 < count; i0 += kWave) {
     const int32_t i = i0 + lane;
@@ -533,15 +578,7 @@ __device__ __forceinline__ void merge_row(const float* base, int32_t count, uint
   }
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) l += __shfl_xor(l, off, kWave);
-  const float inv = 1.f / l;
-  if constexpr (T::kBytes == 4) {
-#pragma unroll
-    for (int e = 0; e < PER; ++e) outw[lane * PER + e] = __float_as_uint(o[e] * inv);
-  } else {
-    uint16_t* out16 = reinterpret_cast<uint16_t*>(outw);
-#pragma unroll
-    for (int e = 0; e < PER; ++e) out16[lane * PER + e] = (uint16_t)f32_to_bf16_rne(o[e] * inv);
-  }
+  store(o, 1.f / l);
 }
 
 #ifndef BATON_ATTN_WAVES_PER_EU
