@@ -321,8 +321,8 @@ void plan_items(baton_cache* c, baton::MetaArgs& m, int64_t& items, int64_t& mul
   for (int32_t b = 0; b < c->d.batch; ++b) {
     m.lens[b] = c->plen[b] > 0 ? -1 : c->lens[b];   // a row prefilled this step has no item
     // The row's first hole, past any that ends at or before its first column:
-    // meta_kernel plans the run after a hole once for every row from whose
-    // first hole on it lies, so the row must hold every hole from there.
+    // meta_kernel counts every run after a row's first hole as the row's own
+    // (it plans each such run once, for all the rows that hold it).
     int32_t f = first_hole(c, b);
     const int64_t c0 = m.L - std::max(m.lens[b], 0);
     while (f < m.holes.n && m.holes.col[f][1] <= c0) ++f;
