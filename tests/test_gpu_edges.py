@@ -177,3 +177,16 @@ def test_dense_interop_with_stock_masked_attention():
         assert torch.max(torch.abs(got - ref[:, :, 0, :])).item() <= 2e-2
         cache.advance()
     cache.close()
+
+
+@pytest.mark.parametrize("dtype,Hq,Hkv,D", [("bf16", 2, 2, 128), ("bf16", 8, 2, 128), ("f32", 2, 1, 64)])
+def test_merge_record_counts(dtype, Hq, Hkv, D):
+    """Rows of 2, 3, 4, 5, 8 and 9 split-K records at the split of 64 (a row
+    of n cached tokens has ceil((n + 1) / 64) items), one more each a step
+    later: the merge's paths for up to two, four and eight records and for
+    more, each at its boundary (VALU and matrix-core attention, bf16 and
+    fp32)."""
+    lens = [127, 128, 191, 255, 256, 319, 511, 512, 575]
+    w = scripted("merge", dtype, 1, len(lens), Hq, Hkv, D, lens, [([], [], []), ([], [], [])])
+    err = parity.run(w, split=64)
+    print(f"[merge records] {dtype} {Hq}/{Hkv}x{D}: max abs error {err:.3g}", flush=True)
